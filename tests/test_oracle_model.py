@@ -1,0 +1,149 @@
+"""Pins for the oracle decoder (CPU): closed forms, invariants, the tree example."""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+from synth import ModelDims, Workload, make_weights
+from oracle.model import Decoder, rope, RMS_EPS
+from oracle.tree import ancestor_mask, flatten
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _tiny_workload(**kw):
+    base = dict(name="t", dtype="fp32",
+                target=ModelDims(2, 32, 4, 64, 4 * 6 + 10, 10),
+                draft=ModelDims(1, 16, 2, 32, 4 * 6 + 10, 10),
+                n_items=200, batch=1, hist_items=3, prompt_len=2, hist_dist="uniform",
+                K=3, N=4, gamma=4, codebook=6)
+    base.update(kw)
+    return Workload(**base)
+
+
+def _zeros_like_weights(w):
+    return {k: (np.zeros_like(v) if k.startswith("l") and not k.endswith("norm") else v.copy())
+            for k, v in w.items()}
+
+
+def _rms(x):
+    return x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + RMS_EPS)
+
+
+def test_zero_blocks_reduce_to_embedding_readout():
+    w = _tiny_workload()
+    W = _zeros_like_weights(make_weights(w, "target"))
+    dec = Decoder(w.target, W, "fp32")
+    toks = np.array([[3, 17, 25, 11]])
+    logits, _ = dec.forward(toks, np.arange(4))
+    E = W["tok_emb"].astype(np.float64)
+    want = _rms(E[toks[0]]) @ W["lm_head_item"].astype(np.float64).T
+    np.testing.assert_allclose(logits[0], want, rtol=0, atol=1e-12)
+
+
+def test_zero_query_gives_uniform_causal_average():
+    # Wq = 0 -> every visible key scores 0 -> attention output is the mean of the
+    # visible values; with Wv = Wo = I and no FFN: x_i + mean_{j<=i} n(x_j).
+    w = _tiny_workload(target=ModelDims(1, 32, 4, 64, 34, 10))
+    W = _zeros_like_weights(make_weights(w, "target"))
+    W["l0.wv"] = np.eye(32, dtype=np.float32)
+    W["l0.wo"] = np.eye(32, dtype=np.float32)
+    W["l0.wk"] = np.random.default_rng(3).standard_normal((32, 32)).astype(np.float32)
+    dec = Decoder(w.target, W, "fp32")
+    toks = np.array([[1, 5, 9, 13, 2]])
+    logits, _ = dec.forward(toks, np.arange(5))
+    x = W["tok_emb"].astype(np.float64)[toks[0]]
+    n = _rms(x)
+    h = x + np.cumsum(n, axis=0) / np.arange(1, 6)[:, None]
+    want = _rms(h) @ W["lm_head_item"].astype(np.float64).T
+    np.testing.assert_allclose(logits[0], want, rtol=0, atol=1e-12)
+
+
+def test_rope_is_complex_rotation_of_half_pairs():
+    rng = np.random.default_rng(0)
+    dh = 16
+    x = rng.standard_normal((3, dh))
+    pos = np.array([0, 7, 1000])
+    z = x[:, :8] + 1j * x[:, 8:]
+    theta = np.array([10000.0 ** (-(2.0 * i) / dh) for i in range(8)])
+    zr = z * np.exp(1j * pos[:, None] * theta[None, :])
+    want = np.concatenate([zr.real, zr.imag], axis=1)
+    np.testing.assert_allclose(rope(x, pos), want, rtol=0, atol=1e-12)
+    # q.k after rotation depends only on the position difference
+    q, k = rng.standard_normal(dh), rng.standard_normal(dh)
+    a = rope(q[None], np.array([5])) @ rope(k[None], np.array([2])).T
+    b = rope(q[None], np.array([105])) @ rope(k[None], np.array([102])).T
+    assert abs(a - b).max() < 1e-12
+
+
+def test_swiglu_hand_value():
+    # d=2, one head, f=1, attention off; gate weight 2, up weight 3, down 0.5 on
+    # the first coordinate: x1' = 1 + 0.5 * silu(2) * 3 with silu(2) = 2/(1+e^-2).
+    dims = ModelDims(1, 2, 1, 1, 2, 0)
+    W = {"tok_emb": np.array([[1.0, 1.0], [0.0, 0.0]], np.float32),
+         "l0.wq": np.zeros((2, 2), np.float32), "l0.wk": np.zeros((2, 2), np.float32),
+         "l0.wv": np.zeros((2, 2), np.float32), "l0.wo": np.zeros((2, 2), np.float32),
+         "l0.w_gate": np.array([[2.0, 0.0]], np.float32), "l0.w_up": np.array([[3.0, 0.0]], np.float32),
+         "l0.w_down": np.array([[0.5], [0.0]], np.float32),
+         "l0.attn_norm": np.ones(2, np.float32), "l0.ffn_norm": np.ones(2, np.float32),
+         "final_norm": np.ones(2, np.float32), "lm_head_item": np.eye(2, dtype=np.float32)}
+    dec = Decoder(dims, W, "fp32")
+    logits, _ = dec.forward(np.array([[0]]), np.arange(1))
+    s = 1.0 / math.sqrt(1.0 + RMS_EPS)          # n([1, 1])
+    x1 = 1.0 + 0.5 * (2 * s / (1 + math.exp(-2 * s))) * (3 * s)
+    want = np.array([x1, 1.0]) / math.sqrt((x1 * x1 + 1.0) / 2 + RMS_EPS)
+    np.testing.assert_allclose(logits[0, 0], want, rtol=0, atol=1e-12)
+    # hand value of the FFN output at eps -> 0: 0.5 * 3 * 2 / (1 + e^-2)
+    assert abs(0.5 * 3 * 2 / (1 + math.exp(-2)) - 2.642391233933647) < 1e-12
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_causality_and_prefix_cache(dtype):
+    w = _tiny_workload(dtype=dtype)
+    dec = Decoder(w.target, make_weights(w, "target"), dtype)
+    rng = np.random.default_rng(5)
+    seq = rng.integers(0, w.target.vocab, size=9)
+    full, _ = dec.forward(seq[None], np.arange(9))
+    for i in (0, 3, 8):
+        part, _ = dec.forward(seq[None, : i + 1], np.arange(i + 1))
+        np.testing.assert_allclose(part[0, -1], full[0, i], rtol=0, atol=1e-12)
+    cache = dec.prefill(seq[:6])
+    got = dec.path_logits(cache, [tuple(seq[6:])])
+    np.testing.assert_allclose(got[0], full[0, 8], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(dec.path_logits(cache, [()])[0], full[0, 5], rtol=0, atol=1e-12)
+
+
+def test_tree_example_flattening():
+    with open(os.path.join(GOLDEN, "tree_example.json")) as f:
+        g = json.load(f)
+    beams = [b for step in g["beams_by_step"] for b in step]
+    nodes, parent, depth = flatten(beams)
+    assert [n[-1] for n in nodes] == g["flattened"]
+    m = ancestor_mask(parent)
+    for i, n in enumerate(nodes):
+        want = set(g["rows"][" ".join(n)])
+        got = {nodes[j][-1] for j in range(len(nodes)) if m[i, j]}
+        assert got == want
+
+
+def test_tree_forward_equals_per_path_forward():
+    # Flattened tree with the ancestor mask and depth positions (P + depth - 1)
+    # gives the same logits as one causal forward per path.
+    w = _tiny_workload()
+    dec = Decoder(w.target, make_weights(w, "target"), "fp32")
+    rng = np.random.default_rng(2)
+    prefix = rng.integers(0, w.target.vocab, size=7)
+    cache = dec.prefill(prefix)
+    paths = [(11,), (12,), (11, 20), (12, 21), (11, 20, 30), (11, 20, 31), (13,), (13, 22)]
+    nodes, parent, depth = flatten(paths)
+    toks = np.array([[n[-1] for n in nodes]])
+    pos = len(prefix) + np.array(depth) - 1
+    tree, _ = dec.forward(toks, pos, prefix=cache, mask=ancestor_mask(parent).astype(bool))
+    per = dec.path_logits(cache, nodes)
+    np.testing.assert_allclose(tree[0], per, rtol=0, atol=1e-12)
+    # flattened positions 0..Lf-1 would be a different (wrong) model
+    bad, _ = dec.forward(toks, len(prefix) + np.arange(len(nodes)), prefix=cache,
+                         mask=ancestor_mask(parent).astype(bool))
+    assert np.abs(bad[0] - per).max() > 1e-6
