@@ -1,0 +1,197 @@
+/*
+ * atspeed.h — C ABI of the MI355X (gfx950) speculative-decoding verify path of
+ * AtSpeed (arXiv 2410.05165): top-K generative recommendation with a draft model
+ * and a target LLM.
+ *
+ * Problem statement (task formulation, Sec. 2): given a user's history x, the
+ * target model returns the top-K item identifiers (L codebook tokens each) by
+ * constrained beam search.  Speculative decoding drafts gamma beam-search levels
+ * of width N with a small model (Eq. 1) and verifies all of them with ONE target
+ * forward over the tree of drafted beams (tree-based attention, Sec. 3.3),
+ * followed by strict top-K verification (Algorithm 1) or relaxed sampling
+ * verification (Sec. 3.2, Algorithm 2).
+ *
+ * Conventions shared by every call
+ *   - "dev" pointers are device (HBM) pointers, "host" pointers are host memory.
+ *   - The caller owns every buffer (weights, workspace, inputs, outputs); they
+ *     must outlive the context.  The library allocates no device memory.
+ *   - All device work is enqueued on config.stream (a hipStream_t; NULL = the
+ *     default stream).  Calls that return host-visible results synchronise that
+ *     stream before returning; this is stated per call.
+ *   - Every call returns a status; no C++ exception crosses the ABI.  Argument
+ *     errors are detected on the host before any launch and leave the context
+ *     unchanged.  The message of the last error of the calling thread is
+ *     returned by atspeed_last_error().
+ *   - Token ids: item code c at item level l (0-based) is token
+ *     item_base + codebook*l + c.  Items are fixed-length: L tokens.
+ *   - A context is bound to one stream and is not thread-safe.
+ */
+#ifndef ATSPEED_H
+#define ATSPEED_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ATSPEED_API __attribute__((visibility("default")))
+
+typedef enum {
+  ATSPEED_OK = 0,
+  ATSPEED_E_INVALID = 1,    /* bad argument (null pointer, value out of range, invalid tree)   */
+  ATSPEED_E_SHAPE = 2,      /* shapes inconsistent with the configuration                      */
+  ATSPEED_E_WORKSPACE = 3,  /* workspace too small or misaligned                               */
+  ATSPEED_E_DEVICE = 4,     /* a HIP call failed (message holds the HIP error string)          */
+  ATSPEED_E_STATE = 5       /* call out of order (e.g. verify before prefill)                  */
+} atspeed_status;
+
+typedef enum {
+  ATSPEED_STRICT = 0,         /* Algorithm 1: accept level j iff TopK(p_j) is a subset of the drafted level */
+  ATSPEED_RELAXED_EXACT = 1,  /* Sec. 3.2 with K i.i.d. slots per level (the with-replacement reading)       */
+  ATSPEED_RELAXED_PAPER = 2   /* Algorithm 2 reading: N distinct drafts, K accepted kept, residual resample  */
+} atspeed_mode;
+
+typedef enum { ATSPEED_FP32 = 0, ATSPEED_BF16 = 1 } atspeed_dtype;
+
+/* LLaMA-style decoder dimensions.  d_model % n_heads == 0, d_head in {32, 64, 128},
+ * d_model and d_ffn multiples of 64. */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, d_ffn, vocab, item_base;
+} atspeed_model_dims;
+
+typedef struct {
+  atspeed_model_dims target, draft;
+  int32_t L;            /* item identifier length (tokens per item), 1..4          */
+  int32_t codebook;     /* codes per level, <= 256                                  */
+  int32_t K;            /* target beam size (recommended items)                     */
+  int32_t N;            /* draft beam size, N >= K                                  */
+  int32_t gamma;        /* drafted levels per speculative step, >= 1                */
+  int32_t max_batch;    /* users per call                                           */
+  int32_t max_prefix;   /* prefix (history) tokens per user                         */
+  int32_t mode;         /* atspeed_mode                                             */
+  float temperature;    /* sampling temperature of the relaxed modes (> 0)          */
+  uint64_t seed;        /* Philox key of the relaxed modes                          */
+  int32_t dtype;        /* atspeed_dtype of weights, activations and KV caches      */
+  void* stream;         /* hipStream_t                                              */
+} atspeed_config;
+
+/* Model weights (device, caller-owned).  Matrices are row-major [out, in] in the
+ * configured dtype (bf16 or fp32); norm gains are fp32 [d_model].
+ *   tok_emb       [vocab, d_model]
+ *   layers        host array of n_layers*9 device pointers, per layer in order:
+ *                 attn_norm, wq, wk, wv, wo ([d,d]), ffn_norm, w_gate, w_up ([f,d]), w_down ([d,f])
+ *   final_norm    [d_model]
+ *   lm_head_item  [L*codebook, d_model]: the output-head rows of the item tokens
+ *                 (item_base .. item_base + L*codebook - 1); no other row is read. */
+typedef struct {
+  const void* tok_emb;
+  const void* const* layers;
+  const float* final_norm;
+  const void* lm_head_item;
+} atspeed_weights;
+
+/* Item catalog (host): n_items distinct identifiers, codes[i*L + l] in [0, codebook). */
+typedef struct {
+  int32_t n_items;
+  const int32_t* codes;
+} atspeed_catalog;
+
+/* Tree of drafted beams (device, structure of arrays, one row of max_nodes slots
+ * per user).  Nodes of a user are level-ordered (depth never decreases with the
+ * slot index); a node's parent has a smaller slot; parent = -1 for depth-1 nodes.
+ * A verify tree must contain the paths of the current target beams Y_t (depths
+ * 1..t) and the drafted levels t+1..t+J (tree-based attention, Sec. 3.3; the
+ * flattened sequence of its appendix is the slot order). */
+typedef struct {
+  int32_t max_nodes;
+  int32_t* n_nodes;   /* [B]             */
+  int32_t* token;     /* [B, max_nodes]  item-token ids                          */
+  int32_t* parent;    /* [B, max_nodes]  parent slot or -1                       */
+  int32_t* depth;     /* [B, max_nodes]  1..L                                    */
+  float* q_score;     /* [B, max_nodes]  draft cumulative log-prob (relaxed modes) */
+} atspeed_tree;
+
+/* Per-call statistics (host).  Arrays are caller-provided; NULL skips them. */
+typedef struct {
+  int32_t n_steps;     /* speculative steps run                                  */
+  int32_t* accepted;   /* [L, max_batch]: accepted levels per step, -1 once done */
+  int32_t* t_after;    /* [L, max_batch]: item level reached after each step     */
+  double ms_prefill, ms_draft, ms_verify;  /* stream time per stage (HIP events) */
+} atspeed_stats;
+
+typedef struct atspeed_ctx atspeed_ctx;
+
+/* Bytes of device workspace a context needs for this configuration and catalog. */
+ATSPEED_API atspeed_status atspeed_workspace_bytes(const atspeed_config* cfg, const atspeed_catalog* cat, size_t* bytes);
+
+/* Create a context.  Builds the item trie on the host from the catalog and copies
+ * it, the rotary tables and the zeroed state into the workspace (256-byte aligned,
+ * >= atspeed_workspace_bytes).  Synchronises the stream.  draft may be NULL, then
+ * atspeed_draft and atspeed_decode_topk return ATSPEED_E_STATE. */
+ATSPEED_API atspeed_status atspeed_create(const atspeed_config* cfg, const atspeed_weights* target,
+                              const atspeed_weights* draft, const atspeed_catalog* cat,
+                              void* workspace_dev, size_t ws_bytes, atspeed_ctx** out);
+ATSPEED_API void atspeed_destroy(atspeed_ctx* ctx);
+ATSPEED_API const char* atspeed_last_error(void);
+
+/* Prefill: one causal forward of the target (and draft) over B prefixes of P
+ * tokens each (prefix_dev [B, P] int32, device), filling the prefix KV caches and
+ * the root log-probs (logits at the last prefix position).  Resets every user to
+ * item level t = 0 with the empty beam.  root_logits_dev (nullable): [B, L*codebook]
+ * fp32 item logits of the target at the last prefix position.  Asynchronous. */
+ATSPEED_API atspeed_status atspeed_prefill(atspeed_ctx* ctx, int32_t B, int32_t P, const int32_t* prefix_dev,
+                               float* root_logits_dev);
+
+/* Draft (Eq. 1): from each user's current target beams Y_t, run J = min(gamma, L-t)
+ * levels of draft beam search of width N over trie-valid codes and write the
+ * verify tree (Y_t paths + drafted levels) into the context's tree.  Users with
+ * t = L get an empty tree.  Asynchronous. */
+ATSPEED_API atspeed_status atspeed_draft(atspeed_ctx* ctx);
+
+/* The context's own tree (device pointers inside the workspace).  A caller may
+ * overwrite its contents to verify a tree of its own. */
+ATSPEED_API atspeed_status atspeed_get_tree(atspeed_ctx* ctx, atspeed_tree* out);
+
+/* Verify: ONE target forward over every tree node of depth < L (tree attention on
+ * the prefix KV cache plus each node's ancestors), log-softmax over the item
+ * tokens, cumulative log-probs, trie-constrained TopK and acceptance (strict:
+ * Algorithm 1; relaxed: Algorithm 2 per the configured mode).  Updates the state
+ * (t, beams, scores).  accepted_dev / t_after_dev: [B] int32 (device, nullable).
+ * logits_dev (nullable): [B, max_nodes, L*codebook] fp32 target item logits of
+ * every forwarded node by slot.  Synchronises the stream (reads back one status
+ * word): ATSPEED_E_INVALID if the tree is malformed (state then unchanged). */
+ATSPEED_API atspeed_status atspeed_verify(atspeed_ctx* ctx, int32_t* accepted_dev, int32_t* t_after_dev,
+                              float* logits_dev);
+
+/* Forward only: target item logits of every tree node of depth < L (the first
+ * part of atspeed_verify), written to logits_dev [B, max_nodes, L*codebook].
+ * Synchronises the stream. */
+ATSPEED_API atspeed_status atspeed_tree_logits(atspeed_ctx* ctx, float* logits_dev);
+
+/* Accept only: the selection and acceptance part of atspeed_verify on caller
+ * logits (logits_dev [B, max_nodes, L*codebook] fp32 by slot; root logits
+ * [B, L*codebook] fp32).  Updates the state like atspeed_verify. */
+ATSPEED_API atspeed_status atspeed_accept(atspeed_ctx* ctx, const float* logits_dev, const float* root_logits_dev,
+                              int32_t* accepted_dev, int32_t* t_after_dev);
+
+/* Whole decode: prefill, then draft/verify steps until every user holds L-token
+ * items.  items_dev [B, K, L] int32 codes (best first), scores_dev [B, K] fp32
+ * cumulative target log-probs, n_items_dev [B] number of valid lists (< K only
+ * when the catalog has fewer candidates).  Synchronises once per step. */
+ATSPEED_API atspeed_status atspeed_decode_topk(atspeed_ctx* ctx, int32_t B, int32_t P, const int32_t* prefix_dev,
+                                   int32_t* items_dev, float* scores_dev, int32_t* n_items_dev,
+                                   atspeed_stats* stats_host);
+
+/* State access (host arrays; synchronise the stream).  t [B]; nbeams [B];
+ * paths [B, K, L] codes (entries past depth t undefined); scores [B, K] fp32. */
+ATSPEED_API atspeed_status atspeed_get_state(atspeed_ctx* ctx, int32_t B, int32_t* t, int32_t* nbeams,
+                                 int32_t* paths, float* scores);
+ATSPEED_API atspeed_status atspeed_set_state(atspeed_ctx* ctx, int32_t B, const int32_t* t, const int32_t* nbeams,
+                                 const int32_t* paths, const float* scores);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ATSPEED_H */

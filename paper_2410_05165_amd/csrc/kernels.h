@@ -1,0 +1,48 @@
+// Host-side launchers of the device kernels (one translation unit per family).
+#pragma once
+#include <hip/hip_runtime.h>
+#include "common.h"
+
+namespace atspeed {
+
+enum GemmKind { GEMM_STORE = 0, GEMM_RESID = 1, GEMM_GU = 2, GEMM_QKV = 3 };
+
+struct GemmCall {
+  int kind;
+  bool bf16;
+  const void* A; int lda;
+  int Mmax; const int* Mdev;
+  int N, K;
+  const void* w0; const void* w1; const void* w2;
+  int split;                 // QKV: d_model; GU: d_ffn
+  float* out; int ldo;       // STORE / RESID
+  void* hout;                // GU output [M, f]
+  void* q; void* kdst; void* vdst;
+  const float* cosT; const float* sinT;
+  Rows rows;
+  int kv_mode, Pmax, d, dh, H;
+  float* scratch;            // fp32 path: [Mmax, N] product
+};
+hipError_t gemm(const GemmCall& g, hipStream_t st);
+
+// Attention of every row over its visible prefix-cache keys and tree keys.
+struct AttnCall {
+  bool bf16;
+  const void* q;        // [M, d]
+  const void* pk; const void* pv;   // prefix cache of this layer [B][H][Pmax][dh]
+  const void* tk; const void* tv;   // tree KV of this layer [slot][d] (may be null)
+  void* out;            // [M, d]
+  Rows rows;
+  int Mmax, B, Tq;      // Tq: max rows per user (grid bound)
+  int H, dh, d, Pmax;
+};
+hipError_t attention(const AttnCall& a, hipStream_t st);
+
+// Misc
+hipError_t embed(bool bf16, const void* emb, const Rows& rows, int Mmax, int d, float* x, hipStream_t st);
+hipError_t rmsnorm(bool bf16, const float* x, const int* Mdev, int Mmax, int d, const float* g, void* out,
+                   const int* row_index, hipStream_t st);
+hipError_t log_softmax_rows(const float* logits, const int* Mdev, int Mmax, int n, const int* dst_index,
+                            float* lp, float* logits_copy, hipStream_t st);
+
+}  // namespace atspeed

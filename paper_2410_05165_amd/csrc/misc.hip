@@ -1,0 +1,100 @@
+// Row-wise kernels of the forward: embedding gather, RMSNorm, item log-softmax.
+#include "common.h"
+#include "kernels.h"
+
+namespace atspeed {
+
+template <class T>
+__global__ void embed_kernel(const T* __restrict__ emb, const int* __restrict__ tok, const int* __restrict__ Mdev,
+                             int d, float* __restrict__ x) {
+  const int M = *Mdev;
+  const size_t total = (size_t)M * d;
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < total; i += (size_t)gridDim.x * blockDim.x) {
+    const size_t r = i / d, c = i % d;
+    x[i] = St<T>::ld(emb + (size_t)tok[r] * d + c);
+  }
+}
+
+hipError_t embed(bool bf16, const void* emb, const Rows& rows, int Mmax, int d, float* x, hipStream_t st) {
+  int blocks = (int)std::min<size_t>(4096, ((size_t)Mmax * d + 255) / 256);
+  if (blocks < 1) blocks = 1;
+  if (bf16) hipLaunchKernelGGL(embed_kernel<bf16_t>, dim3(blocks), dim3(256), 0, st, (const bf16_t*)emb, rows.token, rows.M, d, x);
+  else hipLaunchKernelGGL(embed_kernel<float>, dim3(blocks), dim3(256), 0, st, (const float*)emb, rows.token, rows.M, d, x);
+  return hipGetLastError();
+}
+
+__device__ __forceinline__ float block_sum256(float v, float* red) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  return red[0] + red[1] + red[2] + red[3];
+}
+
+__device__ __forceinline__ float block_max256(float v, float* red) {
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  return fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+}
+
+// out[r] = g * x[src] / sqrt(mean(x[src]^2) + eps), src = row_index ? row_index[r] : r.
+template <class T>
+__global__ void __launch_bounds__(256)
+rmsnorm_kernel(const float* __restrict__ x, const int* __restrict__ Mdev, int d, const float* __restrict__ g,
+               T* __restrict__ out, const int* __restrict__ row_index) {
+  __shared__ float red[4];
+  const int M = *Mdev;
+  for (int r = blockIdx.x; r < M; r += gridDim.x) {
+    const int src = row_index ? row_index[r] : r;
+    const float* xr = x + (size_t)src * d;
+    float ss = 0.f;
+    for (int c = threadIdx.x; c < d; c += 256) ss += xr[c] * xr[c];
+    ss = block_sum256(ss, red);
+    const float inv = rsqrtf(ss / (float)d + 1e-6f);
+    for (int c = threadIdx.x; c < d; c += 256) St<T>::st(out + (size_t)r * d + c, xr[c] * inv * g[c]);
+  }
+}
+
+hipError_t rmsnorm(bool bf16, const float* x, const int* Mdev, int Mmax, int d, const float* g, void* out,
+                   const int* row_index, hipStream_t st) {
+  int blocks = std::max(1, std::min(Mmax, 8192));
+  if (bf16) hipLaunchKernelGGL(rmsnorm_kernel<bf16_t>, dim3(blocks), dim3(256), 0, st, x, Mdev, d, g, (bf16_t*)out, row_index);
+  else hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(blocks), dim3(256), 0, st, x, Mdev, d, g, (float*)out, row_index);
+  return hipGetLastError();
+}
+
+// lp[dst[r]] = z[r] - logsumexp(z[r]) over the n item-token columns (fp32).
+__global__ void __launch_bounds__(256)
+log_softmax_kernel(const float* __restrict__ z, const int* __restrict__ Mdev, int n, const int* __restrict__ dst,
+                   float* __restrict__ lp, float* __restrict__ zcopy) {
+  __shared__ float red[4];
+  const int M = *Mdev;
+  for (int r = blockIdx.x; r < M; r += gridDim.x) {
+    const float* zr = z + (size_t)r * n;
+    float mx = -INFINITY;
+    for (int c = threadIdx.x; c < n; c += 256) mx = fmaxf(mx, zr[c]);
+    mx = block_max256(mx, red);
+    float s = 0.f;
+    for (int c = threadIdx.x; c < n; c += 256) s += expf(zr[c] - mx);
+    s = block_sum256(s, red);
+    const float lse = mx + logf(s);
+    const size_t o = (size_t)(dst ? dst[r] : r) * n;
+    for (int c = threadIdx.x; c < n; c += 256) {
+      lp[o + c] = zr[c] - lse;
+      if (zcopy) zcopy[o + c] = zr[c];
+    }
+  }
+}
+
+hipError_t log_softmax_rows(const float* logits, const int* Mdev, int Mmax, int n, const int* dst_index,
+                            float* lp, float* logits_copy, hipStream_t st) {
+  int blocks = std::max(1, std::min(Mmax, 8192));
+  hipLaunchKernelGGL(log_softmax_kernel, dim3(blocks), dim3(256), 0, st, logits, Mdev, n, dst_index, lp, logits_copy);
+  return hipGetLastError();
+}
+
+}  // namespace atspeed

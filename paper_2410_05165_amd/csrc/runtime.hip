@@ -1,0 +1,689 @@
+// Host runtime behind include/atspeed.h: workspace layout, item trie, the
+// decoder forward over planned rows, and the draft / verify / decode calls.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/atspeed.h"
+#include "common.h"
+#include "kernels.h"
+#include "select.h"
+
+using namespace atspeed;
+
+namespace {
+
+thread_local std::string g_err;
+
+atspeed_status fail(atspeed_status s, const std::string& msg) {
+  g_err = msg;
+  return s;
+}
+
+#define HIP_TRY(expr)                                                                      \
+  do {                                                                                     \
+    hipError_t _e = (expr);                                                                \
+    if (_e != hipSuccess) return fail(ATSPEED_E_DEVICE, std::string(#expr) + ": " + hipGetErrorString(_e)); \
+  } while (0)
+
+#define ST_TRY(expr)                        \
+  do {                                      \
+    atspeed_status _s = (expr);             \
+    if (_s != ATSPEED_OK) return _s;        \
+  } while (0)
+
+// Bump allocator over the caller's workspace (a null base only measures).
+struct Arena {
+  char* base;
+  size_t off = 0;
+  template <class T>
+  T* take(size_t n) {
+    off = (off + 255) & ~size_t(255);
+    T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += n * sizeof(T);
+    return p;
+  }
+};
+
+struct ModelRt {
+  atspeed_model_dims dims{};
+  bool present = false;
+  const void* emb = nullptr;
+  std::vector<const void*> layers;
+  const float* final_norm = nullptr;
+  const void* lm_head = nullptr;
+  void* pk = nullptr;            // prefix cache [layers][B][H][Pmax][dh]
+  void* pv = nullptr;
+  void* tk = nullptr;            // tree KV [tree_layers][B*Tmax][d]
+  void* tv = nullptr;
+  size_t tkv_layer_stride = 0;   // elements between layers (0: one shared buffer)
+  size_t pkv_layer_stride = 0;
+  float* cosT = nullptr;
+  float* sinT = nullptr;
+  float* lp = nullptr;           // [B*Tmax][nitem] log-probs by tree slot
+  float* root = nullptr;         // [B][nitem] log-probs at the last prefix position
+  int dh() const { return dims.d_model / dims.n_heads; }
+};
+
+struct HostTrie {
+  std::vector<int> code, first, cnt;
+  int child(int node, int c) const {
+    int lo = first[node], hi = lo + cnt[node] - 1;
+    while (lo <= hi) {
+      int mid = (lo + hi) / 2;
+      if (code[mid] == c) return mid;
+      if (code[mid] < c) lo = mid + 1; else hi = mid - 1;
+    }
+    return -1;
+  }
+};
+
+}  // namespace
+
+struct atspeed_ctx {
+  atspeed_config cfg{};
+  hipStream_t st = nullptr;
+  bool bf16 = false;
+  int Tmax = 0, Mmax = 0, nitem = 0, max_cand = 0, max_pos = 0;
+  ModelRt tgt, dft;
+  HostTrie htrie;
+  TrieDev trie{};
+  StateDev state{};
+  TreeDev tree{};
+  Rows rows{};
+  float* x = nullptr;
+  void* xn = nullptr;
+  void* q = nullptr;
+  void* ao = nullptr;
+  void* h = nullptr;
+  float* logits = nullptr;
+  float* scratch = nullptr;
+  int* lo = nullptr;
+  int* hi = nullptr;
+  int* lvl_lo = nullptr;
+  int* lvl_hi = nullptr;
+  int* row_last = nullptr;
+  int* Mb = nullptr;         // [1] = B (rows of the last-position head in prefill)
+  int* Mall = nullptr;       // [1] = B * Tmax (every tree slot)
+  int* err = nullptr;
+  int* acc_tmp = nullptr;
+  int* tafter_tmp = nullptr;
+  unsigned long long* keys = nullptr;
+  int B = 0, P = 0;
+  bool prefilled = false;
+  bool drafted = false;
+};
+
+namespace {
+
+size_t esize(const atspeed_ctx& c) { return c.bf16 ? 2 : 4; }
+
+atspeed_status check_dims(const atspeed_model_dims& m, const atspeed_config& c, const char* who) {
+  std::string w(who);
+  if (m.n_layers < 1 || m.d_model < 1 || m.n_heads < 1 || m.d_ffn < 1)
+    return fail(ATSPEED_E_INVALID, w + ": non-positive dimension");
+  if (m.d_model % m.n_heads) return fail(ATSPEED_E_SHAPE, w + ": d_model % n_heads != 0");
+  int dh = m.d_model / m.n_heads;
+  if (c.dtype == ATSPEED_BF16) {
+    if (dh != 64 && dh != 128) return fail(ATSPEED_E_SHAPE, w + ": bf16 needs d_head 64 or 128");
+    if (m.d_model % 256 || m.d_ffn % 128) return fail(ATSPEED_E_SHAPE, w + ": bf16 needs d_model % 256 == 0 and d_ffn % 128 == 0");
+  } else {
+    if (dh != 32 && dh != 64 && dh != 128) return fail(ATSPEED_E_SHAPE, w + ": d_head must be 32, 64 or 128");
+    if (m.d_model % 16 || m.d_ffn % 16) return fail(ATSPEED_E_SHAPE, w + ": d_model, d_ffn must be multiples of 16");
+  }
+  if (m.item_base < 0 || m.vocab < m.item_base + c.L * c.codebook)
+    return fail(ATSPEED_E_SHAPE, w + ": vocab must hold item_base + L*codebook tokens");
+  return ATSPEED_OK;
+}
+
+atspeed_status check_config(const atspeed_config* cfg) {
+  if (!cfg) return fail(ATSPEED_E_INVALID, "config is null");
+  const atspeed_config& c = *cfg;
+  if (c.L < 1 || c.L > 4) return fail(ATSPEED_E_INVALID, "L must be 1..4");
+  if (c.codebook < 1 || c.codebook > 256) return fail(ATSPEED_E_INVALID, "codebook must be 1..256");
+  if (c.K < 1 || c.K > kMaxSel) return fail(ATSPEED_E_INVALID, "K must be 1..128");
+  if (c.N < c.K || c.N > kMaxSel) return fail(ATSPEED_E_INVALID, "N must be K..128");
+  if (c.gamma < 1) return fail(ATSPEED_E_INVALID, "gamma must be >= 1");
+  if (c.max_batch < 1 || c.max_batch > 1024) return fail(ATSPEED_E_INVALID, "max_batch must be 1..1024");
+  if (c.max_prefix < 1) return fail(ATSPEED_E_INVALID, "max_prefix must be >= 1");
+  if (c.dtype != ATSPEED_FP32 && c.dtype != ATSPEED_BF16) return fail(ATSPEED_E_INVALID, "dtype");
+  if (c.mode != ATSPEED_STRICT) return fail(ATSPEED_E_INVALID, "only strict verification is built in this library");
+  ST_TRY(check_dims(c.target, c, "target"));
+  if (c.draft.n_layers > 0) {
+    ST_TRY(check_dims(c.draft, c, "draft"));
+    if (c.draft.item_base != c.target.item_base) return fail(ATSPEED_E_SHAPE, "draft and target item_base differ");
+  }
+  return ATSPEED_OK;
+}
+
+atspeed_status build_trie(const atspeed_config& c, const atspeed_catalog* cat, HostTrie& t) {
+  if (!cat || !cat->codes || cat->n_items < 1) return fail(ATSPEED_E_INVALID, "catalog is empty or null");
+  if (cat->n_items < c.K) return fail(ATSPEED_E_INVALID, "catalog holds fewer than K items");
+  std::vector<uint32_t> keys(cat->n_items);
+  for (int i = 0; i < cat->n_items; ++i) {
+    uint32_t k = 0;
+    for (int l = 0; l < c.L; ++l) {
+      int code = cat->codes[(size_t)i * c.L + l];
+      if (code < 0 || code >= c.codebook) return fail(ATSPEED_E_INVALID, "catalog code out of range");
+      k |= (uint32_t)code << (8 * (3 - l));
+    }
+    keys[i] = k;
+  }
+  std::sort(keys.begin(), keys.end());
+  if (std::adjacent_find(keys.begin(), keys.end()) != keys.end()) return fail(ATSPEED_E_INVALID, "catalog has duplicate items");
+  // level-ordered unique prefixes; node 0 = root
+  std::vector<std::vector<uint32_t>> lv(c.L + 1);
+  lv[0] = {0u};
+  for (int l = 1; l <= c.L; ++l) {
+    uint32_t mask = l == 4 ? 0xFFFFFFFFu : ~(0xFFFFFFFFu >> (8 * l));
+    for (uint32_t k : keys) {
+      uint32_t p = k & mask;
+      if (lv[l].empty() || lv[l].back() != p) lv[l].push_back(p);
+    }
+  }
+  std::vector<int> off(c.L + 2, 0);
+  for (int l = 0; l <= c.L; ++l) off[l + 1] = off[l] + (int)lv[l].size();
+  const int n = off[c.L + 1];
+  t.code.assign(n, 0);
+  t.first.assign(n, 0);
+  t.cnt.assign(n, 0);
+  for (int l = 1; l <= c.L; ++l) {
+    uint32_t pmask = l == 1 ? 0u : ~(0xFFFFFFFFu >> (8 * (l - 1)));
+    size_t pi = 0;
+    for (size_t i = 0; i < lv[l].size(); ++i) {
+      uint32_t p = lv[l][i];
+      while ((lv[l - 1][pi] & pmask) != (p & pmask)) ++pi;
+      int id = off[l] + (int)i, pid = off[l - 1] + (int)pi;
+      t.code[id] = (p >> (8 * (3 - (l - 1)))) & 0xFF;
+      if (t.cnt[pid] == 0) t.first[pid] = id;
+      t.cnt[pid]++;
+    }
+  }
+  return ATSPEED_OK;
+}
+
+// Lays out (base == null: measures) every device buffer of a context.
+void layout(atspeed_ctx& c, const atspeed_config& cfg, int trie_nodes, Arena& a) {
+  const int B = cfg.max_batch, P = cfg.max_prefix, L = cfg.L;
+  c.bf16 = cfg.dtype == ATSPEED_BF16;
+  c.nitem = L * cfg.codebook;
+  c.Tmax = cfg.K * (L - 1) + cfg.gamma * cfg.N;
+  c.Mmax = std::max(B * P, B * c.Tmax);
+  c.max_cand = cfg.N * cfg.codebook;
+  c.max_pos = P + L;
+  const size_t es = c.bf16 ? 2 : 4;
+  const int Tm = c.Tmax;
+  c.trie.code = a.take<int>(trie_nodes);
+  c.trie.first = a.take<int>(trie_nodes);
+  c.trie.cnt = a.take<int>(trie_nodes);
+  int dmax = cfg.target.d_model, fmax = cfg.target.d_ffn;
+  ModelRt* ms[2] = {&c.tgt, &c.dft};
+  const atspeed_model_dims* ds[2] = {&cfg.target, &cfg.draft};
+  for (int w = 0; w < 2; ++w) {
+    const atspeed_model_dims& m = *ds[w];
+    ModelRt& r = *ms[w];
+    r.dims = m;
+    if (m.n_layers <= 0) continue;
+    dmax = std::max(dmax, m.d_model);
+    fmax = std::max(fmax, m.d_ffn);
+    const size_t pkv = (size_t)m.n_layers * B * P * m.d_model;
+    r.pkv_layer_stride = (size_t)B * P * m.d_model;
+    r.pk = a.take<char>(pkv * es);
+    r.pv = a.take<char>(pkv * es);
+    const int tl = w == 0 ? 1 : m.n_layers;
+    r.tkv_layer_stride = w == 0 ? 0 : (size_t)B * Tm * m.d_model;
+    r.tk = a.take<char>((size_t)tl * B * Tm * m.d_model * es);
+    r.tv = a.take<char>((size_t)tl * B * Tm * m.d_model * es);
+    const int half = m.d_model / m.n_heads / 2;
+    r.cosT = a.take<float>((size_t)c.max_pos * half);
+    r.sinT = a.take<float>((size_t)c.max_pos * half);
+    r.lp = a.take<float>((size_t)B * Tm * c.nitem);
+    r.root = a.take<float>((size_t)B * c.nitem);
+  }
+  const size_t M = c.Mmax;
+  c.x = a.take<float>(M * dmax);
+  c.xn = a.take<char>(M * dmax * es);
+  c.q = a.take<char>(M * dmax * es);
+  c.ao = a.take<char>(M * dmax * es);
+  c.h = a.take<char>(M * fmax * es);
+  c.logits = a.take<float>(M * c.nitem);
+  c.scratch = c.bf16 ? nullptr : a.take<float>(M * std::max(3 * dmax, 2 * fmax));
+  c.rows.M = a.take<int>(1);
+  c.rows.user = a.take<int>(M);
+  c.rows.token = a.take<int>(M);
+  c.rows.pos = a.take<int>(M);
+  c.rows.slot = a.take<int>(M);
+  c.rows.nctx = a.take<int>(M);
+  c.rows.anc = a.take<int>(M * 4);
+  c.rows.nanc = a.take<int>(M);
+  c.rows.user_off = a.take<int>(B + 1);
+  const int K = cfg.K;
+  c.state.t = a.take<int>(B);
+  c.state.nb = a.take<int>(B);
+  c.state.path = a.take<uint32_t>((size_t)B * K);
+  c.state.trie = a.take<int>((size_t)B * K);
+  c.state.score = a.take<float>((size_t)B * K);
+  c.state.qscore = a.take<float>((size_t)B * K);
+  c.state.beam_slot = a.take<int>((size_t)B * K);
+  c.state.steps = a.take<int>(B);
+  c.state.npath = a.take<int>(B);
+  c.state.nfwd = a.take<int>(B);
+  c.state.K = K;
+  c.state.gamma = cfg.gamma;
+  c.tree.max_nodes = Tm;
+  c.tree.n_nodes = a.take<int>(B);
+  c.tree.token = a.take<int>((size_t)B * Tm);
+  c.tree.parent = a.take<int>((size_t)B * Tm);
+  c.tree.depth = a.take<int>((size_t)B * Tm);
+  c.tree.q_score = a.take<float>((size_t)B * Tm);
+  c.tree.tpath = a.take<uint32_t>((size_t)B * Tm);
+  c.tree.ttrie = a.take<int>((size_t)B * Tm);
+  c.lo = a.take<int>(B);
+  c.hi = a.take<int>(B);
+  c.lvl_lo = a.take<int>(B);
+  c.lvl_hi = a.take<int>(B);
+  c.row_last = a.take<int>(B);
+  c.Mb = a.take<int>(1);
+  c.Mall = a.take<int>(1);
+  c.err = a.take<int>(1);
+  c.acc_tmp = a.take<int>(B);
+  c.tafter_tmp = a.take<int>(B);
+  c.keys = a.take<unsigned long long>((size_t)B * c.max_cand);
+}
+
+atspeed_status bind_weights(ModelRt& r, const atspeed_weights* w, const char* who) {
+  std::string s(who);
+  if (!w || !w->tok_emb || !w->layers || !w->final_norm || !w->lm_head_item)
+    return fail(ATSPEED_E_INVALID, s + " weights: null pointer");
+  r.emb = w->tok_emb;
+  r.final_norm = w->final_norm;
+  r.lm_head = w->lm_head_item;
+  r.layers.assign(w->layers, w->layers + (size_t)r.dims.n_layers * 9);
+  for (const void* p : r.layers)
+    if (!p) return fail(ATSPEED_E_INVALID, s + " weights: null layer pointer");
+  r.present = true;
+  return ATSPEED_OK;
+}
+
+atspeed_status upload_rope(atspeed_ctx& c, ModelRt& r) {
+  const int dh = r.dh(), half = dh / 2;
+  std::vector<float> cs((size_t)c.max_pos * half), sn((size_t)c.max_pos * half);
+  for (int p = 0; p < c.max_pos; ++p)
+    for (int i = 0; i < half; ++i) {
+      double ang = (double)p * std::pow(10000.0, -2.0 * i / dh);
+      cs[(size_t)p * half + i] = (float)std::cos(ang);
+      sn[(size_t)p * half + i] = (float)std::sin(ang);
+    }
+  HIP_TRY(hipMemcpyAsync(r.cosT, cs.data(), cs.size() * 4, hipMemcpyHostToDevice, c.st));
+  HIP_TRY(hipMemcpyAsync(r.sinT, sn.data(), sn.size() * 4, hipMemcpyHostToDevice, c.st));
+  HIP_TRY(hipStreamSynchronize(c.st));
+  return ATSPEED_OK;
+}
+
+// One decoder forward over the planned rows.  prefill: K/V into the prefix cache,
+// log-probs at each user's last position into r.root; else K/V into the tree
+// buffer and log-probs into r.lp by tree slot (logits copied to dbg if given).
+atspeed_status forward(atspeed_ctx& c, ModelRt& r, bool prefill, int Mmax, int Tq, float* dbg) {
+  const atspeed_model_dims& m = r.dims;
+  const int d = m.d_model, f = m.d_ffn, H = m.n_heads, dh = r.dh();
+  const int B = c.B, P = c.P;
+  const size_t es = esize(c);
+  hipStream_t st = c.st;
+  HIP_TRY(embed(c.bf16, r.emb, c.rows, Mmax, d, c.x, st));
+  for (int l = 0; l < m.n_layers; ++l) {
+    const void* const* w = &r.layers[(size_t)l * 9];
+    HIP_TRY(rmsnorm(c.bf16, c.x, c.rows.M, Mmax, d, (const float*)w[0], c.xn, nullptr, st));
+    GemmCall g{};
+    g.bf16 = c.bf16;
+    g.Mmax = Mmax; g.Mdev = c.rows.M; g.scratch = c.scratch; g.rows = c.rows;
+    g.cosT = r.cosT; g.sinT = r.sinT; g.d = d; g.dh = dh; g.H = H; g.Pmax = c.cfg.max_prefix;
+    // q, k, v (+ rotary), k/v to their cache
+    g.kind = GEMM_QKV; g.A = c.xn; g.lda = d; g.N = 3 * d; g.K = d;
+    g.w0 = w[1]; g.w1 = w[2]; g.w2 = w[3]; g.split = d; g.q = c.q;
+    char* pk = (char*)r.pk + (size_t)l * r.pkv_layer_stride * es;
+    char* pv = (char*)r.pv + (size_t)l * r.pkv_layer_stride * es;
+    char* tk = (char*)r.tk + (size_t)l * r.tkv_layer_stride * es;
+    char* tv = (char*)r.tv + (size_t)l * r.tkv_layer_stride * es;
+    g.kv_mode = prefill ? 0 : 1;
+    g.kdst = prefill ? (void*)pk : (void*)tk;
+    g.vdst = prefill ? (void*)pv : (void*)tv;
+    HIP_TRY(gemm(g, st));
+    AttnCall at{};
+    at.bf16 = c.bf16; at.q = c.q; at.pk = pk; at.pv = pv;
+    at.tk = prefill ? nullptr : tk; at.tv = prefill ? nullptr : tv;
+    at.out = c.ao; at.rows = c.rows; at.Mmax = Mmax; at.B = B; at.Tq = Tq;
+    at.H = H; at.dh = dh; at.d = d; at.Pmax = c.cfg.max_prefix;
+    HIP_TRY(attention(at, st));
+    g.kind = GEMM_RESID; g.A = c.ao; g.lda = d; g.N = d; g.K = d; g.w0 = w[4]; g.out = c.x; g.ldo = d;
+    HIP_TRY(gemm(g, st));
+    HIP_TRY(rmsnorm(c.bf16, c.x, c.rows.M, Mmax, d, (const float*)w[5], c.xn, nullptr, st));
+    g.kind = GEMM_GU; g.A = c.xn; g.lda = d; g.N = 2 * f; g.K = d; g.w0 = w[6]; g.w1 = w[7]; g.split = f; g.hout = c.h;
+    HIP_TRY(gemm(g, st));
+    g.kind = GEMM_RESID; g.A = c.h; g.lda = f; g.N = d; g.K = f; g.w0 = w[8]; g.out = c.x; g.ldo = d;
+    HIP_TRY(gemm(g, st));
+  }
+  // final norm + item rows of the output head + log-softmax
+  const int* Mfin = prefill ? c.Mb : c.rows.M;
+  const int Mmf = prefill ? B : Mmax;
+  HIP_TRY(rmsnorm(c.bf16, c.x, Mfin, Mmf, d, r.final_norm, c.xn, prefill ? c.row_last : nullptr, st));
+  GemmCall g{};
+  g.kind = GEMM_STORE; g.bf16 = c.bf16; g.A = c.xn; g.lda = d; g.Mmax = Mmf; g.Mdev = Mfin;
+  g.N = c.nitem; g.K = d; g.w0 = r.lm_head; g.out = c.logits; g.ldo = c.nitem; g.scratch = c.scratch;
+  HIP_TRY(gemm(g, st));
+  if (prefill) HIP_TRY(log_softmax_rows(c.logits, c.Mb, B, c.nitem, nullptr, r.root, dbg, st));
+  else HIP_TRY(log_softmax_rows(c.logits, c.rows.M, Mmax, c.nitem, c.rows.slot, r.lp, dbg, st));
+  return ATSPEED_OK;
+}
+
+atspeed_status read_err(atspeed_ctx& c, int* out) {
+  HIP_TRY(hipMemcpyAsync(out, c.err, sizeof(int), hipMemcpyDeviceToHost, c.st));
+  HIP_TRY(hipStreamSynchronize(c.st));
+  return ATSPEED_OK;
+}
+
+// Tree of the context or the caller: the same layout, the caller's arrays.
+TreeDev tree_view(atspeed_ctx& c) { return c.tree; }
+
+atspeed_status tree_forward(atspeed_ctx& c, float* dbg_logits) {
+  HIP_TRY(hipMemsetAsync(c.err, 0, sizeof(int), c.st));
+  launch_tree_index(c.tree, c.trie, c.state, c.B, c.cfg.target.item_base, c.cfg.codebook, c.cfg.L, c.err, c.st);
+  HIP_TRY(hipGetLastError());
+  HIP_TRY(hipMemsetAsync(c.lo, 0, sizeof(int) * c.B, c.st));
+  launch_plan_tree(c.tree, c.lo, c.state.nfwd, c.B, c.P, c.rows, c.st);
+  HIP_TRY(hipGetLastError());
+  ST_TRY(forward(c, c.tgt, false, c.B * c.Tmax, c.Tmax, dbg_logits));
+  return ATSPEED_OK;
+}
+
+}  // namespace
+
+// ====================================================================== ABI
+
+extern "C" {
+
+const char* atspeed_last_error(void) { return g_err.c_str(); }
+
+atspeed_status atspeed_workspace_bytes(const atspeed_config* cfg, const atspeed_catalog* cat, size_t* bytes) {
+  if (!bytes) return fail(ATSPEED_E_INVALID, "bytes is null");
+  ST_TRY(check_config(cfg));
+  HostTrie t;
+  ST_TRY(build_trie(*cfg, cat, t));
+  atspeed_ctx c;
+  Arena a{nullptr};
+  layout(c, *cfg, (int)t.code.size(), a);
+  *bytes = a.off + 256;
+  return ATSPEED_OK;
+}
+
+atspeed_status atspeed_create(const atspeed_config* cfg, const atspeed_weights* target, const atspeed_weights* draft,
+                              const atspeed_catalog* cat, void* ws, size_t ws_bytes, atspeed_ctx** out) {
+  if (!out) return fail(ATSPEED_E_INVALID, "out is null");
+  *out = nullptr;
+  ST_TRY(check_config(cfg));
+  if (!ws) return fail(ATSPEED_E_WORKSPACE, "workspace is null");
+  if (reinterpret_cast<uintptr_t>(ws) & 255) return fail(ATSPEED_E_WORKSPACE, "workspace is not 256-byte aligned");
+  HostTrie t;
+  ST_TRY(build_trie(*cfg, cat, t));
+  size_t need = 0;
+  {
+    atspeed_ctx tmp;
+    Arena a{nullptr};
+    layout(tmp, *cfg, (int)t.code.size(), a);
+    need = a.off + 256;
+  }
+  if (ws_bytes < need) return fail(ATSPEED_E_WORKSPACE, "workspace too small: need " + std::to_string(need) + " bytes");
+  atspeed_ctx* c = new atspeed_ctx();
+  c->cfg = *cfg;
+  c->st = (hipStream_t)cfg->stream;
+  Arena a{(char*)ws};
+  layout(*c, *cfg, (int)t.code.size(), a);
+  c->htrie = std::move(t);
+  atspeed_status s = bind_weights(c->tgt, target, "target");
+  if (s == ATSPEED_OK && draft && cfg->draft.n_layers > 0) s = bind_weights(c->dft, draft, "draft");
+  auto bail = [&](atspeed_status e) { delete c; return e; };
+  if (s != ATSPEED_OK) return bail(s);
+  const size_t nn = c->htrie.code.size();
+  hipError_t e = hipMemcpyAsync((void*)c->trie.code, c->htrie.code.data(), nn * 4, hipMemcpyHostToDevice, c->st);
+  if (e == hipSuccess) e = hipMemcpyAsync((void*)c->trie.first, c->htrie.first.data(), nn * 4, hipMemcpyHostToDevice, c->st);
+  if (e == hipSuccess) e = hipMemcpyAsync((void*)c->trie.cnt, c->htrie.cnt.data(), nn * 4, hipMemcpyHostToDevice, c->st);
+  if (e == hipSuccess) e = hipMemsetAsync(c->state.t, 0, sizeof(int) * cfg->max_batch, c->st);
+  if (e == hipSuccess) e = hipMemsetAsync(c->state.steps, 0, sizeof(int) * cfg->max_batch, c->st);
+  if (e == hipSuccess) e = hipMemsetAsync(c->tree.n_nodes, 0, sizeof(int) * cfg->max_batch, c->st);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->st);
+  if (e != hipSuccess) return bail(fail(ATSPEED_E_DEVICE, std::string("create: ") + hipGetErrorString(e)));
+  s = upload_rope(*c, c->tgt);
+  if (s == ATSPEED_OK && c->dft.present) s = upload_rope(*c, c->dft);
+  if (s != ATSPEED_OK) return bail(s);
+  *out = c;
+  return ATSPEED_OK;
+}
+
+void atspeed_destroy(atspeed_ctx* ctx) { delete ctx; }
+
+atspeed_status atspeed_prefill(atspeed_ctx* c, int32_t B, int32_t P, const int32_t* prefix, float* root_logits) {
+  if (!c) return fail(ATSPEED_E_INVALID, "ctx is null");
+  if (!prefix) return fail(ATSPEED_E_INVALID, "prefix is null");
+  if (B < 1 || B > c->cfg.max_batch) return fail(ATSPEED_E_SHAPE, "B out of range");
+  if (P < 1 || P > c->cfg.max_prefix) return fail(ATSPEED_E_SHAPE, "P out of range");
+  c->B = B;
+  c->P = P;
+  std::vector<int> last(B), sizes{B, B * c->Tmax};
+  for (int u = 0; u < B; ++u) last[u] = u * P + P - 1;
+  HIP_TRY(hipMemcpyAsync(c->row_last, last.data(), B * 4, hipMemcpyHostToDevice, c->st));
+  HIP_TRY(hipMemcpyAsync(c->Mb, &sizes[0], 4, hipMemcpyHostToDevice, c->st));
+  HIP_TRY(hipMemcpyAsync(c->Mall, &sizes[1], 4, hipMemcpyHostToDevice, c->st));
+  launch_plan_prefix(prefix, B, P, c->rows, c->st);
+  HIP_TRY(hipGetLastError());
+  ST_TRY(forward(*c, c->tgt, true, B * P, P, root_logits));
+  if (c->dft.present) ST_TRY(forward(*c, c->dft, true, B * P, P, nullptr));
+  HIP_TRY(hipMemsetAsync(c->state.t, 0, sizeof(int) * B, c->st));
+  HIP_TRY(hipMemsetAsync(c->state.steps, 0, sizeof(int) * B, c->st));
+  std::vector<int> ones(B, 1);
+  HIP_TRY(hipMemcpyAsync(c->state.nb, ones.data(), B * 4, hipMemcpyHostToDevice, c->st));
+  HIP_TRY(hipMemsetAsync(c->tree.n_nodes, 0, sizeof(int) * B, c->st));
+  HIP_TRY(hipStreamSynchronize(c->st));  // host vectors above go out of scope
+  c->prefilled = true;
+  c->drafted = false;
+  return ATSPEED_OK;
+}
+
+atspeed_status atspeed_draft(atspeed_ctx* c) {
+  if (!c) return fail(ATSPEED_E_INVALID, "ctx is null");
+  if (!c->dft.present) return fail(ATSPEED_E_STATE, "context has no draft model");
+  if (!c->prefilled) return fail(ATSPEED_E_STATE, "draft before prefill");
+  const atspeed_config& cf = c->cfg;
+  const int B = c->B, L = cf.L;
+  launch_tree_from_beams(c->state, c->tree, c->trie, B, cf.target.item_base, cf.codebook, L, c->st);
+  HIP_TRY(hipGetLastError());
+  // draft log-probs along the Y_t paths (none at t = 0), then the beams' draft scores
+  HIP_TRY(hipMemsetAsync(c->lo, 0, sizeof(int) * B, c->st));
+  launch_plan_tree(c->tree, c->lo, c->state.npath, B, c->P, c->rows, c->st);
+  HIP_TRY(hipGetLastError());
+  ST_TRY(forward(*c, c->dft, false, B * c->Tmax, c->Tmax, nullptr));
+  launch_draft_beam_scores(c->state, c->tree, c->dft.lp, c->dft.root, c->nitem, cf.codebook, L, B, c->st);
+  HIP_TRY(hipGetLastError());
+  for (int j = 1; j <= std::min(cf.gamma, L); ++j) {
+    launch_draft_select(c->state, c->tree, c->trie, c->dft.lp, c->dft.root, c->nitem, cf.target.item_base,
+                        cf.codebook, L, j, cf.N, c->lvl_lo, c->lvl_hi, c->keys, c->max_cand, B, c->st);
+    HIP_TRY(hipGetLastError());
+    if (j < std::min(cf.gamma, L)) {  // log-probs of the new level feed the next one
+      launch_plan_tree(c->tree, c->lvl_lo, c->lvl_hi, B, c->P, c->rows, c->st);
+      HIP_TRY(hipGetLastError());
+      ST_TRY(forward(*c, c->dft, false, B * c->Tmax, c->Tmax, nullptr));
+    }
+  }
+  c->drafted = true;
+  return ATSPEED_OK;
+}
+
+atspeed_status atspeed_get_tree(atspeed_ctx* c, atspeed_tree* out) {
+  if (!c || !out) return fail(ATSPEED_E_INVALID, "null argument");
+  out->max_nodes = c->tree.max_nodes;
+  out->n_nodes = c->tree.n_nodes;
+  out->token = c->tree.token;
+  out->parent = c->tree.parent;
+  out->depth = c->tree.depth;
+  out->q_score = c->tree.q_score;
+  return ATSPEED_OK;
+}
+
+atspeed_status atspeed_tree_logits(atspeed_ctx* c, float* logits) {
+  if (!c || !logits) return fail(ATSPEED_E_INVALID, "null argument");
+  if (!c->prefilled) return fail(ATSPEED_E_STATE, "tree_logits before prefill");
+  ST_TRY(tree_forward(*c, logits));
+  int err = 0;
+  ST_TRY(read_err(*c, &err));
+  if (err) return fail(ATSPEED_E_INVALID, "malformed tree (code " + std::to_string(err) + ")");
+  return ATSPEED_OK;
+}
+
+static atspeed_status accept_on(atspeed_ctx* c, const float* lpt, const float* roott, int32_t* accepted,
+                                int32_t* t_after) {
+  const atspeed_config& cf = c->cfg;
+  launch_verify_strict(c->state, c->tree, c->trie, lpt, roott, c->nitem, cf.codebook, cf.L, c->keys, c->max_cand,
+                       accepted ? accepted : c->acc_tmp, t_after ? t_after : c->tafter_tmp, c->B, c->st);
+  HIP_TRY(hipGetLastError());
+  return ATSPEED_OK;
+}
+
+atspeed_status atspeed_verify(atspeed_ctx* c, int32_t* accepted, int32_t* t_after, float* logits) {
+  if (!c) return fail(ATSPEED_E_INVALID, "ctx is null");
+  if (!c->prefilled) return fail(ATSPEED_E_STATE, "verify before prefill");
+  ST_TRY(tree_forward(*c, logits));
+  int err = 0;
+  ST_TRY(read_err(*c, &err));
+  if (err) return fail(ATSPEED_E_INVALID, "malformed tree (code " + std::to_string(err) + ")");
+  ST_TRY(accept_on(c, c->tgt.lp, c->tgt.root, accepted, t_after));
+  c->drafted = false;
+  return ATSPEED_OK;
+}
+
+atspeed_status atspeed_accept(atspeed_ctx* c, const float* logits, const float* root_logits, int32_t* accepted,
+                              int32_t* t_after) {
+  if (!c || !logits || !root_logits) return fail(ATSPEED_E_INVALID, "null argument");
+  if (!c->prefilled) return fail(ATSPEED_E_STATE, "accept before prefill");
+  HIP_TRY(hipMemsetAsync(c->err, 0, sizeof(int), c->st));
+  launch_tree_index(c->tree, c->trie, c->state, c->B, c->cfg.target.item_base, c->cfg.codebook, c->cfg.L, c->err, c->st);
+  HIP_TRY(hipGetLastError());
+  int err = 0;
+  ST_TRY(read_err(*c, &err));
+  if (err) return fail(ATSPEED_E_INVALID, "malformed tree (code " + std::to_string(err) + ")");
+  // log-softmax of the caller's logits into the slot-indexed buffers (row = slot)
+  HIP_TRY(log_softmax_rows(logits, c->Mall, c->B * c->Tmax, c->nitem, nullptr, c->tgt.lp, nullptr, c->st));
+  HIP_TRY(log_softmax_rows(root_logits, c->Mb, c->B, c->nitem, nullptr, c->tgt.root, nullptr, c->st));
+  ST_TRY(accept_on(c, c->tgt.lp, c->tgt.root, accepted, t_after));
+  HIP_TRY(hipStreamSynchronize(c->st));
+  return ATSPEED_OK;
+}
+
+atspeed_status atspeed_get_state(atspeed_ctx* c, int32_t B, int32_t* t, int32_t* nbeams, int32_t* paths, float* scores) {
+  if (!c || !t || !nbeams || !paths || !scores) return fail(ATSPEED_E_INVALID, "null argument");
+  if (B < 1 || B > c->cfg.max_batch) return fail(ATSPEED_E_SHAPE, "B out of range");
+  const int K = c->cfg.K, L = c->cfg.L;
+  std::vector<uint32_t> pk((size_t)B * K);
+  HIP_TRY(hipMemcpyAsync(t, c->state.t, B * 4, hipMemcpyDeviceToHost, c->st));
+  HIP_TRY(hipMemcpyAsync(nbeams, c->state.nb, B * 4, hipMemcpyDeviceToHost, c->st));
+  HIP_TRY(hipMemcpyAsync(pk.data(), c->state.path, pk.size() * 4, hipMemcpyDeviceToHost, c->st));
+  HIP_TRY(hipMemcpyAsync(scores, c->state.score, (size_t)B * K * 4, hipMemcpyDeviceToHost, c->st));
+  HIP_TRY(hipStreamSynchronize(c->st));
+  for (size_t i = 0; i < pk.size(); ++i)
+    for (int l = 0; l < L; ++l) paths[i * L + l] = (pk[i] >> (8 * (3 - l))) & 0xFF;
+  return ATSPEED_OK;
+}
+
+atspeed_status atspeed_set_state(atspeed_ctx* c, int32_t B, const int32_t* t, const int32_t* nbeams,
+                                 const int32_t* paths, const float* scores) {
+  if (!c || !t || !nbeams || !paths || !scores) return fail(ATSPEED_E_INVALID, "null argument");
+  if (B < 1 || B != c->B) return fail(ATSPEED_E_SHAPE, "B must equal the prefilled batch");
+  const int K = c->cfg.K, L = c->cfg.L;
+  std::vector<uint32_t> pk((size_t)B * K, 0);
+  std::vector<int> tr((size_t)B * K, 0);
+  for (int u = 0; u < B; ++u) {
+    if (t[u] < 0 || t[u] > L) return fail(ATSPEED_E_INVALID, "t out of range");
+    if (nbeams[u] < 1 || nbeams[u] > K) return fail(ATSPEED_E_INVALID, "nbeams out of range");
+    if (t[u] == 0 && nbeams[u] != 1) return fail(ATSPEED_E_INVALID, "t = 0 holds one (empty) beam");
+    for (int k = 0; k < nbeams[u]; ++k) {
+      int node = 0;
+      uint32_t p = 0;
+      for (int l = 0; l < t[u]; ++l) {
+        int code = paths[((size_t)u * K + k) * L + l];
+        if (code < 0 || code >= c->cfg.codebook) return fail(ATSPEED_E_INVALID, "path code out of range");
+        node = c->htrie.child(node, code);
+        if (node < 0) return fail(ATSPEED_E_INVALID, "beam is not a catalog prefix");
+        p |= (uint32_t)code << (8 * (3 - l));
+      }
+      pk[(size_t)u * K + k] = p;
+      tr[(size_t)u * K + k] = node;
+    }
+  }
+  HIP_TRY(hipMemcpyAsync(c->state.t, t, B * 4, hipMemcpyHostToDevice, c->st));
+  HIP_TRY(hipMemcpyAsync(c->state.nb, nbeams, B * 4, hipMemcpyHostToDevice, c->st));
+  HIP_TRY(hipMemcpyAsync(c->state.path, pk.data(), pk.size() * 4, hipMemcpyHostToDevice, c->st));
+  HIP_TRY(hipMemcpyAsync(c->state.trie, tr.data(), tr.size() * 4, hipMemcpyHostToDevice, c->st));
+  HIP_TRY(hipMemcpyAsync(c->state.score, scores, (size_t)B * K * 4, hipMemcpyHostToDevice, c->st));
+  HIP_TRY(hipStreamSynchronize(c->st));
+  return ATSPEED_OK;
+}
+
+atspeed_status atspeed_decode_topk(atspeed_ctx* c, int32_t B, int32_t P, const int32_t* prefix, int32_t* items,
+                                   float* scores, int32_t* n_items, atspeed_stats* stats) {
+  if (!c) return fail(ATSPEED_E_INVALID, "ctx is null");
+  if (!items || !scores || !n_items) return fail(ATSPEED_E_INVALID, "null output");
+  if (!c->dft.present) return fail(ATSPEED_E_STATE, "context has no draft model");
+  hipEvent_t ev[2];
+  const bool timing = stats != nullptr;
+  if (timing) {
+    HIP_TRY(hipEventCreate(&ev[0]));
+    HIP_TRY(hipEventCreate(&ev[1]));
+    stats->n_steps = 0;
+    stats->ms_prefill = stats->ms_draft = stats->ms_verify = 0;
+    HIP_TRY(hipEventRecord(ev[0], c->st));
+  }
+  auto lap = [&](double* acc) -> atspeed_status {
+    if (!timing) return ATSPEED_OK;
+    HIP_TRY(hipEventRecord(ev[1], c->st));
+    HIP_TRY(hipEventSynchronize(ev[1]));
+    float ms = 0;
+    HIP_TRY(hipEventElapsedTime(&ms, ev[0], ev[1]));
+    *acc += ms;
+    HIP_TRY(hipEventRecord(ev[0], c->st));
+    return ATSPEED_OK;
+  };
+  ST_TRY(atspeed_prefill(c, B, P, prefix, nullptr));
+  ST_TRY(lap(timing ? &stats->ms_prefill : nullptr));
+  const int L = c->cfg.L;
+  std::vector<int> acc(B), ta(B);
+  for (int step = 0; step < L; ++step) {
+    ST_TRY(atspeed_draft(c));
+    ST_TRY(lap(timing ? &stats->ms_draft : nullptr));
+    ST_TRY(atspeed_verify(c, c->acc_tmp, c->tafter_tmp, nullptr));
+    HIP_TRY(hipMemcpyAsync(acc.data(), c->acc_tmp, B * 4, hipMemcpyDeviceToHost, c->st));
+    HIP_TRY(hipMemcpyAsync(ta.data(), c->tafter_tmp, B * 4, hipMemcpyDeviceToHost, c->st));
+    HIP_TRY(hipStreamSynchronize(c->st));
+    ST_TRY(lap(timing ? &stats->ms_verify : nullptr));
+    if (timing) {
+      if (stats->accepted) std::copy(acc.begin(), acc.end(), stats->accepted + (size_t)step * c->cfg.max_batch);
+      if (stats->t_after) std::copy(ta.begin(), ta.end(), stats->t_after + (size_t)step * c->cfg.max_batch);
+      stats->n_steps = step + 1;
+    }
+    if (std::all_of(ta.begin(), ta.end(), [&](int v) { return v >= L; })) break;
+  }
+  if (timing) {
+    hipEventDestroy(ev[0]);
+    hipEventDestroy(ev[1]);
+  }
+  // outputs from the final state
+  const int K = c->cfg.K;
+  std::vector<int> t(B), nb(B), paths((size_t)B * K * L);
+  std::vector<float> sc((size_t)B * K);
+  ST_TRY(atspeed_get_state(c, B, t.data(), nb.data(), paths.data(), sc.data()));
+  HIP_TRY(hipMemcpyAsync(items, paths.data(), paths.size() * 4, hipMemcpyHostToDevice, c->st));
+  HIP_TRY(hipMemcpyAsync(scores, sc.data(), sc.size() * 4, hipMemcpyHostToDevice, c->st));
+  HIP_TRY(hipMemcpyAsync(n_items, nb.data(), B * 4, hipMemcpyHostToDevice, c->st));
+  HIP_TRY(hipStreamSynchronize(c->st));
+  return ATSPEED_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,60 @@
+// Device views of the trie, the per-user decoding state and the drafted tree.
+#pragma once
+#include <hip/hip_runtime.h>
+#include "common.h"
+
+namespace atspeed {
+
+constexpr int kMaxPar = 128;  // parents per level (>= max(K, N))
+constexpr int kMaxSel = 128;  // selected per level (>= max(K, N))
+
+// Item trie: node 0 is the root; the children of node n are the nodes
+// first[n] .. first[n] + cnt[n] - 1, sorted by code.
+struct TrieDev {
+  const int* code;
+  const int* first;
+  const int* cnt;
+};
+
+// Per-user state: current item level t and the target beams Y_t.
+struct StateDev {
+  int* t;           // [B]
+  int* nb;          // [B] beams held
+  uint32_t* path;   // [B, K] path keys
+  int* trie;        // [B, K] trie node of each beam
+  float* score;     // [B, K] target cumulative log-prob
+  float* qscore;    // [B, K] draft cumulative log-prob (drafting)
+  int* beam_slot;   // [B, K] tree slot of each beam's last node (t > 0)
+  int* steps;       // [B] speculative steps run
+  int* npath;       // [B] tree nodes holding the Y_t paths
+  int* nfwd;        // [B] tree nodes forwarded by verify (depth < L)
+  int K, gamma;
+};
+
+struct TreeDev {
+  int max_nodes;
+  int* n_nodes;
+  int* token;
+  int* parent;
+  int* depth;
+  float* q_score;
+  uint32_t* tpath;  // derived: path key of each node
+  int* ttrie;       // derived: trie node of each node
+};
+
+void launch_tree_from_beams(const StateDev& s, const TreeDev& tr, const TrieDev& trie, int B, int item_base,
+                            int codebook, int L, hipStream_t st);
+void launch_tree_index(const TreeDev& tr, const TrieDev& trie, const StateDev& s, int B, int item_base, int codebook,
+                       int L, int* err, hipStream_t st);
+void launch_plan_tree(const TreeDev& tr, const int* lo, const int* hi, int B, int P, const Rows& rows, hipStream_t st);
+void launch_plan_prefix(const int* prefix, int B, int P, const Rows& rows, hipStream_t st);
+void launch_draft_beam_scores(const StateDev& s, const TreeDev& tr, const float* lpq, const float* rootq, int nitem,
+                              int codebook, int L, int B, hipStream_t st);
+void launch_draft_select(const StateDev& s, const TreeDev& tr, const TrieDev& trie, const float* lpq,
+                         const float* rootq, int nitem, int item_base, int codebook, int L, int j, int N, int* lvl_lo,
+                         int* lvl_hi, unsigned long long* keys, int max_cand, int B, hipStream_t st);
+void launch_verify_strict(const StateDev& s, const TreeDev& tr, const TrieDev& trie, const float* lpt,
+                          const float* roott, int nitem, int codebook, int L, unsigned long long* keys, int max_cand,
+                          int* accepted, int* t_after, int B, hipStream_t st);
+
+}  // namespace atspeed

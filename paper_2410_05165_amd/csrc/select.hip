@@ -1,0 +1,495 @@
+// Tree bookkeeping, trie-constrained beam selection and strict acceptance.
+//
+// A sequence of codes is packed into a 32-bit path key, code of item level l in
+// byte 3-l, so comparing path keys of equal depth compares the sequences
+// lexicographically.  A candidate's 64-bit selection key is
+//   (~orderkey(score) << 32) | pathkey
+// whose ascending order is: higher score first, then lexicographically smaller
+// sequence (the pinned tie-break).  Keys are unique because paths are.
+// TopK is a radix select on those keys (8 bits per pass, 256-bin LDS histogram)
+// followed by a rank sort of the K survivors, one workgroup per user.
+#include "common.h"
+#include "select.h"
+
+namespace atspeed {
+
+__device__ __forceinline__ uint32_t path_with(uint32_t path, int level0, int code) {
+  return path | ((uint32_t)code << (8 * (3 - level0)));
+}
+__device__ __forceinline__ int path_code(uint32_t path, int level0) { return (path >> (8 * (3 - level0))) & 0xFF; }
+
+__device__ __forceinline__ uint64_t make_key(float score, uint32_t path) {
+  return ((uint64_t)(~float_order_key(score)) << 32) | path;
+}
+__device__ __forceinline__ float key_score(uint64_t key) {
+  uint32_t k = ~(uint32_t)(key >> 32);
+  uint32_t u = (k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k;
+  return __uint_as_float(u);
+}
+
+__device__ int trie_child(const TrieDev& t, int node, int code) {
+  int lo = t.first[node], hi = lo + t.cnt[node] - 1;
+  while (lo <= hi) {
+    int mid = (lo + hi) >> 1, c = t.code[mid];
+    if (c == code) return mid;
+    if (c < code) lo = mid + 1; else hi = mid - 1;
+  }
+  return -1;
+}
+
+// ---------------------------------------------------------------- selection core
+struct SelShared {
+  int hist[256];
+  int cum[4];
+  unsigned long long prefix, mask;
+  int need, done, count;
+  int par_off[kMaxPar + 1];
+};
+
+// Keys of all trie-valid one-code extensions of the parents, into keys[].
+// par_lp[i] is the log-prob row of parent i; codes of item level lvl0 (0-based).
+__device__ int gen_candidates(const TrieDev& trie, int npar, const uint32_t* par_path, const float* par_score,
+                              const int* par_trie, const float* const* par_lp, int lvl0, int codebook,
+                              unsigned long long* keys, SelShared& sh) {
+  const int tid = threadIdx.x;
+  if (tid == 0) {
+    int acc = 0;
+    for (int i = 0; i < npar; ++i) { sh.par_off[i] = acc; acc += trie.cnt[par_trie[i]]; }
+    sh.par_off[npar] = acc;
+  }
+  __syncthreads();
+  const int n = sh.par_off[npar];
+  for (int c = tid; c < n; c += blockDim.x) {
+    int lo = 0, hi = npar - 1;
+    while (lo < hi) {  // last parent whose offset <= c
+      int mid = (lo + hi + 1) >> 1;
+      if (sh.par_off[mid] <= c) lo = mid; else hi = mid - 1;
+    }
+    const int child = trie.first[par_trie[lo]] + (c - sh.par_off[lo]);
+    const int code = trie.code[child];
+    const float s = par_score[lo] + par_lp[lo][codebook * lvl0 + code];
+    keys[c] = make_key(s, path_with(par_path[lo], lvl0, code));
+  }
+  __syncthreads();
+  return n;
+}
+
+// The nsel smallest keys, ascending, into out[]; returns their number.
+__device__ int select_smallest(const unsigned long long* keys, int n, int nsel, unsigned long long* out, SelShared& sh) {
+  const int tid = threadIdx.x, nt = blockDim.x;
+  if (nsel > n) nsel = n;
+  if (tid == 0) { sh.prefix = 0; sh.mask = 0; sh.need = nsel; sh.done = (nsel == n); sh.count = 0; }
+  __syncthreads();
+  for (int shift = 56; shift >= 0 && !sh.done; shift -= 8) {
+    for (int i = tid; i < 256; i += nt) sh.hist[i] = 0;
+    __syncthreads();
+    const unsigned long long pf = sh.prefix, mk = sh.mask;
+    for (int c = tid; c < n; c += nt) {
+      unsigned long long k = keys[c];
+      if ((k & mk) == pf) atomicAdd(&sh.hist[(k >> shift) & 255], 1);
+    }
+    __syncthreads();
+    if (tid == 0) {
+      int below = 0, b = 0;
+      for (; b < 256; ++b) {
+        if (below + sh.hist[b] >= sh.need) break;
+        below += sh.hist[b];
+      }
+      sh.need -= below;
+      sh.prefix |= (unsigned long long)b << shift;
+      sh.mask |= 0xFFull << shift;
+      if (sh.hist[b] == sh.need) sh.done = 1;
+    }
+    __syncthreads();
+  }
+  const unsigned long long pf = sh.prefix, mk = sh.mask;
+  const bool all = (nsel == n);
+  for (int c = tid; c < n; c += nt) {
+    unsigned long long k = keys[c];
+    if (all || (k & mk) <= pf) {
+      int slot = atomicAdd(&sh.count, 1);
+      if (slot < kMaxSel) out[kMaxSel + slot] = k;  // unsorted staging half
+    }
+  }
+  __syncthreads();
+  for (int i = tid; i < nsel; i += nt) {
+    unsigned long long k = out[kMaxSel + i];
+    int rank = 0;
+    for (int j = 0; j < nsel; ++j) rank += out[kMaxSel + j] < k;
+    out[rank] = k;
+  }
+  __syncthreads();
+  return nsel;
+}
+
+// ---------------------------------------------------------------- tree kernels
+
+// Paths of the current beams Y_t (depths 1..t), deduplicated and level-ordered,
+// become the first nodes of each user's tree; beam_slot[k] is beam k's node.
+__global__ void tree_from_beams_kernel(StateDev s, TreeDev tr, TrieDev trie, int item_base, int codebook, int L) {
+  const int u = blockIdx.x;
+  if (threadIdx.x != 0) return;
+  const int t = s.t[u];
+  const int nb = s.nb[u];
+  int n = 0;
+  const size_t tb = (size_t)u * tr.max_nodes;
+  const int K = s.K;
+  if (t > 0 && t < L) {
+    for (int l = 1; l <= t; ++l) {
+      const uint32_t mask = l == 4 ? 0xFFFFFFFFu : ~(0xFFFFFFFFu >> (8 * l));
+      for (int k = 0; k < nb; ++k) {
+        const uint32_t pre = s.path[u * K + k] & mask;
+        int found = -1;
+        for (int i = 0; i < n; ++i)
+          if (tr.depth[tb + i] == l && tr.tpath[tb + i] == pre) { found = i; break; }
+        if (found < 0) {
+          int parent = -1, ptrie = 0;
+          if (l > 1) {
+            const uint32_t pm = ~(0xFFFFFFFFu >> (8 * (l - 1)));
+            for (int i = 0; i < n; ++i)
+              if (tr.depth[tb + i] == l - 1 && tr.tpath[tb + i] == (pre & pm)) { parent = i; break; }
+            ptrie = tr.ttrie[tb + parent];
+          }
+          const int code = path_code(pre, l - 1);
+          tr.token[tb + n] = item_base + codebook * (l - 1) + code;
+          tr.parent[tb + n] = parent;
+          tr.depth[tb + n] = l;
+          tr.q_score[tb + n] = 0.f;
+          tr.tpath[tb + n] = pre;
+          tr.ttrie[tb + n] = trie_child(trie, ptrie, code);
+          found = n++;
+        }
+        if (l == t) s.beam_slot[u * K + k] = found;
+      }
+    }
+  }
+  tr.n_nodes[u] = n;
+  s.npath[u] = n;
+}
+
+// Derived per-node data of a caller or draft tree: path key, trie node, ancestors;
+// validation; number of nodes to forward (depth < L, a prefix of the level order).
+__global__ void tree_index_kernel(TreeDev tr, TrieDev trie, StateDev s, int item_base, int codebook, int L, int* err) {
+  const int u = blockIdx.x;
+  const size_t tb = (size_t)u * tr.max_nodes;
+  const int n = s.t[u] >= L ? 0 : tr.n_nodes[u];
+  __shared__ int nfwd;
+  if (threadIdx.x == 0) nfwd = n;
+  __syncthreads();
+  if (n < 0 || n > tr.max_nodes) {
+    if (threadIdx.x == 0) atomicOr(err, 1);
+    return;
+  }
+  for (int i = threadIdx.x; i < n; i += blockDim.x) {
+    int chain[4], dep = tr.depth[tb + i], cur = i, ok = dep >= 1 && dep <= L;
+    for (int l = dep; ok && l >= 1; --l) {
+      if (cur < 0 || cur > i || tr.depth[tb + cur] != l) { ok = 0; break; }
+      chain[l - 1] = cur;
+      const int p = tr.parent[tb + cur];
+      if (l == 1 ? p != -1 : (p < 0 || p >= cur)) { ok = 0; break; }
+      cur = p;
+    }
+    if (ok && i > 0 && tr.depth[tb + i - 1] > dep) ok = 0;  // level order
+    uint32_t path = 0;
+    int node = 0;
+    for (int l = 1; ok && l <= dep; ++l) {
+      const int code = tr.token[tb + chain[l - 1]] - item_base - codebook * (l - 1);
+      if (code < 0 || code >= codebook) { ok = 0; break; }
+      node = trie_child(trie, node, code);
+      if (node < 0) { ok = 0; break; }
+      path = path_with(path, l - 1, code);
+    }
+    if (!ok) { atomicOr(err, 1); continue; }
+    tr.tpath[tb + i] = path;
+    tr.ttrie[tb + i] = node;
+    if (dep == L) atomicMin(&nfwd, i);
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) s.nfwd[u] = nfwd;
+}
+
+// Beam slots of Y_t in a caller tree (verify): every beam path must be a node of depth t.
+__global__ void find_beam_slots_kernel(TreeDev tr, StateDev s, int L, int* err) {
+  const int u = blockIdx.x;
+  const int t = s.t[u];
+  if (t <= 0 || t >= L) return;
+  const size_t tb = (size_t)u * tr.max_nodes;
+  const int n = tr.n_nodes[u];
+  for (int k = threadIdx.x; k < s.nb[u]; k += blockDim.x) {
+    const uint32_t p = s.path[u * s.K + k];
+    int found = -1;
+    for (int i = 0; i < n; ++i)
+      if (tr.depth[tb + i] == t && tr.tpath[tb + i] == p) { found = i; break; }
+    if (found < 0) atomicOr(err, 2);
+    s.beam_slot[u * s.K + k] = found;
+  }
+}
+
+// Rows of one forward: nodes with slot in [lo[u], hi[u]) of every user, users in order.
+__global__ void plan_tree_rows_kernel(TreeDev tr, const int* lo, const int* hi, int B, int P, Rows rows) {
+  __shared__ int off[1025];
+  if (threadIdx.x == 0) {
+    int acc = 0;
+    for (int u = 0; u < B; ++u) {
+      off[u] = acc;
+      rows.user_off[u] = acc;
+      acc += max(0, hi[u] - lo[u]);
+    }
+    off[B] = acc;
+    rows.user_off[B] = acc;
+    *rows.M = acc;
+  }
+  __syncthreads();
+  for (int u = 0; u < B; ++u) {
+    const int a = lo[u], cnt = off[u + 1] - off[u];
+    const size_t tb = (size_t)u * tr.max_nodes;
+    for (int i = threadIdx.x; i < cnt; i += blockDim.x) {
+      const int s = a + i, r = off[u] + i;
+      const int dep = tr.depth[tb + s];
+      rows.user[r] = u;
+      rows.token[r] = tr.token[tb + s];
+      rows.pos[r] = P + dep - 1;
+      rows.slot[r] = (int)(tb + s);
+      rows.nctx[r] = P;
+      int cur = s;
+      for (int l = dep; l >= 1; --l) {
+        rows.anc[r * 4 + l - 1] = (int)(tb + cur);
+        cur = tr.parent[tb + cur];
+      }
+      for (int l = dep; l < 4; ++l) rows.anc[r * 4 + l] = 0;
+      rows.nanc[r] = dep;
+    }
+  }
+}
+
+// Rows of the prefill: B users x P positions.
+__global__ void plan_prefix_rows_kernel(const int* prefix, int B, int P, Rows rows) {
+  const int total = B * P;
+  for (int r = blockIdx.x * blockDim.x + threadIdx.x; r < total; r += gridDim.x * blockDim.x) {
+    const int u = r / P, p = r % P;
+    rows.user[r] = u;
+    rows.token[r] = prefix[r];
+    rows.pos[r] = p;
+    rows.slot[r] = -1;
+    rows.nctx[r] = p + 1;
+    rows.nanc[r] = 0;
+    if (p == 0) rows.user_off[u] = r;
+    if (r == 0) { rows.user_off[B] = total; *rows.M = total; }
+  }
+}
+
+// ---------------------------------------------------------------- draft
+// Draft score of every beam of Y_t: sum of draft log-probs along its path.
+__global__ void draft_beam_scores_kernel(StateDev s, TreeDev tr, const float* lpq, const float* rootq, int nitem,
+                                         int codebook, int L) {
+  const int u = blockIdx.x;
+  const int t = s.t[u];
+  if (t >= L) return;
+  for (int k = threadIdx.x; k < s.nb[u]; k += blockDim.x) {
+    float acc = 0.f;
+    if (t > 0) {
+      int chain[4], cur = s.beam_slot[u * s.K + k];
+      for (int l = t; l >= 1; --l) { chain[l - 1] = cur; cur = tr.parent[(size_t)u * tr.max_nodes + cur]; }
+      const uint32_t p = s.path[u * s.K + k];
+      for (int l = 1; l <= t; ++l) {
+        const float* row = l == 1 ? rootq + (size_t)u * nitem
+                                  : lpq + ((size_t)u * tr.max_nodes + chain[l - 2]) * nitem;
+        acc += row[codebook * (l - 1) + path_code(p, l - 1)];
+      }
+    }
+    s.qscore[u * s.K + k] = acc;
+  }
+}
+
+// One drafted level: TopN over the extensions of the previous level (level 1:
+// the beams of Y_t), appended to the tree; lvl[u] = [begin, end) of the new nodes.
+__global__ void __launch_bounds__(256)
+draft_select_kernel(StateDev s, TreeDev tr, TrieDev trie, const float* lpq, const float* rootq, int nitem,
+                    int item_base, int codebook, int L, int j, int N, int* lvl_lo, int* lvl_hi,
+                    unsigned long long* keys_all, int max_cand) {
+  __shared__ SelShared sh;
+  __shared__ uint32_t ppath[kMaxPar];
+  __shared__ float pscore[kMaxPar];
+  __shared__ int ptrie[kMaxPar], pslot[kMaxPar];
+  __shared__ const float* plp[kMaxPar];
+  __shared__ unsigned long long sel[2 * kMaxSel];
+  const int u = blockIdx.x, tid = threadIdx.x;
+  const int t = s.t[u];
+  const int J = min(s.gamma, L - t);
+  const size_t tb = (size_t)u * tr.max_nodes;
+  if (t >= L || j > J) {
+    if (tid == 0) { lvl_lo[u] = tr.n_nodes[u]; lvl_hi[u] = tr.n_nodes[u]; }
+    return;
+  }
+  int npar;
+  if (j == 1) {
+    npar = t == 0 ? 1 : s.nb[u];
+    for (int i = tid; i < npar; i += blockDim.x) {
+      if (t == 0) { ppath[i] = 0; pscore[i] = 0.f; ptrie[i] = 0; pslot[i] = -1; plp[i] = rootq + (size_t)u * nitem; }
+      else {
+        const int sl = s.beam_slot[u * s.K + i];
+        ppath[i] = s.path[u * s.K + i]; pscore[i] = s.qscore[u * s.K + i]; ptrie[i] = s.trie[u * s.K + i];
+        pslot[i] = sl; plp[i] = lpq + (tb + sl) * nitem;
+      }
+    }
+  } else {
+    const int a = lvl_lo[u];
+    npar = lvl_hi[u] - a;
+    for (int i = tid; i < npar; i += blockDim.x) {
+      const int sl = a + i;
+      ppath[i] = tr.tpath[tb + sl]; pscore[i] = tr.q_score[tb + sl]; ptrie[i] = tr.ttrie[tb + sl];
+      pslot[i] = sl; plp[i] = lpq + (tb + sl) * nitem;
+    }
+  }
+  __syncthreads();
+  unsigned long long* keys = keys_all + (size_t)u * max_cand;
+  const int lvl0 = t + j - 1;
+  const int n = gen_candidates(trie, npar, ppath, pscore, ptrie, plp, lvl0, codebook, keys, sh);
+  const int ns = select_smallest(keys, n, N, sel, sh);
+  const int base = tr.n_nodes[u];
+  for (int i = tid; i < ns; i += blockDim.x) {
+    const unsigned long long k = sel[i];
+    const uint32_t path = (uint32_t)k;
+    const int code = path_code(path, lvl0);
+    const uint32_t ppre = lvl0 == 0 ? 0u : (path & ~(0xFFFFFFFFu >> (8 * lvl0)));
+    int pi = 0;
+    for (int q = 0; q < npar; ++q) if (ppath[q] == ppre) { pi = q; break; }
+    const int sl = base + i;
+    tr.token[tb + sl] = item_base + codebook * lvl0 + code;
+    tr.parent[tb + sl] = pslot[pi];
+    tr.depth[tb + sl] = lvl0 + 1;
+    tr.q_score[tb + sl] = key_score(k);
+    tr.tpath[tb + sl] = path;
+    tr.ttrie[tb + sl] = trie_child(trie, ptrie[pi], code);
+  }
+  __syncthreads();
+  if (tid == 0) {
+    tr.n_nodes[u] = base + ns;
+    lvl_lo[u] = base;
+    lvl_hi[u] = base + ns;
+  }
+}
+
+// ---------------------------------------------------------------- strict verify
+// Algorithm 1 per user, on target log-probs by tree slot (lpt) and at the root.
+__global__ void __launch_bounds__(256)
+verify_strict_kernel(StateDev s, TreeDev tr, TrieDev trie, const float* lpt, const float* roott, int nitem,
+                     int codebook, int L, unsigned long long* keys_all, int max_cand, int* accepted_out,
+                     int* t_after_out) {
+  __shared__ SelShared sh;
+  __shared__ uint32_t ppath[kMaxPar];
+  __shared__ float pscore[kMaxPar];
+  __shared__ int ptrie[kMaxPar], pslot[kMaxPar];
+  __shared__ const float* plp[kMaxPar];
+  __shared__ unsigned long long sel[2 * kMaxSel];
+  __shared__ int ok_s, stop_s, npar_s;
+  const int u = blockIdx.x, tid = threadIdx.x;
+  const int t = s.t[u];
+  const int K = s.K;
+  if (t >= L) {
+    if (tid == 0) { if (accepted_out) accepted_out[u] = -1; if (t_after_out) t_after_out[u] = t; }
+    return;
+  }
+  const size_t tb = (size_t)u * tr.max_nodes;
+  const int J = min(s.gamma, L - t);
+  int npar = t == 0 ? 1 : s.nb[u];
+  for (int i = tid; i < npar; i += blockDim.x) {
+    if (t == 0) { ppath[i] = 0; pscore[i] = 0.f; ptrie[i] = 0; pslot[i] = -1; plp[i] = roott + (size_t)u * nitem; }
+    else {
+      const int sl = s.beam_slot[u * K + i];
+      ppath[i] = s.path[u * K + i]; pscore[i] = s.score[u * K + i]; ptrie[i] = s.trie[u * K + i];
+      pslot[i] = sl; plp[i] = lpt + (tb + sl) * nitem;
+    }
+  }
+  if (tid == 0) stop_s = 0;
+  __syncthreads();
+  unsigned long long* keys = keys_all + (size_t)u * max_cand;
+  int accepted = 0, t_after = t;
+  const int ntree = tr.n_nodes[u];
+  for (int j = 1; j <= J + 1; ++j) {
+    const int lvl0 = t + j - 1;        // 0-based level of the codes chosen now
+    if (lvl0 >= L) break;
+    const bool bonus = (j == J + 1);   // every drafted level accepted, item not complete
+    const int n = gen_candidates(trie, npar, ppath, pscore, ptrie, plp, lvl0, codebook, keys, sh);
+    const int ns = select_smallest(keys, n, K, sel, sh);
+    // T_j and its membership in the drafted level t+j
+    if (tid == 0) ok_s = 1;
+    __syncthreads();
+    uint32_t mypath = 0; float myscore = 0.f; int mytrie = -1, myslot = -1;
+    if (tid < ns) {
+      const unsigned long long k = sel[tid];
+      mypath = (uint32_t)k;
+      myscore = key_score(k);
+      const int code = path_code(mypath, lvl0);
+      const uint32_t ppre = lvl0 == 0 ? 0u : (mypath & ~(0xFFFFFFFFu >> (8 * lvl0)));
+      int pi = 0;
+      for (int q = 0; q < npar; ++q) if (ppath[q] == ppre) { pi = q; break; }
+      mytrie = trie_child(trie, ptrie[pi], code);
+      if (!bonus) {
+        for (int i = 0; i < ntree; ++i)
+          if (tr.depth[tb + i] == lvl0 + 1 && tr.tpath[tb + i] == mypath) { myslot = i; break; }
+        if (myslot < 0) atomicAnd(&ok_s, 0);
+      }
+    }
+    __syncthreads();
+    const int ok = ok_s;
+    if (tid < ns) {
+      ppath[tid] = mypath; pscore[tid] = myscore; ptrie[tid] = mytrie; pslot[tid] = myslot;
+      plp[tid] = myslot >= 0 ? lpt + (tb + myslot) * nitem : nullptr;
+    }
+    npar = ns;
+    __syncthreads();
+    if (bonus) { accepted = J; t_after = lvl0 + 1; break; }
+    if (lvl0 + 1 == L) { accepted = ok ? j : j - 1; t_after = L; break; }
+    if (!ok) { accepted = j - 1; t_after = lvl0 + 1; break; }
+  }
+  // new state: T (ppath, pscore, ptrie)
+  for (int i = tid; i < npar; i += blockDim.x) {
+    s.path[u * K + i] = ppath[i];
+    s.score[u * K + i] = pscore[i];
+    s.trie[u * K + i] = ptrie[i];
+  }
+  if (tid == 0) {
+    s.nb[u] = npar;
+    s.t[u] = t_after;
+    s.steps[u] += 1;
+    if (accepted_out) accepted_out[u] = accepted;
+    if (t_after_out) t_after_out[u] = t_after;
+  }
+}
+
+// ---------------------------------------------------------------- launchers
+void launch_tree_from_beams(const StateDev& s, const TreeDev& tr, const TrieDev& trie, int B, int item_base,
+                            int codebook, int L, hipStream_t st) {
+  hipLaunchKernelGGL(tree_from_beams_kernel, dim3(B), dim3(64), 0, st, s, tr, trie, item_base, codebook, L);
+}
+void launch_tree_index(const TreeDev& tr, const TrieDev& trie, const StateDev& s, int B, int item_base, int codebook,
+                       int L, int* err, hipStream_t st) {
+  hipLaunchKernelGGL(tree_index_kernel, dim3(B), dim3(256), 0, st, tr, trie, s, item_base, codebook, L, err);
+  hipLaunchKernelGGL(find_beam_slots_kernel, dim3(B), dim3(64), 0, st, tr, s, L, err);
+}
+void launch_plan_tree(const TreeDev& tr, const int* lo, const int* hi, int B, int P, const Rows& rows, hipStream_t st) {
+  hipLaunchKernelGGL(plan_tree_rows_kernel, dim3(1), dim3(1024), 0, st, tr, lo, hi, B, P, rows);
+}
+void launch_plan_prefix(const int* prefix, int B, int P, const Rows& rows, hipStream_t st) {
+  int blocks = std::max(1, std::min(1024, (B * P + 255) / 256));
+  hipLaunchKernelGGL(plan_prefix_rows_kernel, dim3(blocks), dim3(256), 0, st, prefix, B, P, rows);
+}
+void launch_draft_beam_scores(const StateDev& s, const TreeDev& tr, const float* lpq, const float* rootq, int nitem,
+                              int codebook, int L, int B, hipStream_t st) {
+  hipLaunchKernelGGL(draft_beam_scores_kernel, dim3(B), dim3(64), 0, st, s, tr, lpq, rootq, nitem, codebook, L);
+}
+void launch_draft_select(const StateDev& s, const TreeDev& tr, const TrieDev& trie, const float* lpq,
+                         const float* rootq, int nitem, int item_base, int codebook, int L, int j, int N, int* lvl_lo,
+                         int* lvl_hi, unsigned long long* keys, int max_cand, int B, hipStream_t st) {
+  hipLaunchKernelGGL(draft_select_kernel, dim3(B), dim3(256), 0, st, s, tr, trie, lpq, rootq, nitem, item_base,
+                     codebook, L, j, N, lvl_lo, lvl_hi, keys, max_cand);
+}
+void launch_verify_strict(const StateDev& s, const TreeDev& tr, const TrieDev& trie, const float* lpt,
+                          const float* roott, int nitem, int codebook, int L, unsigned long long* keys, int max_cand,
+                          int* accepted, int* t_after, int B, hipStream_t st) {
+  hipLaunchKernelGGL(verify_strict_kernel, dim3(B), dim3(256), 0, st, s, tr, trie, lpt, roott, nitem, codebook, L,
+                     keys, max_cand, accepted, t_after);
+}
+
+}  // namespace atspeed
