@@ -1,0 +1,307 @@
+#!/usr/bin/env python3
+"""Throughput of the AtSpeed verify step on one MI355X.
+
+Workload (default): the LLaMA-7B-shaped target (32 layers, d 4096, 32 heads,
+FFN 11008, vocabulary 33,024 with 1,024 item tokens), 4-layer draft, 100,000
+random 4-token items, 32 users with 144-token prefixes, K = 10, N = 20,
+gamma = 4, strict verification; random-init bf16 weights N(0, 0.02).
+
+A step is one ``atspeed_verify`` over the batch: tree planning, one target
+forward over the t = 0 tree (drafted depths 1..3 forwarded, 60 nodes per user),
+item log-softmax, cumulative log-probs, trie-constrained TopK and strict
+acceptance.  The tree is the replay-all-accept tree (every drafted level holds
+the target's TopK, padded to N with other valid extensions), so each step
+completes the top-K lists of all users: value = users x steps / time.  Random
+weights make natural acceptance ~0, so the end-to-end decode (prefill + draft +
+verify until complete, natural acceptance) is reported beside it.
+
+Prints ONE JSON line.  Progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def log(msg):
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+def catalog_children(cat):
+    """prefix (tuple of codes) -> sorted codes that extend it within the catalog."""
+    kids = {}
+    for row in cat.tolist():
+        for l in range(len(row)):
+            kids.setdefault(tuple(row[:l]), set()).add(row[l])
+    return {k: sorted(v) for k, v in kids.items()}
+
+
+def upload_tree(eng, trees, B):
+    """Write per-user path lists into the context's tree (level-ordered, deduplicated)."""
+    import numpy as np
+    import torch
+    w = eng.w
+    T = eng.max_nodes
+    n = np.zeros(B, np.int32)
+    tok = np.zeros((B, T), np.int32)
+    par = np.full((B, T), -1, np.int32)
+    dep = np.zeros((B, T), np.int32)
+    for u, paths in enumerate(trees):
+        order = {}
+        for p in paths:
+            for d in range(1, len(p) + 1):
+                order.setdefault(tuple(p[:d]), len(order))
+        nodes = sorted(order, key=lambda q: (len(q), order[q]))
+        index = {q: i for i, q in enumerate(nodes)}
+        n[u] = len(nodes)
+        for i, q in enumerate(nodes):
+            tok[u, i] = w.target.item_base + w.codebook * (len(q) - 1) + q[-1]
+            par[u, i] = index[q[:-1]] if len(q) > 1 else -1
+            dep[u, i] = len(q)
+    tn, tt, tp, td, tq = eng.tree_tensors(B)
+    tn.copy_(torch.from_numpy(n))
+    tt.copy_(torch.from_numpy(tok))
+    tp.copy_(torch.from_numpy(par))
+    td.copy_(torch.from_numpy(dep))
+    tq.zero_()
+
+
+def replay_all_accept_tree(eng, kids, w, levels):
+    """Per user: drafted level j = the target's TopK of level j, padded to N with
+    other valid extensions of the drafted level j-1 (in slot and code order)."""
+    B = w.batch
+    trees = []
+    for u in range(B):
+        nodes = []
+        prev = [()]
+        for j, (t, nb, paths, _) in enumerate(levels):
+            top = [tuple(int(c) for c in paths[u, k, :j + 1]) for k in range(nb[u])]
+            lvl = list(top)
+            seen = set(top)
+            for p in prev:
+                if len(lvl) >= w.N:
+                    break
+                for c in kids.get(p, []):
+                    q = p + (c,)
+                    if q not in seen:
+                        lvl.append(q)
+                        seen.add(q)
+                        if len(lvl) >= w.N:
+                            break
+            nodes.extend(lvl)
+            prev = lvl
+        trees.append(nodes)
+    return trees
+
+
+def gpu_target_beam_search(eng, w, prefix, upload_tree):
+    """GPU target-only beam search: verify on trees holding only the Y_t paths."""
+    eng.atspeed_prefill(prefix)
+    levels = []
+    for _ in range(w.L):
+        t, nb, paths, sc = eng.atspeed_get_state(w.batch)
+        trees = [[tuple(int(c) for c in paths[u, k, :t[u]]) for k in range(nb[u])] if t[u] > 0 else []
+                 for u in range(w.batch)]
+        upload_tree(eng, trees, w.batch)
+        eng.atspeed_verify()
+        levels.append(eng.atspeed_get_state(w.batch))
+    return levels
+
+
+def cpu_baseline(w, tw, pre, cat, tree_paths):
+    """The oracle's verify step for one user of the same workload (fp64, per-path forwards)."""
+    import numpy as np
+    from oracle.model import Decoder
+    from oracle.search import model_scorer, verify_strict
+    from oracle.trie import Trie
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    trie = Trie(cat)
+    dec = Decoder(w.target, tw, w.dtype, cache_f64=False)
+    log("cpu baseline: oracle prefill of user 0 (untimed set-up)")
+    cache = dec.prefill(pre[0])
+    lp = model_scorer(dec, cache, w.target.item_base, w.codebook)
+    D = [[p for p in tree_paths if len(p) == d] for d in range(1, w.L + 1)]
+    fwd = [p for lvl in D[:-1] for p in lvl]
+    log("cpu baseline: oracle verify of user 0 (timed)")
+    t0 = time.perf_counter()
+    lp(fwd)                        # logits of every forwarded tree node (one causal forward per path)
+    res = verify_strict(lp, trie, [((), 0.0)], D, w.K, w.L, w.codebook)
+    dt = time.perf_counter() - t0
+    return dict(value=1.0 / dt, unit="lists/s", cores=int(threads), kind="oracle",
+                sample=f"verify step of 1 of {w.batch} users (t=0 replay tree, {len(fwd)} forwarded nodes: "
+                       f"per-path fp64 forwards of all of them + Algorithm 1), {dt:.1f} s; "
+                       f"accepted={res.accepted}, host cpus={os.cpu_count()}"), res
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="b7")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-e2e", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="also run one plain device copy of this size (HBM counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: the verify path has no multi-GPU mode "
+              f"(users shard across GPUs with no exchange); got --gpus {args.gpus}", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from synth import get_workload, make_catalog, make_prefixes, make_weights
+    from paper_2410_05165_amd.binding import Engine, Stats
+
+    w = get_workload(args.workload)
+    dev = torch.device("cuda:0")
+    t0 = time.time()
+    cat = make_catalog(w)
+    pre = make_prefixes(w, cat)
+    log(f"catalog {cat.shape}, prefixes {pre.shape} ({time.time() - t0:.1f}s)")
+    tw = make_weights(w, "target")
+    log(f"target weights {sum(a.nbytes for a in tw.values()) / 2**30:.1f} GiB ({time.time() - t0:.1f}s)")
+    dw = make_weights(w, "draft")
+    eng = Engine(w, tw, dw, cat)
+    log(f"engine ready, workspace {eng.ws.numel() / 2**30:.2f} GiB ({time.time() - t0:.1f}s)")
+    kids = catalog_children(cat)
+    prefix = torch.from_numpy(pre).to(dev)
+    B, K, L = w.batch, w.K, w.L
+
+    # ---- end-to-end decode (natural acceptance)
+    e2e = None
+    if not args.no_e2e:
+        items = torch.zeros((B, K, L), dtype=torch.int32, device=dev)
+        scores = torch.zeros((B, K), dtype=torch.float32, device=dev)
+        n = torch.zeros(B, dtype=torch.int32, device=dev)
+        st = Stats()
+        eng.atspeed_decode_topk(prefix, items, scores, n, None)
+        torch.cuda.synchronize()
+        reps, tt = 3, []
+        for _ in range(reps):
+            torch.cuda.synchronize()
+            a = time.perf_counter()
+            eng.atspeed_decode_topk(prefix, items, scores, n, st)
+            torch.cuda.synchronize()
+            tt.append(time.perf_counter() - a)
+        e2e = dict(lists_per_s=B / float(np.median(tt)), ms_per_decode=1e3 * float(np.median(tt)),
+                   steps=int(st.n_steps), ms_prefill=st.ms_prefill, ms_draft=st.ms_draft, ms_verify=st.ms_verify,
+                   lists_per_s_decode_only=B / ((st.ms_draft + st.ms_verify) / 1e3), profile="natural")
+        log(f"e2e decode: {e2e['ms_per_decode']:.1f} ms ({e2e['lists_per_s']:.0f} lists/s), steps {st.n_steps}")
+
+    # ---- replay-all-accept tree from the GPU's own target beam search
+    levels = gpu_target_beam_search(eng, w, prefix, upload_tree)
+    trees = replay_all_accept_tree(eng, kids, w, levels)
+    final = levels[-1]
+    eng.atspeed_prefill(prefix)
+    upload_tree(eng, trees, B)
+    n_fwd = sum(sum(1 for p in t if len(p) < L) for t in trees)
+    root_state = (np.zeros(B, np.int32), np.ones(B, np.int32), np.zeros((B, K, L), np.int32),
+                  np.zeros((B, K), np.float32))
+    acc = torch.zeros(B, dtype=torch.int32, device=dev)
+    tafter = torch.zeros(B, dtype=torch.int32, device=dev)
+
+    def step():
+        eng.atspeed_set_state(*root_state)
+        eng.atspeed_verify(acc, tafter)
+
+    step()
+    t_, nb_, paths_, sc_ = eng.atspeed_get_state(B)
+    assert (acc.cpu().numpy() == L).all() and (t_ == L).all(), "replay tree is not all-accept"
+    assert (paths_ == final[2]).all() and (sc_ == final[3]).all(), "verify differs from target beam search"
+    log(f"replay tree: {n_fwd} forwarded nodes ({n_fwd // B}/user), all levels accepted")
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    eng.atspeed_set_timing(True)
+    torch.cuda.synchronize()
+    a = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - a
+    kt = eng.atspeed_get_timing()
+    eng.atspeed_set_timing(False)
+    ms_step = 1e3 * elapsed / args.steps
+    value = B * args.steps / elapsed
+    log(f"verify step {ms_step:.2f} ms -> {value:.0f} lists/s")
+
+    # ---- roofline of the dominant kernel (gate/up GEMM) and of the other classes
+    M, d, f, H = n_fwd, w.target.d_model, w.target.d_ffn, w.target.n_heads
+    P, nl = w.prefix_len, w.target.n_layers
+    flops = {"qkv": 2 * M * d * 3 * d, "o": 2 * M * d * d, "gu": 2 * M * d * 2 * f, "down": 2 * M * f * d,
+             "lm_head": 2 * M * d * w.n_item_tokens}
+    classes = {}
+    for k, (ms, nlaunch) in kt.items():
+        if nlaunch == 0:
+            continue
+        avg = ms / nlaunch
+        ent = dict(ms_per_step=ms / args.steps, launches_per_step=nlaunch / args.steps, avg_launch_ms=avg)
+        if k in flops:
+            ent["tflops"] = flops[k] / (avg * 1e-3) / 1e12
+            ent["mfma_frac"] = ent["tflops"] / PEAK_BF16_TFLOPS
+        if k == "attention":
+            kv = B * P * 2 * d * 2                      # prefix K and V of every user, read once
+            tree = M * d * 2 * 4                        # q, tree k/v and output rows (bf16)
+            ent["gbs"] = (kv + tree) / (avg * 1e-3) / 1e9
+            ent["hbm_frac"] = ent["gbs"] / PEAK_HBM_GBS
+        classes[k] = ent
+    gemm_ms = sum(kt[k][0] for k in flops) / args.steps
+    gemm_flops = nl * sum(flops[k] for k in ("qkv", "o", "gu", "down")) + flops["lm_head"]
+    gu = classes["gu"]
+    roofline = dict(bound="mfma", kernel="gemm_bf16 gate/up (SiLU*up epilogue)",
+                    achieved=round(gu["tflops"], 2), peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
+                    frac=round(gu["tflops"] / PEAK_BF16_TFLOPS, 4), traffic=None,
+                    per_launch_flops=flops["gu"], avg_launch_ms=round(gu["avg_launch_ms"], 4))
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu, _ = cpu_baseline(w, tw, pre, cat, trees[0])
+        log(f"cpu baseline: {cpu['value']:.4f} lists/s ({cpu['sample']})")
+
+    if args.copy_calibration_mib:
+        x = torch.empty(args.copy_calibration_mib * 2**20 // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        y = torch.empty_like(x)
+        torch.cuda.synchronize()
+        y.copy_(x)
+        torch.cuda.synchronize()
+        log(f"copy calibration: {args.copy_calibration_mib} MiB read + write")
+
+    out = {
+        "metric": "top-K lists/sec/GPU at 7B shape K=10; verify-step MFMA util + HBM GB/s",
+        "value": round(value, 2), "unit": "lists/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic (seeded catalog, Zipf histories, random-init N(0,0.02) weights)",
+        "config": {"workload": f"{w.name}: verify step at t=0 over the replay-all-accept tree; target 32L/4096/32h/"
+                               f"FFN 11008, V 33024 (1024 item tokens), B={B} users, P={P}, K={K}, N={w.N}, "
+                               f"gamma={w.gamma}, strict; {M} tree rows; prefill and drafting excluded",
+                   "global_batch": B, "seq_len": P, "parallelism": "none (1 GPU)"},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "kernels": classes,
+        "verify_gemm": dict(tflops=gemm_flops / (gemm_ms * 1e-3) / 1e12,
+                            mfma_frac=gemm_flops / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+                            ms_per_step=gemm_ms),
+        "e2e_decode": e2e,
+    }
+    print(json.dumps(out), flush=True)
+    eng.close()
+
+
+if __name__ == "__main__":
+    main()

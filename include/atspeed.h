@@ -121,6 +121,26 @@ typedef struct {
   double ms_prefill, ms_draft, ms_verify;  /* stream time per stage (HIP events) */
 } atspeed_stats;
 
+/* Kernel classes timed by atspeed_get_timing. */
+enum {
+  ATSPEED_K_QKV = 0,     /* q/k/v projection + rotary + KV scatter (bf16 MFMA GEMM) */
+  ATSPEED_K_O = 1,       /* attention output projection + residual                  */
+  ATSPEED_K_GU = 2,      /* gate/up projection + SiLU * up                           */
+  ATSPEED_K_DOWN = 3,    /* down projection + residual                               */
+  ATSPEED_K_LMHEAD = 4,  /* item rows of the output head                             */
+  ATSPEED_K_ATTN = 5,    /* tree / prefill attention                                 */
+  ATSPEED_K_ROW = 6,     /* embedding, RMSNorm, log-softmax                          */
+  ATSPEED_K_SELECT = 7,  /* tree planning, TopK selection, acceptance                */
+  ATSPEED_K_COUNT = 8
+};
+
+/* Stream time per kernel class, from HIP events recorded between consecutive
+ * launches on the context's stream while timing is enabled. */
+typedef struct {
+  double ms[ATSPEED_K_COUNT];
+  int64_t launches[ATSPEED_K_COUNT];
+} atspeed_kernel_times;
+
 typedef struct atspeed_ctx atspeed_ctx;
 
 /* Bytes of device workspace a context needs for this configuration and catalog. */
@@ -190,6 +210,13 @@ ATSPEED_API atspeed_status atspeed_get_state(atspeed_ctx* ctx, int32_t B, int32_
                                  int32_t* paths, float* scores);
 ATSPEED_API atspeed_status atspeed_set_state(atspeed_ctx* ctx, int32_t B, const int32_t* t, const int32_t* nbeams,
                                  const int32_t* paths, const float* scores);
+
+/* Kernel timing (instrumentation for measurement).  enable != 0 starts recording
+ * one HIP event before every launch (and one after the last) on the context's
+ * stream and clears the totals; 0 stops.  atspeed_get_timing synchronises the
+ * stream, folds the recorded intervals into out (totals since enabling). */
+ATSPEED_API atspeed_status atspeed_set_timing(atspeed_ctx* ctx, int32_t enable);
+ATSPEED_API atspeed_status atspeed_get_timing(atspeed_ctx* ctx, atspeed_kernel_times* out);
 
 #ifdef __cplusplus
 }

@@ -21,7 +21,9 @@ STATUS = {0: "OK", 1: "E_INVALID", 2: "E_SHAPE", 3: "E_WORKSPACE", 4: "E_DEVICE"
 LAYER_ORDER = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down")
 SYMBOLS = ("atspeed_workspace_bytes", "atspeed_create", "atspeed_destroy", "atspeed_last_error",
            "atspeed_prefill", "atspeed_draft", "atspeed_get_tree", "atspeed_verify", "atspeed_tree_logits",
-           "atspeed_accept", "atspeed_decode_topk", "atspeed_get_state", "atspeed_set_state")
+           "atspeed_accept", "atspeed_decode_topk", "atspeed_get_state", "atspeed_set_state",
+           "atspeed_set_timing", "atspeed_get_timing")
+KERNEL_CLASSES = ("qkv", "o", "gu", "down", "lm_head", "attention", "row", "select")
 
 
 class Dims(C.Structure):
@@ -55,6 +57,10 @@ class Stats(C.Structure):
                 ("ms_prefill", C.c_double), ("ms_draft", C.c_double), ("ms_verify", C.c_double)]
 
 
+class KernelTimes(C.Structure):
+    _fields_ = [("ms", C.c_double * 8), ("launches", C.c_int64 * 8)]
+
+
 class AtspeedError(RuntimeError):
     def __init__(self, status: int, msg: str):
         super().__init__(f"{STATUS.get(status, status)}: {msg}")
@@ -83,6 +89,8 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
                                       C.POINTER(C.c_float)]
     lib.atspeed_set_state.argtypes = [vp, i32, C.POINTER(C.c_int32), C.POINTER(C.c_int32), C.POINTER(C.c_int32),
                                       C.POINTER(C.c_float)]
+    lib.atspeed_set_timing.argtypes = [vp, i32]
+    lib.atspeed_get_timing.argtypes = [vp, C.POINTER(KernelTimes)]
     for name in SYMBOLS:
         fn = getattr(lib, name)
         if fn.restype is C.c_int:  # default
@@ -228,6 +236,14 @@ class Engine:
         scores = np.ascontiguousarray(scores, np.float32)
         self._check(self.lib.atspeed_set_state(self.ctx, len(t), _np_ptr(t, C.c_int32), _np_ptr(nb, C.c_int32),
                                                _np_ptr(paths, C.c_int32), _np_ptr(scores, C.c_float)))
+
+    def atspeed_set_timing(self, enable: bool):
+        self._check(self.lib.atspeed_set_timing(self.ctx, 1 if enable else 0))
+
+    def atspeed_get_timing(self) -> Dict[str, tuple]:
+        kt = KernelTimes()
+        self._check(self.lib.atspeed_get_timing(self.ctx, C.byref(kt)))
+        return {k: (kt.ms[i], kt.launches[i]) for i, k in enumerate(KERNEL_CLASSES)}
 
     # -- tree upload / download (device SoA of the context)
     def tree_tensors(self, B: int):

@@ -114,11 +114,55 @@ struct atspeed_ctx {
   int B = 0, P = 0;
   bool prefilled = false;
   bool drafted = false;
+  // timing instrumentation
+  bool timing = false;
+  std::vector<hipEvent_t> ev_pool;
+  std::vector<int> ev_kind;   // kind of the interval that starts at event i (-1: end marker)
+  size_t ev_used = 0;
+  double t_ms[ATSPEED_K_COUNT] = {};
+  int64_t t_n[ATSPEED_K_COUNT] = {};
+  ~atspeed_ctx() {
+    for (hipEvent_t e : ev_pool) hipEventDestroy(e);
+  }
 };
 
 namespace {
 
 size_t esize(const atspeed_ctx& c) { return c.bf16 ? 2 : 4; }
+
+// Marks the start of a launch of class `kind` (or, with kind -1, the end of the
+// previous one) when timing is on.
+hipError_t mark(atspeed_ctx& c, int kind) {
+  if (!c.timing) return hipSuccess;
+  if (c.ev_used == c.ev_pool.size()) {
+    hipEvent_t e;
+    hipError_t err = hipEventCreate(&e);
+    if (err != hipSuccess) return err;
+    c.ev_pool.push_back(e);
+    c.ev_kind.push_back(-1);
+  }
+  c.ev_kind[c.ev_used] = kind;
+  return hipEventRecord(c.ev_pool[c.ev_used++], c.st);
+}
+
+hipError_t fold_timing(atspeed_ctx& c) {
+  if (c.ev_used == 0) return hipSuccess;
+  hipError_t err = hipEventSynchronize(c.ev_pool[c.ev_used - 1]);
+  if (err != hipSuccess) return err;
+  for (size_t i = 0; i + 1 < c.ev_used; ++i) {
+    const int k = c.ev_kind[i];
+    if (k < 0) continue;
+    float ms = 0.f;
+    err = hipEventElapsedTime(&ms, c.ev_pool[i], c.ev_pool[i + 1]);
+    if (err != hipSuccess) return err;
+    c.t_ms[k] += ms;
+    c.t_n[k] += 1;
+  }
+  c.ev_used = 0;
+  return hipSuccess;
+}
+
+#define MARK(kind) HIP_TRY(mark(c, kind))
 
 atspeed_status check_dims(const atspeed_model_dims& m, const atspeed_config& c, const char* who) {
   std::string w(who);
@@ -331,9 +375,11 @@ atspeed_status forward(atspeed_ctx& c, ModelRt& r, bool prefill, int Mmax, int T
   const int B = c.B, P = c.P;
   const size_t es = esize(c);
   hipStream_t st = c.st;
+  MARK(ATSPEED_K_ROW);
   HIP_TRY(embed(c.bf16, r.emb, c.rows, Mmax, d, c.x, st));
   for (int l = 0; l < m.n_layers; ++l) {
     const void* const* w = &r.layers[(size_t)l * 9];
+    MARK(ATSPEED_K_ROW);
     HIP_TRY(rmsnorm(c.bf16, c.x, c.rows.M, Mmax, d, (const float*)w[0], c.xn, nullptr, st));
     GemmCall g{};
     g.bf16 = c.bf16;
@@ -349,31 +395,41 @@ atspeed_status forward(atspeed_ctx& c, ModelRt& r, bool prefill, int Mmax, int T
     g.kv_mode = prefill ? 0 : 1;
     g.kdst = prefill ? (void*)pk : (void*)tk;
     g.vdst = prefill ? (void*)pv : (void*)tv;
+    MARK(ATSPEED_K_QKV);
     HIP_TRY(gemm(g, st));
     AttnCall at{};
     at.bf16 = c.bf16; at.q = c.q; at.pk = pk; at.pv = pv;
     at.tk = prefill ? nullptr : tk; at.tv = prefill ? nullptr : tv;
     at.out = c.ao; at.rows = c.rows; at.Mmax = Mmax; at.B = B; at.Tq = Tq;
     at.H = H; at.dh = dh; at.d = d; at.Pmax = c.cfg.max_prefix;
+    MARK(ATSPEED_K_ATTN);
     HIP_TRY(attention(at, st));
     g.kind = GEMM_RESID; g.A = c.ao; g.lda = d; g.N = d; g.K = d; g.w0 = w[4]; g.out = c.x; g.ldo = d;
+    MARK(ATSPEED_K_O);
     HIP_TRY(gemm(g, st));
+    MARK(ATSPEED_K_ROW);
     HIP_TRY(rmsnorm(c.bf16, c.x, c.rows.M, Mmax, d, (const float*)w[5], c.xn, nullptr, st));
     g.kind = GEMM_GU; g.A = c.xn; g.lda = d; g.N = 2 * f; g.K = d; g.w0 = w[6]; g.w1 = w[7]; g.split = f; g.hout = c.h;
+    MARK(ATSPEED_K_GU);
     HIP_TRY(gemm(g, st));
     g.kind = GEMM_RESID; g.A = c.h; g.lda = f; g.N = d; g.K = f; g.w0 = w[8]; g.out = c.x; g.ldo = d;
+    MARK(ATSPEED_K_DOWN);
     HIP_TRY(gemm(g, st));
   }
   // final norm + item rows of the output head + log-softmax
   const int* Mfin = prefill ? c.Mb : c.rows.M;
   const int Mmf = prefill ? B : Mmax;
+  MARK(ATSPEED_K_ROW);
   HIP_TRY(rmsnorm(c.bf16, c.x, Mfin, Mmf, d, r.final_norm, c.xn, prefill ? c.row_last : nullptr, st));
   GemmCall g{};
   g.kind = GEMM_STORE; g.bf16 = c.bf16; g.A = c.xn; g.lda = d; g.Mmax = Mmf; g.Mdev = Mfin;
   g.N = c.nitem; g.K = d; g.w0 = r.lm_head; g.out = c.logits; g.ldo = c.nitem; g.scratch = c.scratch;
+  MARK(ATSPEED_K_LMHEAD);
   HIP_TRY(gemm(g, st));
+  MARK(ATSPEED_K_ROW);
   if (prefill) HIP_TRY(log_softmax_rows(c.logits, c.Mb, B, c.nitem, nullptr, r.root, dbg, st));
   else HIP_TRY(log_softmax_rows(c.logits, c.rows.M, Mmax, c.nitem, c.rows.slot, r.lp, dbg, st));
+  MARK(-1);
   return ATSPEED_OK;
 }
 
@@ -388,9 +444,10 @@ TreeDev tree_view(atspeed_ctx& c) { return c.tree; }
 
 atspeed_status tree_forward(atspeed_ctx& c, float* dbg_logits) {
   HIP_TRY(hipMemsetAsync(c.err, 0, sizeof(int), c.st));
+  HIP_TRY(hipMemsetAsync(c.lo, 0, sizeof(int) * c.B, c.st));
+  MARK(ATSPEED_K_SELECT);
   launch_tree_index(c.tree, c.trie, c.state, c.B, c.cfg.target.item_base, c.cfg.codebook, c.cfg.L, c.err, c.st);
   HIP_TRY(hipGetLastError());
-  HIP_TRY(hipMemsetAsync(c.lo, 0, sizeof(int) * c.B, c.st));
   launch_plan_tree(c.tree, c.lo, c.state.nfwd, c.B, c.P, c.rows, c.st);
   HIP_TRY(hipGetLastError());
   ST_TRY(forward(c, c.tgt, false, c.B * c.Tmax, c.Tmax, dbg_logits));
@@ -542,9 +599,11 @@ atspeed_status atspeed_tree_logits(atspeed_ctx* c, float* logits) {
 static atspeed_status accept_on(atspeed_ctx* c, const float* lpt, const float* roott, int32_t* accepted,
                                 int32_t* t_after) {
   const atspeed_config& cf = c->cfg;
+  HIP_TRY(mark(*c, ATSPEED_K_SELECT));
   launch_verify_strict(c->state, c->tree, c->trie, lpt, roott, c->nitem, cf.codebook, cf.L, c->keys, c->max_cand,
                        accepted ? accepted : c->acc_tmp, t_after ? t_after : c->tafter_tmp, c->B, c->st);
   HIP_TRY(hipGetLastError());
+  HIP_TRY(mark(*c, -1));
   return ATSPEED_OK;
 }
 
@@ -683,6 +742,21 @@ atspeed_status atspeed_decode_topk(atspeed_ctx* c, int32_t B, int32_t P, const i
   HIP_TRY(hipMemcpyAsync(scores, sc.data(), sc.size() * 4, hipMemcpyHostToDevice, c->st));
   HIP_TRY(hipMemcpyAsync(n_items, nb.data(), B * 4, hipMemcpyHostToDevice, c->st));
   HIP_TRY(hipStreamSynchronize(c->st));
+  return ATSPEED_OK;
+}
+
+atspeed_status atspeed_set_timing(atspeed_ctx* c, int32_t enable) {
+  if (!c) return fail(ATSPEED_E_INVALID, "ctx is null");
+  HIP_TRY(fold_timing(*c));
+  c->timing = enable != 0;
+  for (int k = 0; k < ATSPEED_K_COUNT; ++k) { c->t_ms[k] = 0; c->t_n[k] = 0; }
+  return ATSPEED_OK;
+}
+
+atspeed_status atspeed_get_timing(atspeed_ctx* c, atspeed_kernel_times* out) {
+  if (!c || !out) return fail(ATSPEED_E_INVALID, "null argument");
+  HIP_TRY(fold_timing(*c));
+  for (int k = 0; k < ATSPEED_K_COUNT; ++k) { out->ms[k] = c->t_ms[k]; out->launches[k] = c->t_n[k]; }
   return ATSPEED_OK;
 }
 
