@@ -208,6 +208,205 @@ attn_kernel(const T* __restrict__ q, const T* __restrict__ pk, const T* __restri
   }
 }
 
+// ---------------------------------------------------------------- bf16 MFMA kernel
+// Per workgroup: (user, head, 64 query rows); wave w owns queries 16w..16w+15.
+// S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (A = K rows from LDS, B = Q from
+// registers): lane l holds S^T[key 4g+i][query l%16] (g = l/16) of each 16-key
+// block, so the probabilities of its query sit in registers in exactly the
+// B-operand layout of O^T = V^T P^T, with the 32 keys of a k-step ordered
+// {4g..4g+3, 16+4g..16+4g+3} on both operands.  V^T is staged transposed in LDS.
+// Each query's tree keys (ancestors and itself) follow, one dot product split
+// over the 4 lanes of the query.
+template <int DH>
+__global__ void __launch_bounds__(256)
+attn_mfma_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ pk, const bf16_t* __restrict__ pv,
+                 const bf16_t* __restrict__ tk, const bf16_t* __restrict__ tv, bf16_t* __restrict__ out, Rows rows,
+                 int H, int Pmax, float qscale) {
+  constexpr int KT = 64;          // keys per tile
+  constexpr int NKS = DH / 32;    // k-steps of S^T
+  constexpr int NDB = DH / 16;    // 16-dim blocks of O^T
+  constexpr int CPR = DH / 8;     // 16-byte chunks per K row
+  __shared__ __align__(16) bf16_t Ks[KT * DH];
+  __shared__ __align__(16) bf16_t Vt[DH * KT];
+  __shared__ int kmax_s;
+
+  const int u = blockIdx.z, h = blockIdx.y;
+  const int ubeg = rows.user_off[u], uend = rows.user_off[u + 1];
+  const int r0 = ubeg + blockIdx.x * 64;
+  if (r0 >= uend) return;
+  const int nq = min(64, uend - r0);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, ql = lane & 15;
+  const int qi = wave * 16 + ql;
+  const bool valid = qi < nq;
+  const int row = r0 + (valid ? qi : 0);
+  const int d = H * DH;
+
+  if (tid == 0) kmax_s = 0;
+  __syncthreads();
+  const int nctx = valid ? rows.nctx[row] : 0;
+  if (g == 0) atomicMax(&kmax_s, nctx);
+
+  bf16x8_t qf[NKS];
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks) {
+    if (valid) qf[ks] = *reinterpret_cast<const bf16x8_t*>(q + (size_t)row * d + h * DH + ks * 32 + g * 8);
+    else qf[ks] = bf16x8_t{};
+  }
+  f32x4_t o[NDB];
+#pragma unroll
+  for (int i = 0; i < NDB; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float m = -INFINITY, lsum = 0.f;
+  __syncthreads();
+  const int kmax = kmax_s;
+  const size_t kvbase = ((size_t)u * H + h) * Pmax * DH;
+
+  for (int k0 = 0; k0 < kmax; k0 += KT) {
+    const int nk = min(KT, kmax - k0);
+    // stage K (swizzled rows) and V^T (swizzled 4-key chunks)
+#pragma unroll
+    for (int c = tid; c < KT * CPR; c += 256) {
+      const int key = c / CPR, j = c % CPR;
+      u32x4_t kv = {0u, 0u, 0u, 0u}, vv = {0u, 0u, 0u, 0u};
+      if (key < nk) {
+        kv = *reinterpret_cast<const u32x4_t*>(pk + kvbase + (size_t)(k0 + key) * DH + j * 8);
+        vv = *reinterpret_cast<const u32x4_t*>(pv + kvbase + (size_t)(k0 + key) * DH + j * 8);
+      }
+      *reinterpret_cast<u32x4_t*>(Ks + key * DH + ((j ^ (key & (CPR - 1))) * 8)) = kv;
+      const bf16_t* ve = reinterpret_cast<const bf16_t*>(&vv);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int dim = j * 8 + e;
+        Vt[dim * KT + ((((key >> 2) ^ (dim & 15)) << 2)) + (key & 3)] = ve[e];
+      }
+    }
+    __syncthreads();
+    // S^T for 4 blocks of 16 keys
+    f32x4_t sc[4];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      sc[kb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      const int key = kb * 16 + ql;
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks) {
+        const int j = ks * 4 + g;
+        const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(Ks + key * DH + ((j ^ (key & (CPR - 1))) * 8));
+        sc[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ks], sc[kb], 0, 0, 0);
+      }
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int key = k0 + kb * 16 + g * 4 + i;
+        const float v = key < nctx ? sc[kb][i] * qscale : -INFINITY;
+        sc[kb][i] = v;
+        mx = fmaxf(mx, v);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float mnew = fmaxf(m, mx);
+    const float alpha = (m == -INFINITY) ? 0.f : exp2f(m - mnew);
+    float ps = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float p = (sc[kb][i] == -INFINITY) ? 0.f : exp2f(sc[kb][i] - mnew);
+        sc[kb][i] = p;
+        ps += p;
+      }
+    lsum = lsum * alpha + ps;
+    m = mnew;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) o[db] *= alpha;
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      bf16x8_t pf;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        pf[i] = (__bf16)sc[2 * kk][i];
+        pf[4 + i] = (__bf16)sc[2 * kk + 1][i];
+      }
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        const int dim = db * 16 + ql;
+        const int c0 = ((kk * 8 + g) ^ (dim & 15)) << 2, c1 = ((kk * 8 + 4 + g) ^ (dim & 15)) << 2;
+        const uint2 lo = *reinterpret_cast<const uint2*>(Vt + dim * KT + c0);
+        const uint2 hi = *reinterpret_cast<const uint2*>(Vt + dim * KT + c1);
+        u32x4_t w4 = {lo.x, lo.y, hi.x, hi.y};
+        bf16x8_t vf = __builtin_bit_cast(bf16x8_t, w4);
+        o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[db], 0, 0, 0);
+      }
+    }
+    __syncthreads();
+  }
+
+  if (tk != nullptr && valid) {  // tree keys: ancestors and self
+    const int na = rows.nanc[row];
+    float sa[4];
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+      float part = 0.f;
+      if (a < na) {
+        const bf16_t* kp = tk + (size_t)rows.anc[row * 4 + a] * d + h * DH;
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks) {
+          const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(kp + ks * 32 + g * 8);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) part += (float)qf[ks][e] * (float)kf[e];
+        }
+      }
+      part += __shfl_xor(part, 16);
+      part += __shfl_xor(part, 32);
+      sa[a] = a < na ? part * qscale : -INFINITY;
+    }
+    float mx = fmaxf(fmaxf(sa[0], sa[1]), fmaxf(sa[2], sa[3]));
+    const float mnew = fmaxf(m, mx);
+    const float alpha = (m == -INFINITY) ? 0.f : exp2f(m - mnew);
+    float ps = 0.f;
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+      sa[a] = a < na ? exp2f(sa[a] - mnew) : 0.f;
+      ps += sa[a];
+    }
+    lsum = lsum * alpha + (g == 0 ? ps : 0.f);
+    m = mnew;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+      o[db] *= alpha;
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        if (a < na) {
+          const bf16_t* vp = tv + (size_t)rows.anc[row * 4 + a] * d + h * DH + db * 16 + g * 4;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) o[db][i] += sa[a] * bf2f(vp[i]);
+        }
+      }
+    }
+  }
+  lsum += __shfl_xor(lsum, 16);
+  lsum += __shfl_xor(lsum, 32);
+  if (valid) {
+    const float inv = 1.f / lsum;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) out[(size_t)row * d + h * DH + db * 16 + g * 4 + i] = f2bf(o[db][i] * inv);
+  }
+}
+
+template <int DH>
+static hipError_t launch_attn_mfma(const AttnCall& a, hipStream_t st) {
+  const float qscale = 1.4426950408889634f / sqrtf((float)DH);
+  dim3 grid((a.Tq + 63) / 64, a.H, a.B);
+  hipLaunchKernelGGL(attn_mfma_kernel<DH>, grid, dim3(256), 0, st, (const bf16_t*)a.q, (const bf16_t*)a.pk,
+                     (const bf16_t*)a.pv, (const bf16_t*)a.tk, (const bf16_t*)a.tv, (bf16_t*)a.out, a.rows, a.H,
+                     a.Pmax, qscale);
+  return hipGetLastError();
+}
+
 template <class T, int DH>
 static hipError_t launch_attn(const AttnCall& a, hipStream_t st) {
   constexpr int DP = DH + 1;
@@ -228,9 +427,8 @@ static hipError_t launch_attn(const AttnCall& a, hipStream_t st) {
 
 hipError_t attention(const AttnCall& a, hipStream_t st) {
   if (a.bf16) {
-    if (a.dh == 64) return launch_attn<bf16_t, 64>(a, st);
-    if (a.dh == 128) return launch_attn<bf16_t, 128>(a, st);
-    if (a.dh == 32) return launch_attn<bf16_t, 32>(a, st);
+    if (a.dh == 64) return launch_attn_mfma<64>(a, st);
+    if (a.dh == 128) return launch_attn_mfma<128>(a, st);
   } else {
     if (a.dh == 64) return launch_attn<float, 64>(a, st);
     if (a.dh == 128) return launch_attn<float, 128>(a, st);

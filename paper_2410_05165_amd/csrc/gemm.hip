@@ -1,8 +1,8 @@
 // Dense projections of the decoder block: Y[M, N] = X[M, K] · W[N, K]^T.
 //
 // bf16 path: MFMA v_mfma_f32_32x32x16_bf16 (fp32 accumulate), block tile
-// BM x BN x 64 staged through LDS (double buffer, XOR-swizzled 16-byte chunks),
-// wave tile TM x TN blocks of 32x32.  Epilogues are fused:
+// BM x BN x 64 fetched by direct global->LDS DMA into two LDS stages
+// (XOR-swizzled 16-byte chunks), wave tile TM x TN blocks of 32x32.  Epilogues are fused:
 //   QKV   rotary embedding on q and k (rotate-half pairs sit in registers of the
 //         same lane: partner block tn ^ (d_head/64)), rounding to bf16, q to its
 //         row buffer, k/v scattered into the prefix cache or the tree KV buffer;
@@ -61,63 +61,105 @@ struct Tile {
   static constexpr int STAGE = A_BYTES + B_BYTES;
 };
 
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// One k-tile (64 columns of A and W) into an LDS stage with direct global->LDS
+// DMA (global_load_lds_dwordx4): each wave instruction fills 1 KB = 8 rows of
+// 128 B; lane i lands at byte 16*i, i.e. row i/8, physical chunk i%8, and so
+// fetches logical chunk (i%8) ^ (row & 7) -- the XOR swizzle the fragment reads
+// undo.  No VGPRs hold the tile.
+template <int NA, int NB>
+__device__ __forceinline__ void load_stage(unsigned char* stage, int wave, const bf16_t* A, const int* a_off,
+                                           const bf16_t* B0, const bf16_t* B1, const int* b_off, const bool* b_hi,
+                                           int k0, int a_bytes) {
+#pragma unroll
+  for (int j = 0; j < NA; ++j)
+    __builtin_amdgcn_global_load_lds((void*)(A + a_off[j] + k0), (lds_void_t*)(stage + (wave * NA + j) * 1024), 16, 0, 0);
+#pragma unroll
+  for (int j = 0; j < NB; ++j)
+    __builtin_amdgcn_global_load_lds((void*)((b_hi[j] ? B1 : B0) + b_off[j] + k0),
+                                     (lds_void_t*)(stage + a_bytes + (wave * NB + j) * 1024), 16, 0, 0);
+}
+
+template <int WM, int WN, int TM, int TN>
+__device__ __forceinline__ void mma_stage(const unsigned char* stage, int wave_m, int wave_n, int fr, int fc,
+                                          f32x16_t (&acc)[TM][TN], int a_bytes) {
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) {
+    bf16x8_t af[TM], bfr[TN];
+    const int ch = kk * 2 + fc;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int r = wave_m * TM * 32 + i * 32 + fr;
+      af[i] = *reinterpret_cast<const bf16x8_t*>(stage + r * 128 + ((ch ^ (r & 7)) << 4));
+    }
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int r = wave_n * TN * 32 + j * 32 + fr;
+      bfr[j] = *reinterpret_cast<const bf16x8_t*>(stage + a_bytes + r * 128 + ((ch ^ (r & 7)) << 4));
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+  }
+}
+
 template <int WM, int WN, int TM, int TN, int BMAP, int EPI>
 __global__ void __launch_bounds__(64 * WM * WN)
 gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ Mdev, int N, int K,
                  BArgs b, EpiArgs e) {
   using T = Tile<WM, WN, TM, TN>;
-  extern __shared__ __align__(16) unsigned char smem[];
+  static_assert(WM * WN == 4, "four waves");
+  constexpr int NA = T::BM / 32;   // wave instructions per stage for A (8 rows each, 4 waves)
+  constexpr int NB = T::BN / 32;
+  __shared__ __align__(1024) unsigned char st0[T::STAGE];
+  __shared__ __align__(1024) unsigned char st1[T::STAGE];
   const int M = *Mdev;
   const int tile_m = blockIdx.y, tile_n = blockIdx.x;
   const int m0 = tile_m * T::BM;
   if (m0 >= M) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wave_m = wave / WN, wave_n = wave % WN;
+  const int lrow = lane >> 3, lchunk = (lane & 7) ^ (lrow & 7);
 
-  // global -> register staging: 16-byte chunk offsets (uint4 units) from a base
-  // pointer.  A tile lies in one matrix for PLAIN/QKV (d % BN == 0 is checked on
-  // the host); for GU the chunk's block picks the gate or the up matrix.
-  const u32x4_t* a_base = reinterpret_cast<const u32x4_t*>(A);
-  int a_off[T::A_CH], b_off[T::B_CH];
-  bool b_hi[T::B_CH];
+  // per-lane element offsets of the 16-byte chunks this lane fetches
+  int a_off[NA], b_off[NB];
+  bool b_hi[NB];
 #pragma unroll
-  for (int i = 0; i < T::A_CH; ++i) {
-    int ci = tid + i * T::NT, r = ci >> 3, c = ci & 7;
+  for (int j = 0; j < NA; ++j) {
+    int r = (wave * NA + j) * 8 + lrow;
     int gr = m0 + r;
     gr = gr < M ? gr : M - 1;
-    a_off[i] = gr * (lda >> 3) + c;
+    a_off[j] = gr * lda + lchunk * 8;
   }
-  const u32x4_t* b_base0;
-  const u32x4_t* b_base1 = nullptr;
-  {
-    const int n_first = tile_n * T::BN;
-    if (BMAP == BMAP_QKV) {
-      const int which = n_first / b.split;
-      b_base0 = reinterpret_cast<const u32x4_t*>(which == 0 ? b.w0 : (which == 1 ? b.w1 : b.w2));
-    } else if (BMAP == BMAP_GU) {
-      b_base0 = reinterpret_cast<const u32x4_t*>(b.w0);
-      b_base1 = reinterpret_cast<const u32x4_t*>(b.w1);
-    } else {
-      b_base0 = reinterpret_cast<const u32x4_t*>(b.w0);
-    }
+  const bf16_t* B0;
+  const bf16_t* B1 = nullptr;
+  if (BMAP == BMAP_QKV) {
+    const int which = (tile_n * T::BN) / b.split;
+    B0 = which == 0 ? b.w0 : (which == 1 ? b.w1 : b.w2);
+  } else {
+    B0 = b.w0;
+    B1 = b.w1;
   }
 #pragma unroll
-  for (int i = 0; i < T::B_CH; ++i) {
-    int ci = tid + i * T::NT, r = ci >> 3, c = ci & 7;
+  for (int j = 0; j < NB; ++j) {
+    const int r = (wave * NB + j) * 8 + lrow;
     int row;
-    b_hi[i] = false;
+    b_hi[j] = false;
     if (BMAP == BMAP_GU) {
       constexpr int half = TN / 2;
-      int wn = r / (TN * 32), blk = (r / 32) % TN, cc = r % 32;
+      const int wn = r / (TN * 32), blk = (r / 32) % TN, cc = r % 32;
       row = tile_n * (T::BN / 2) + wn * (half * 32) + (blk % half) * 32 + cc;
       row = row < b.split ? row : b.split - 1;
-      b_hi[i] = blk >= half;
+      b_hi[j] = blk >= half;
     } else {
       row = tile_n * T::BN + r;
       row = row < N ? row : N - 1;
       if (BMAP == BMAP_QKV) row -= (tile_n * T::BN / b.split) * b.split;
     }
-    b_off[i] = row * (K >> 3) + c;
+    b_off[j] = row * K + lchunk * 8;
   }
 
   f32x16_t acc[TM][TN];
@@ -128,83 +170,37 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  u32x4_t ra[T::A_CH], rb[T::B_CH];
   const int nk = K / T::BK;
-  int adst[T::A_CH], bdst[T::B_CH];
-#pragma unroll
-  for (int i = 0; i < T::A_CH; ++i) {
-    int ci = tid + i * T::NT, r = ci >> 3, c = ci & 7;
-    adst[i] = r * 128 + ((c ^ (r & 7)) << 4);
-  }
-#pragma unroll
-  for (int i = 0; i < T::B_CH; ++i) {
-    int ci = tid + i * T::NT, r = ci >> 3, c = ci & 7;
-    bdst[i] = T::A_BYTES + r * 128 + ((c ^ (r & 7)) << 4);
-  }
-
-#pragma unroll
-  for (int i = 0; i < T::A_CH; ++i) ra[i] = a_base[a_off[i]];
-#pragma unroll
-  for (int i = 0; i < T::B_CH; ++i) rb[i] = (BMAP == BMAP_GU && b_hi[i] ? b_base1 : b_base0)[b_off[i]];
-#pragma unroll
-  for (int i = 0; i < T::A_CH; ++i) *reinterpret_cast<u32x4_t*>(smem + adst[i]) = ra[i];
-#pragma unroll
-  for (int i = 0; i < T::B_CH; ++i) *reinterpret_cast<u32x4_t*>(smem + bdst[i]) = rb[i];
-  __syncthreads();
   const int fr = lane & 31, fc = lane >> 5;
-  for (int kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) {
-      const int ko = (kt + 1) * 8;
-#pragma unroll
-      for (int i = 0; i < T::A_CH; ++i) ra[i] = a_base[a_off[i] + ko];
-#pragma unroll
-      for (int i = 0; i < T::B_CH; ++i) rb[i] = (BMAP == BMAP_GU && b_hi[i] ? b_base1 : b_base0)[b_off[i] + ko];
-    }
-    const unsigned char* base = smem + (kt & 1) * T::STAGE;
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      bf16x8_t af[TM], bfr[TN];
-      const int ch = kk * 2 + fc;
-#pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        int r = wave_m * TM * 32 + i * 32 + fr;
-        af[i] = *reinterpret_cast<const bf16x8_t*>(base + r * 128 + ((ch ^ (r & 7)) << 4));
-      }
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        int r = wave_n * TN * 32 + j * 32 + fr;
-        bfr[j] = *reinterpret_cast<const bf16x8_t*>(base + T::A_BYTES + r * 128 + ((ch ^ (r & 7)) << 4));
-      }
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-    }
-    if (kt + 1 < nk) {
-      unsigned char* nb = smem + ((kt + 1) & 1) * T::STAGE;
-#pragma unroll
-      for (int i = 0; i < T::A_CH; ++i) *reinterpret_cast<u32x4_t*>(nb + adst[i]) = ra[i];
-#pragma unroll
-      for (int i = 0; i < T::B_CH; ++i) *reinterpret_cast<u32x4_t*>(nb + bdst[i]) = rb[i];
-    }
+  load_stage<NA, NB>(st0, wave, A, a_off, B0, B1, b_off, b_hi, 0, T::A_BYTES);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  // nk is even (K % 128 == 0 is checked on the host): stages alternate st0, st1
+  for (int kt = 0; kt < nk; kt += 2) {
+    load_stage<NA, NB>(st1, wave, A, a_off, B0, B1, b_off, b_hi, (kt + 1) * 64, T::A_BYTES);
+    mma_stage<WM, WN, TM, TN>(st0, wave_m, wave_n, fr, fc, acc, T::A_BYTES);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (kt + 2 < nk) load_stage<NA, NB>(st0, wave, A, a_off, B0, B1, b_off, b_hi, (kt + 2) * 64, T::A_BYTES);
+    mma_stage<WM, WN, TM, TN>(st1, wave_m, wave_n, fr, fc, acc, T::A_BYTES);
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
   }
 
   // ---- epilogue.  acc[i][j][r] is row (r/4)*8 + (lane/32)*4 + r%4, column lane%32 of block (i, j).
   const int row0 = m0 + wave_m * TM * 32;
   const int col0 = tile_n * T::BN + wave_n * TN * 32;
-#pragma unroll
-  for (int i = 0; i < TM; ++i) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
+  static_for<TM>([&](auto I) {
+    constexpr int i = decltype(I)::value;
+    static_for<16>([&](auto R) {
+      constexpr int r = decltype(R)::value;
       const int row = row0 + i * 32 + (r >> 2) * 8 + fc * 4 + (r & 3);
-      if (row >= M) continue;
+      const bool rok = row < M;
       if (EPI == EPI_STORE || EPI == EPI_RESID) {
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
-          int col = col0 + j * 32 + fr;
-          if (col < N) {
+          const int col = col0 + j * 32 + fr;
+          if (rok && col < N) {
             float* p = e.out + (size_t)row * e.ldo + col;
             if (EPI == EPI_STORE) *p = acc[i][j][r];
             else *p += acc[i][j][r];
@@ -214,38 +210,39 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
         constexpr int half = TN / 2;
 #pragma unroll
         for (int j = 0; j < half; ++j) {
-          int fcol = tile_n * (T::BN / 2) + wave_n * (half * 32) + j * 32 + fr;
-          if (fcol < b.split)
-            e.hout[(size_t)row * b.split + fcol] = f2bf(silu(acc[i][j][r]) * acc[i][j + half][r]);
+          const int fcol = tile_n * (T::BN / 2) + wave_n * (half * 32) + j * 32 + fr;
+          const float v = silu(acc[i][j][r]) * acc[i][j + half][r];
+          if (rok && fcol < b.split) e.hout[(size_t)row * b.split + fcol] = f2bf(v);
         }
-      } else {  // EPI_QKV
-        const int pos = e.rows.pos[row];
+      } else {  // EPI_QKV: the wave's 128 columns are one head (d_head 128) or two (d_head 64)
+        const int rr = rok ? row : 0;
+        const int pos = e.rows.pos[rr];
         const int halfdh = e.dh >> 1;
-        const int pb = halfdh >> 5;  // partner block distance (1 for d_head 64, 2 for 128)
+        const bool pair1 = halfdh == 32;  // partner block j^1 (d_head 64) or j^2 (d_head 128)
+        const int which = col0 / e.d;     // the wave's columns lie in one of q, k, v
         size_t kvoff;
-        if (e.kv_mode == 0) kvoff = ((size_t)e.rows.user[row] * e.H * e.Pmax + pos) * e.dh;
-        else kvoff = (size_t)e.rows.slot[row] * e.d;
+        if (e.kv_mode == 0) kvoff = ((size_t)e.rows.user[rr] * e.H * e.Pmax + pos) * e.dh;
+        else kvoff = (size_t)e.rows.slot[rr] * e.d;
         const size_t hstride = e.kv_mode == 0 ? (size_t)e.Pmax * e.dh : (size_t)e.dh;
+        bf16_t* dst = which == 0 ? e.q + (size_t)rr * e.d : (which == 1 ? e.kdst : e.vdst) + kvoff;
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
           const int col = col0 + j * 32 + fr;
-          if (col >= N) continue;
-          const int which = col / e.d, hc = col - which * e.d;
+          const int hc = col - which * e.d;
           const int head = hc / e.dh, ii = hc - head * e.dh;
           float v = acc[i][j][r];
           if (which < 2) {
-            const float pv = pb == 1 ? acc[i][j ^ 1][r] : acc[i][j ^ 2][r];
+            const float pv = pair1 ? acc[i][j ^ 1][r] : acc[i][j ^ 2][r];
             const int fi = ii & (halfdh - 1);
             const float c = e.cosT[pos * halfdh + fi], s = e.sinT[pos * halfdh + fi];
             v = ii < halfdh ? v * c - pv * s : v * c + pv * s;
           }
-          const bf16_t o = f2bf(v);
-          if (which == 0) e.q[(size_t)row * e.d + hc] = o;
-          else (which == 1 ? e.kdst : e.vdst)[kvoff + head * hstride + ii] = o;
+          const size_t off = which == 0 ? (size_t)hc : head * hstride + ii;
+          if (rok && col < N) dst[off] = f2bf(v);
         }
       }
-    }
-  }
+    });
+  });
 }
 
 // ------------------------------------------------------------------ fp32 path
@@ -339,11 +336,12 @@ __global__ void epi_f32_kernel(const float* __restrict__ C, const int* __restric
 }
 
 // ------------------------------------------------------------------ launchers
-using TileBig = Tile<2, 2, 2, 4>;
-
-template <int BMAP, int EPI>
+// 256x256 tiles (4 waves of 128x128) for the wide projections (q/k/v, gate/up);
+// 128x256 tiles for the d_model-wide ones (o, down, output head), which keeps
+// their tile count near the CU count at a few thousand rows without split-K.
+template <int BMAP, int EPI, int TMW>
 static hipError_t launch_bf16(const GemmCall& g, hipStream_t st) {
-  using T = TileBig;
+  using T = Tile<2, 2, TMW, 4>;
   BArgs b{(const bf16_t*)g.w0, (const bf16_t*)g.w1, (const bf16_t*)g.w2, g.split};
   EpiArgs e{};
   e.out = g.out; e.ldo = g.ldo; e.hout = (bf16_t*)g.hout;
@@ -351,24 +349,18 @@ static hipError_t launch_bf16(const GemmCall& g, hipStream_t st) {
   e.cosT = g.cosT; e.sinT = g.sinT; e.rows = g.rows; e.kv_mode = g.kv_mode; e.Pmax = g.Pmax;
   e.d = g.d; e.dh = g.dh; e.H = g.H;
   dim3 grid((g.N + T::BN - 1) / T::BN, (g.Mmax + T::BM - 1) / T::BM);
-  auto kern = gemm_bf16_kernel<2, 2, 2, 4, BMAP, EPI>;
-  static bool attr = false;
-  if (!attr) {
-    hipError_t err = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, 2 * T::STAGE);
-    if (err != hipSuccess) return err;
-    attr = true;
-  }
-  hipLaunchKernelGGL(kern, grid, dim3(T::NT), 2 * T::STAGE, st, (const bf16_t*)g.A, g.lda, g.Mdev, g.N, g.K, b, e);
+  auto kern = gemm_bf16_kernel<2, 2, TMW, 4, BMAP, EPI>;
+  hipLaunchKernelGGL(kern, grid, dim3(T::NT), 0, st, (const bf16_t*)g.A, g.lda, g.Mdev, g.N, g.K, b, e);
   return hipGetLastError();
 }
 
 hipError_t gemm(const GemmCall& g, hipStream_t st) {
   if (g.bf16) {
     switch (g.kind) {
-      case GEMM_QKV: return launch_bf16<BMAP_QKV, EPI_QKV>(g, st);
-      case GEMM_GU: return launch_bf16<BMAP_GU, EPI_GU>(g, st);
-      case GEMM_RESID: return launch_bf16<BMAP_PLAIN, EPI_RESID>(g, st);
-      default: return launch_bf16<BMAP_PLAIN, EPI_STORE>(g, st);
+      case GEMM_QKV: return launch_bf16<BMAP_QKV, EPI_QKV, 4>(g, st);
+      case GEMM_GU: return launch_bf16<BMAP_GU, EPI_GU, 4>(g, st);
+      case GEMM_RESID: return launch_bf16<BMAP_PLAIN, EPI_RESID, 2>(g, st);
+      default: return launch_bf16<BMAP_PLAIN, EPI_STORE, 2>(g, st);
     }
   }
   // fp32: raw product into g.scratch (or straight into the logits), then the
