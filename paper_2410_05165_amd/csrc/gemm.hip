@@ -108,7 +108,7 @@ __device__ __forceinline__ void mma_stage(const unsigned char* stage, int wave_m
 
 template <int WM, int WN, int TM, int TN, int BMAP, int EPI>
 __global__ void __launch_bounds__(64 * WM * WN)
-gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ Mdev, int N, int K,
+gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ Mdev, int Mt, int N, int K,
                  BArgs b, EpiArgs e) {
   using T = Tile<WM, WN, TM, TN>;
   static_assert(WM * WN == 4, "four waves");
@@ -117,7 +117,15 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
   __shared__ __align__(1024) unsigned char st0[T::STAGE];
   __shared__ __align__(1024) unsigned char st1[T::STAGE];
   const int M = *Mdev;
-  const int tile_m = blockIdx.y, tile_n = blockIdx.x;
+  // XCD-aware tile order: workgroup L is dispatched to XCD L % 8; XCD x owns the
+  // contiguous range x*per .. x*per+per-1 of the tiles in N-major order, so the
+  // M-tiles that share a weight tile run together on one XCD and share its L2.
+  const int Nt = (N + T::BN - 1) / T::BN;
+  const int ntiles = Mt * Nt, per = (ntiles + 7) >> 3;
+  const int L = blockIdx.x;
+  const int t = (L & 7) * per + (L >> 3);
+  if (t >= ntiles) return;
+  const int tile_n = t / Mt, tile_m = t - tile_n * Mt;
   const int m0 = tile_m * T::BM;
   if (m0 >= M) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -348,9 +356,11 @@ static hipError_t launch_bf16(const GemmCall& g, hipStream_t st) {
   e.q = (bf16_t*)g.q; e.kdst = (bf16_t*)g.kdst; e.vdst = (bf16_t*)g.vdst;
   e.cosT = g.cosT; e.sinT = g.sinT; e.rows = g.rows; e.kv_mode = g.kv_mode; e.Pmax = g.Pmax;
   e.d = g.d; e.dh = g.dh; e.H = g.H;
-  dim3 grid((g.N + T::BN - 1) / T::BN, (g.Mmax + T::BM - 1) / T::BM);
+  const int Mt = (g.Mmax + T::BM - 1) / T::BM, Nt = (g.N + T::BN - 1) / T::BN;
+  const int per = (Mt * Nt + 7) / 8;
+  dim3 grid(8 * per);
   auto kern = gemm_bf16_kernel<2, 2, TMW, 4, BMAP, EPI>;
-  hipLaunchKernelGGL(kern, grid, dim3(T::NT), 0, st, (const bf16_t*)g.A, g.lda, g.Mdev, g.N, g.K, b, e);
+  hipLaunchKernelGGL(kern, grid, dim3(T::NT), 0, st, (const bf16_t*)g.A, g.lda, g.Mdev, Mt, g.N, g.K, b, e);
   return hipGetLastError();
 }
 
