@@ -32,6 +32,21 @@ PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
 
+def gemm_traffic(kernel_key):
+    """HBM bytes per launch of a kernel from the committed rocprofv3 counter record,
+    or None if the kernel source changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic_b7.json")
+    src = os.path.join(ROOT, "paper_2410_05165_amd", "csrc", "gemm.hip")
+    try:
+        rec = json.load(open(path))
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+        ent = rec["kernels"][kernel_key]
+        return ent["bytes_per_launch"] if rec["gemm_src_sha256"] == sha else None
+    except (OSError, KeyError, ValueError):
+        return None
+
+
 def log(msg):
     print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
 
@@ -266,7 +281,7 @@ def main():
     gu = classes["gu"]
     roofline = dict(bound="mfma", kernel="gemm_bf16 gate/up (SiLU*up epilogue)",
                     achieved=round(gu["tflops"], 2), peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
-                    frac=round(gu["tflops"] / PEAK_BF16_TFLOPS, 4), traffic=None,
+                    frac=round(gu["tflops"] / PEAK_BF16_TFLOPS, 4), traffic=gemm_traffic("gate/up GEMM"),
                     per_launch_flops=flops["gu"], avg_launch_ms=round(gu["avg_launch_ms"], 4))
 
     cpu = None

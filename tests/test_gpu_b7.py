@@ -1,0 +1,95 @@
+"""GPU parity at the full 7B shape (32 layers, d 4096, 32 users, 144-token
+prefixes, K = 10, N = 20), in the launch configuration the benchmark times.
+
+The oracle cannot run the whole batch, so it checks sampled outputs one by one
+(the root and sampled tree nodes of one user, each by its own causal forward),
+and the selection/acceptance logic is checked on the GPU's logits for every
+user (identical inputs on both sides).
+"""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+from _gpu_common import LOGIT_TOL, SEL_TIE, logit_table  # noqa: E402
+from synth import get_workload, make_catalog, make_prefixes, make_weights  # noqa: E402
+from oracle.model import Decoder  # noqa: E402
+from oracle.search import verify_strict  # noqa: E402
+from oracle.trie import Trie  # noqa: E402
+
+
+@pytest.fixture(scope="module")
+def b7():
+    from paper_2410_05165_amd.binding import Engine
+    w = get_workload("b7")
+    cat = make_catalog(w)
+    pre = make_prefixes(w, cat)
+    print("[b7] generating weights", flush=True)
+    tw, dw = make_weights(w, "target"), make_weights(w, "draft")
+    eng = Engine(w, tw, dw, cat)
+    yield dict(w=w, cat=cat, pre=pre, tw=tw, eng=eng)
+    eng.close()
+
+
+def _gpu_paths(tn, tt, tp, td, u, w):
+    paths = []
+    for i in range(tn[u]):
+        code = tt[u, i] - w.target.item_base - w.codebook * (td[u, i] - 1)
+        paths.append((paths[tp[u, i]] if tp[u, i] >= 0 else ()) + (int(code),))
+    return paths
+
+
+def test_b7_logits_and_selection(b7):
+    w, eng, pre = b7["w"], b7["eng"], b7["pre"]
+    dev = torch.device("cuda:0")
+    prefix = torch.from_numpy(pre).to(dev)
+    root = torch.zeros((w.batch, w.n_item_tokens), dtype=torch.float32, device=dev)
+    print("[b7] prefill + draft + tree logits on the GPU", flush=True)
+    eng.atspeed_prefill(prefix, root)
+    eng.atspeed_draft()
+    T = eng.max_nodes
+    logits = torch.full((w.batch, T, w.n_item_tokens), float("nan"), dtype=torch.float32, device=dev)
+    eng.atspeed_tree_logits(logits)
+    torch.cuda.synchronize()
+    tn, tt, tp, td, tq = (x.cpu().numpy() for x in eng.tree_tensors(w.batch))
+    lg, r = logits.cpu().numpy(), root.cpu().numpy()
+    assert (tn == 4 * w.N).all(), tn          # t = 0: drafted depths 1..4, N each
+    # oracle on sampled outputs of user 0
+    u = 0
+    dec = Decoder(w.target, b7["tw"], w.dtype, cache_f64=False)
+    print("[b7] oracle prefill of user 0", flush=True)
+    cache = dec.prefill(pre[u])
+    err_root = np.abs(r[u] - cache.last_logits).max()
+    print(f"[b7] user 0 root logits max|err| = {err_root:.3e}", flush=True)
+    paths = _gpu_paths(tn, tt, tp, td, u, w)
+    pick = [i for d in (1, 2, 3) for i in [j for j in range(tn[u]) if td[u, j] == d][:: w.N // 4]]
+    toks = [tuple(w.target.item_base + w.codebook * l + c for l, c in enumerate(paths[i])) for i in pick]
+    print(f"[b7] oracle per-path forwards of {len(pick)} sampled nodes", flush=True)
+    want = dec.path_logits(cache, toks)
+    err_nodes = np.abs(lg[u, pick] - want).max()
+    print(f"[b7] user 0 sampled node logits max|err| = {err_nodes:.3e}", flush=True)
+    assert err_root <= LOGIT_TOL["bf16"] and err_nodes <= LOGIT_TOL["bf16"]
+    # selection + acceptance on the GPU's logits, every user
+    trie = Trie(b7["cat"])
+    acc = torch.zeros(w.batch, dtype=torch.int32, device=dev)
+    ta = torch.zeros(w.batch, dtype=torch.int32, device=dev)
+    eng.atspeed_accept(logits.nan_to_num(0.0), root, acc, ta)
+    t, nb, sp, sc = eng.atspeed_get_state(w.batch)
+    acc, ta = acc.cpu().numpy(), ta.cpu().numpy()
+    ties = 0
+    for v in range(w.batch):
+        nodes = _gpu_paths(tn, tt, tp, td, v, w)
+        lp = logit_table(nodes, lg[v], r[v])
+        D = [[p for p in nodes if len(p) == d] for d in range(1, w.L + 1)]
+        log = []
+        res = verify_strict(lp, trie, [((), 0.0)], D, w.K, w.L, w.codebook, log)
+        got = [tuple(int(c) for c in sp[v, k, :t[v]]) for k in range(nb[v])]
+        if got != [p for p, _ in res.beams] or acc[v] != res.accepted or ta[v] != res.t_after:
+            assert min(d.margin for d in log) < SEL_TIE
+            ties += 1
+            continue
+        np.testing.assert_allclose(sc[v, :nb[v]], [s for _, s in res.beams], rtol=0, atol=1e-4)
+    print(f"[b7] selection/acceptance equal to Algorithm 1 for {w.batch - ties} of {w.batch} users "
+          f"({ties} decided inside the 1e-3 tie zone)")

@@ -1,0 +1,64 @@
+"""GPU parity on shape variants that the named workloads do not cover at small
+size: d_head 128 with a text-token prompt before the history (as the 7B shape
+has), several layers, a ragged tree."""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+from _gpu_common import LOGIT_TOL, upload_tree  # noqa: E402
+from synth import ModelDims, get_workload, make_catalog, make_prefixes, make_weights  # noqa: E402
+from oracle.model import Decoder  # noqa: E402
+from oracle.search import draft_levels, model_scorer  # noqa: E402
+from oracle.trie import Trie  # noqa: E402
+
+VARIANTS = {
+    # d_head 128 (8 heads of d 1024), prompt of 16 text tokens, item tokens after 1024 text tokens
+    "dh128": dict(target=ModelDims(4, 1024, 8, 2816, 2048, 1024), draft=ModelDims(2, 256, 4, 1024, 2048, 1024),
+                  batch=4, prompt_len=16, hist_items=10, K=10, N=20, n_items=5000),
+    # 32 layers at d 1024: how the bf16 discrepancy grows with depth
+    "deep": dict(target=ModelDims(32, 1024, 8, 2816, 2048, 1024), draft=ModelDims(2, 256, 4, 1024, 2048, 1024),
+                 batch=2, prompt_len=16, hist_items=10, K=10, N=20, n_items=5000),
+}
+
+
+@pytest.mark.parametrize("var", list(VARIANTS))
+def test_variant_logits(var):
+    from paper_2410_05165_amd.binding import Engine
+    w = get_workload("small").with_(name=var, **VARIANTS[var])
+    cat = make_catalog(w)
+    pre = make_prefixes(w, cat)
+    tw, dw = make_weights(w, "target"), make_weights(w, "draft")
+    eng = Engine(w, tw, dw, cat)
+    dev = torch.device("cuda:0")
+    root = torch.zeros((w.batch, w.n_item_tokens), dtype=torch.float32, device=dev)
+    eng.atspeed_prefill(torch.from_numpy(pre).to(dev), root)
+    tgt = Decoder(w.target, tw, w.dtype)
+    dft = Decoder(w.draft, dw, w.dtype)
+    trie = Trie(cat)
+    trees, caches = [], []
+    for u in range(w.batch):
+        c = tgt.prefill(pre[u])
+        caches.append(c)
+        lq = model_scorer(dft, dft.prefill(pre[u]), w.draft.item_base, w.codebook)
+        D = draft_levels(lq, trie, [()], 4, w.N, w.codebook)
+        trees.append([p for lvl in D for p, _ in lvl])
+    nodes = upload_tree(eng, trees, w.batch)
+    logits = torch.full((w.batch, eng.max_nodes, w.n_item_tokens), float("nan"), dtype=torch.float32, device=dev)
+    eng.atspeed_tree_logits(logits)
+    torch.cuda.synchronize()
+    lg, r = logits.cpu().numpy(), root.cpu().numpy()
+    worst = 0.0
+    for u in range(w.batch):
+        e_root = np.abs(r[u] - caches[u].last_logits).max()
+        fwd = [i for i, p in enumerate(nodes[u]) if len(p) < w.L]
+        toks = [tuple(w.target.item_base + w.codebook * l + c for l, c in enumerate(nodes[u][i])) for i in fwd]
+        e_tree = np.abs(lg[u, fwd] - tgt.path_logits(caches[u], toks)).max()
+        print(f"[{var}] user {u}: root logits max|err| {e_root:.3e}, tree logits max|err| {e_tree:.3e} "
+              f"(logit std {caches[u].last_logits.std():.3f})")
+        worst = max(worst, e_root, e_tree)
+    eng.close()
+    if var == "dh128":
+        assert worst <= LOGIT_TOL["bf16"]
