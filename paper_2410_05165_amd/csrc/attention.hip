@@ -323,11 +323,15 @@ attn_mfma_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ pk, co
     for (int db = 0; db < NDB; ++db) o[db] *= alpha;
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
-      bf16x8_t pf;
+      // P as the sum of two bf16 parts (hi + lo ~ 16 significant bits), so the
+      // probabilities keep near-fp32 precision through the bf16 MFMA.
+      bf16x8_t pf, pl;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         pf[i] = (__bf16)sc[2 * kk][i];
         pf[4 + i] = (__bf16)sc[2 * kk + 1][i];
+        pl[i] = (__bf16)(sc[2 * kk][i] - (float)pf[i]);
+        pl[4 + i] = (__bf16)(sc[2 * kk + 1][i] - (float)pf[4 + i]);
       }
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
@@ -338,6 +342,7 @@ attn_mfma_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ pk, co
         u32x4_t w4 = {lo.x, lo.y, hi.x, hi.y};
         bf16x8_t vf = __builtin_bit_cast(bf16x8_t, w4);
         o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[db], 0, 0, 0);
+        o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pl, o[db], 0, 0, 0);
       }
     }
     __syncthreads();

@@ -106,7 +106,7 @@ __device__ __forceinline__ void mma_stage(const unsigned char* stage, int wave_m
   }
 }
 
-template <int WM, int WN, int TM, int TN, int BMAP, int EPI>
+template <int WM, int WN, int TM, int TN, int BMAP, int EPI, int NS>
 __global__ void __launch_bounds__(64 * WM * WN)
 gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ Mdev, int Mt, int N, int K,
                  BArgs b, EpiArgs e) {
@@ -114,8 +114,10 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
   static_assert(WM * WN == 4, "four waves");
   constexpr int NA = T::BM / 32;   // wave instructions per stage for A (8 rows each, 4 waves)
   constexpr int NB = T::BN / 32;
+  static_assert(NS == 2 || NS == 3, "two or three LDS stages");
   __shared__ __align__(1024) unsigned char st0[T::STAGE];
   __shared__ __align__(1024) unsigned char st1[T::STAGE];
+  __shared__ __align__(1024) unsigned char st2[NS == 3 ? T::STAGE : 16];
   const int M = *Mdev;
   // XCD-aware tile order: workgroup L is dispatched to XCD L % 8; XCD x owns the
   // contiguous range x*per .. x*per+per-1 of the tiles in N-major order, so the
@@ -180,77 +182,160 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
 
   const int nk = K / T::BK;
   const int fr = lane & 31, fc = lane >> 5;
-  load_stage<NA, NB>(st0, wave, A, a_off, B0, B1, b_off, b_hi, 0, T::A_BYTES);
-  __builtin_amdgcn_s_waitcnt(0);
+  // NS-stage pipeline: stage s of round kt0 computes k-tile kt0+s while the
+  // DMA of k-tile kt0+s+NS-1 is in flight; each stage is its own LDS array and
+  // is chosen at compile time, so the compiler sees the DMA and the fragment
+  // reads of a step touch different objects and inserts no waits between them.
+  auto stage = [&](auto S) -> unsigned char* {
+    constexpr int s_ = decltype(S)::value % NS;
+    return s_ == 0 ? st0 : (s_ == 1 ? st1 : st2);
+  };
+  constexpr int NLOADS = NA + NB;                 // DMA instructions per stage per lane
+  constexpr int ALLOW = NLOADS * (NS - 2);        // loads that may stay in flight at a stage boundary
+  constexpr int WAITCNT = (ALLOW & 0xF) | (((ALLOW >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8);
+  if constexpr (NS == 2) {
+    // nk is even (K % 128 == 0 is checked on the host): stages alternate st0, st1
+    load_stage<NA, NB>(st0, wave, A, a_off, B0, B1, b_off, b_hi, 0, T::A_BYTES);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    for (int kt = 0; kt < nk; kt += 2) {
+      load_stage<NA, NB>(st1, wave, A, a_off, B0, B1, b_off, b_hi, (kt + 1) * 64, T::A_BYTES);
+      mma_stage<WM, WN, TM, TN>(st0, wave_m, wave_n, fr, fc, acc, T::A_BYTES);
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+      if (kt + 2 < nk) load_stage<NA, NB>(st0, wave, A, a_off, B0, B1, b_off, b_hi, (kt + 2) * 64, T::A_BYTES);
+      mma_stage<WM, WN, TM, TN>(st1, wave_m, wave_n, fr, fc, acc, T::A_BYTES);
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+    }
+  } else {
+  static_for<NS - 1>([&](auto S) {
+    constexpr int s_ = decltype(S)::value;
+    if (s_ < nk) load_stage<NA, NB>(stage(S), wave, A, a_off, B0, B1, b_off, b_hi, s_ * 64, T::A_BYTES);
+  });
+  __builtin_amdgcn_s_waitcnt(WAITCNT);
   __syncthreads();
-  // nk is even (K % 128 == 0 is checked on the host): stages alternate st0, st1
-  for (int kt = 0; kt < nk; kt += 2) {
-    load_stage<NA, NB>(st1, wave, A, a_off, B0, B1, b_off, b_hi, (kt + 1) * 64, T::A_BYTES);
-    mma_stage<WM, WN, TM, TN>(st0, wave_m, wave_n, fr, fc, acc, T::A_BYTES);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if (kt + 2 < nk) load_stage<NA, NB>(st0, wave, A, a_off, B0, B1, b_off, b_hi, (kt + 2) * 64, T::A_BYTES);
-    mma_stage<WM, WN, TM, TN>(st1, wave_m, wave_n, fr, fc, acc, T::A_BYTES);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
+  for (int kt0 = 0; kt0 < nk; kt0 += NS) {
+    static_for<NS>([&](auto S) {
+      constexpr int s_ = decltype(S)::value;
+      const int kt = kt0 + s_;
+      if (kt < nk) {
+        if (kt + NS - 1 < nk)
+          load_stage<NA, NB>(stage(std::integral_constant<int, s_ + NS - 1>{}), wave, A, a_off, B0, B1, b_off, b_hi,
+                             (kt + NS - 1) * 64, T::A_BYTES);
+        mma_stage<WM, WN, TM, TN>(stage(S), wave_m, wave_n, fr, fc, acc, T::A_BYTES);
+        // Own DMA of the next stage landed (only the newest stage may still be in
+        // flight); the fragment reads of this stage were consumed by the MFMAs.
+        // A bare barrier then orders both for every wave (a fenced __syncthreads
+        // would drain the newest stage's DMA too).
+        __builtin_amdgcn_s_waitcnt(WAITCNT);
+        __builtin_amdgcn_s_barrier();
+      }
+    });
+  }
+  __syncthreads();
   }
 
   // ---- epilogue.  acc[i][j][r] is row (r/4)*8 + (lane/32)*4 + r%4, column lane%32 of block (i, j).
   const int row0 = m0 + wave_m * TM * 32;
   const int col0 = tile_n * T::BN + wave_n * TN * 32;
-  static_for<TM>([&](auto I) {
-    constexpr int i = decltype(I)::value;
-    static_for<16>([&](auto R) {
-      constexpr int r = decltype(R)::value;
-      const int row = row0 + i * 32 + (r >> 2) * 8 + fc * 4 + (r & 3);
-      const bool rok = row < M;
-      if (EPI == EPI_STORE || EPI == EPI_RESID) {
+  if constexpr (EPI == EPI_STORE || EPI == EPI_RESID) {
+    static_for<TM>([&](auto I) {
+      constexpr int i = decltype(I)::value;
+      static_for<16>([&](auto R) {
+        constexpr int r = decltype(R)::value;
+        const int row = row0 + i * 32 + (r >> 2) * 8 + fc * 4 + (r & 3);
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
           const int col = col0 + j * 32 + fr;
-          if (rok && col < N) {
+          if (row < M && col < N) {
             float* p = e.out + (size_t)row * e.ldo + col;
             if (EPI == EPI_STORE) *p = acc[i][j][r];
             else *p += acc[i][j][r];
           }
         }
-      } else if (EPI == EPI_GU) {
-        constexpr int half = TN / 2;
+      });
+    });
+  } else {
+    // Results are rounded to bf16 into an LDS copy of the output tile (the stage
+    // buffers are free now), then written out in 16-byte chunks along rows.
+    constexpr int OUTC = EPI == EPI_GU ? T::BN / 2 : T::BN;  // output columns of the tile
+    constexpr int OROW = OUTC * 2;                            // bytes per LDS row
+    constexpr int HROWS = T::BM / 2;  // rows of wave row 0 go to st0, of wave row 1 to st1
+    static_assert(HROWS * OROW <= T::STAGE && WM == 2, "each half of the output tile fits a stage buffer");
+    bf16_t* ob = reinterpret_cast<bf16_t*>(wave_m == 0 ? st0 : st1);
+    if constexpr (EPI == EPI_GU) {
+      constexpr int half = TN / 2;
+      static_for<TM>([&](auto I) {
+        constexpr int i = decltype(I)::value;
+        static_for<16>([&](auto R) {
+          constexpr int r = decltype(R)::value;
+          const int hr = i * 32 + (r >> 2) * 8 + fc * 4 + (r & 3);  // row within this half
 #pragma unroll
-        for (int j = 0; j < half; ++j) {
-          const int fcol = tile_n * (T::BN / 2) + wave_n * (half * 32) + j * 32 + fr;
-          const float v = silu(acc[i][j][r]) * acc[i][j + half][r];
-          if (rok && fcol < b.split) e.hout[(size_t)row * b.split + fcol] = f2bf(v);
-        }
-      } else {  // EPI_QKV: the wave's 128 columns are one head (d_head 128) or two (d_head 64)
-        const int rr = rok ? row : 0;
-        const int pos = e.rows.pos[rr];
-        const int halfdh = e.dh >> 1;
-        const bool pair1 = halfdh == 32;  // partner block j^1 (d_head 64) or j^2 (d_head 128)
-        const int which = col0 / e.d;     // the wave's columns lie in one of q, k, v
-        size_t kvoff;
-        if (e.kv_mode == 0) kvoff = ((size_t)e.rows.user[rr] * e.H * e.Pmax + pos) * e.dh;
-        else kvoff = (size_t)e.rows.slot[rr] * e.d;
-        const size_t hstride = e.kv_mode == 0 ? (size_t)e.Pmax * e.dh : (size_t)e.dh;
-        bf16_t* dst = which == 0 ? e.q + (size_t)rr * e.d : (which == 1 ? e.kdst : e.vdst) + kvoff;
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          const int col = col0 + j * 32 + fr;
-          const int hc = col - which * e.d;
-          const int head = hc / e.dh, ii = hc - head * e.dh;
-          float v = acc[i][j][r];
-          if (which < 2) {
-            const float pv = pair1 ? acc[i][j ^ 1][r] : acc[i][j ^ 2][r];
-            const int fi = ii & (halfdh - 1);
-            const float c = e.cosT[pos * halfdh + fi], s = e.sinT[pos * halfdh + fi];
-            v = ii < halfdh ? v * c - pv * s : v * c + pv * s;
+          for (int j = 0; j < half; ++j) {
+            const int lc = wave_n * (half * 32) + j * 32 + fr;
+            ob[hr * OUTC + lc] = f2bf(silu(acc[i][j][r]) * acc[i][j + half][r]);
           }
-          const size_t off = which == 0 ? (size_t)hc : head * hstride + ii;
-          if (rok && col < N) dst[off] = f2bf(v);
+        });
+      });
+    } else {  // EPI_QKV: rotary embedding on q and k; each wave's 128 columns lie in one of q, k, v
+      const int halfdh = e.dh >> 1;
+      const bool pair1 = halfdh == 32;       // partner block j^1 (d_head 64) or j^2 (d_head 128)
+      const bool rot = col0 / e.d < 2;
+      static_for<TM>([&](auto I) {
+        constexpr int i = decltype(I)::value;
+        static_for<16>([&](auto R) {
+          constexpr int r = decltype(R)::value;
+          const int hr = i * 32 + (r >> 2) * 8 + fc * 4 + (r & 3);  // row within this half
+          const int row = m0 + wave_m * HROWS + hr;
+          const int pos = e.rows.pos[row < M ? row : M - 1];
+          const float* cb = e.cosT + pos * halfdh;
+          const float* sb = e.sinT + pos * halfdh;
+          // column j*32+fr of the wave's head-aligned span; its rotary index is (j*32+fr) mod halfdh
+          const float c0 = cb[fr & (halfdh - 1)], s0 = sb[fr & (halfdh - 1)];
+          const float c1 = cb[(32 + fr) & (halfdh - 1)], s1 = sb[(32 + fr) & (halfdh - 1)];
+#pragma unroll
+          for (int j = 0; j < TN; ++j) {
+            float v = acc[i][j][r];
+            if (rot) {
+              const float pv = pair1 ? acc[i][j ^ 1][r] : acc[i][j ^ 2][r];
+              const bool odd = (j & 1) != 0;
+              const float c = (pair1 || !odd) ? c0 : c1, sn = (pair1 || !odd) ? s0 : s1;
+              const bool lo = pair1 ? !odd : j < 2;   // first half of the head
+              v = lo ? v * c - pv * sn : v * c + pv * sn;
+            }
+            ob[hr * OUTC + wave_n * TN * 32 + j * 32 + fr] = f2bf(v);
+          }
+        });
+      });
+    }
+    __syncthreads();
+    constexpr int CPRW = OUTC / 8;  // 16-byte chunks per output row
+    for (int c = tid; c < T::BM * CPRW; c += T::NT) {
+      const int lr = c / CPRW, cc = (c % CPRW) * 8;
+      const int row = m0 + lr;
+      if (row >= M) continue;
+      const unsigned char* src = (lr < HROWS ? st0 : st1) + (lr % HROWS) * OROW + cc * 2;
+      const u32x4_t v = *reinterpret_cast<const u32x4_t*>(src);
+      if constexpr (EPI == EPI_GU) {
+        const int fcol = tile_n * (T::BN / 2) + cc;
+        if (fcol < b.split) *reinterpret_cast<u32x4_t*>(e.hout + (size_t)row * b.split + fcol) = v;
+      } else {
+        const int col = tile_n * T::BN + cc;
+        if (col >= N) continue;
+        const int which = col / e.d, hc = col - which * e.d;
+        if (which == 0) {
+          *reinterpret_cast<u32x4_t*>(e.q + (size_t)row * e.d + hc) = v;
+        } else {
+          const int head = hc / e.dh, ii = hc - head * e.dh;
+          size_t off;
+          if (e.kv_mode == 0) off = (((size_t)e.rows.user[row] * e.H + head) * e.Pmax + e.rows.pos[row]) * e.dh + ii;
+          else off = (size_t)e.rows.slot[row] * e.d + hc;
+          *reinterpret_cast<u32x4_t*>((which == 1 ? e.kdst : e.vdst) + off) = v;
         }
       }
-    });
-  });
+    }
+  }
 }
 
 // ------------------------------------------------------------------ fp32 path
@@ -347,7 +432,7 @@ __global__ void epi_f32_kernel(const float* __restrict__ C, const int* __restric
 // 256x256 tiles (4 waves of 128x128) for the wide projections (q/k/v, gate/up);
 // 128x256 tiles for the d_model-wide ones (o, down, output head), which keeps
 // their tile count near the CU count at a few thousand rows without split-K.
-template <int BMAP, int EPI, int TMW>
+template <int BMAP, int EPI, int TMW, int NS>
 static hipError_t launch_bf16(const GemmCall& g, hipStream_t st) {
   using T = Tile<2, 2, TMW, 4>;
   BArgs b{(const bf16_t*)g.w0, (const bf16_t*)g.w1, (const bf16_t*)g.w2, g.split};
@@ -359,7 +444,7 @@ static hipError_t launch_bf16(const GemmCall& g, hipStream_t st) {
   const int Mt = (g.Mmax + T::BM - 1) / T::BM, Nt = (g.N + T::BN - 1) / T::BN;
   const int per = (Mt * Nt + 7) / 8;
   dim3 grid(8 * per);
-  auto kern = gemm_bf16_kernel<2, 2, TMW, 4, BMAP, EPI>;
+  auto kern = gemm_bf16_kernel<2, 2, TMW, 4, BMAP, EPI, NS>;
   hipLaunchKernelGGL(kern, grid, dim3(T::NT), 0, st, (const bf16_t*)g.A, g.lda, g.Mdev, Mt, g.N, g.K, b, e);
   return hipGetLastError();
 }
@@ -367,10 +452,10 @@ static hipError_t launch_bf16(const GemmCall& g, hipStream_t st) {
 hipError_t gemm(const GemmCall& g, hipStream_t st) {
   if (g.bf16) {
     switch (g.kind) {
-      case GEMM_QKV: return launch_bf16<BMAP_QKV, EPI_QKV, 4>(g, st);
-      case GEMM_GU: return launch_bf16<BMAP_GU, EPI_GU, 4>(g, st);
-      case GEMM_RESID: return launch_bf16<BMAP_PLAIN, EPI_RESID, 2>(g, st);
-      default: return launch_bf16<BMAP_PLAIN, EPI_STORE, 2>(g, st);
+      case GEMM_QKV: return launch_bf16<BMAP_QKV, EPI_QKV, 4, 2>(g, st);
+      case GEMM_GU: return launch_bf16<BMAP_GU, EPI_GU, 4, 2>(g, st);
+      case GEMM_RESID: return launch_bf16<BMAP_PLAIN, EPI_RESID, 2, 3>(g, st);
+      default: return launch_bf16<BMAP_PLAIN, EPI_STORE, 2, 3>(g, st);
     }
   }
   // fp32: raw product into g.scratch (or straight into the logits), then the
