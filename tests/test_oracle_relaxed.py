@@ -1,0 +1,118 @@
+"""Pins for the oracle's relaxed sampling verification (CPU).
+
+Output law (speculative sampling, Leviathan et al. A.1, as restated in the
+relaxed-verification appendix): every RELAXED_EXACT slot is distributed as the
+target's level distribution pi_p; a slot is accepted with probability
+b = sum min(pi_p, pi_q) = 1 - TVD (Eq. 6); a level with K slots is accepted with
+probability b^K.  Small table scorers keep the Philox-driven runs fast.
+"""
+import math
+
+import numpy as np
+import pytest
+
+from oracle.relaxed import Streams, draft_exact, draft_paper, level_dist, verify_exact, verify_paper
+from oracle.search import table_scorer
+from oracle.trie import Trie
+
+CB, L = 4, 2
+
+
+def _tables(seed, same=False):
+    rng = np.random.default_rng(seed)
+    def tab():
+        t = {(): np.log(rng.dirichlet(np.ones(CB)))}
+        for c in range(CB):
+            t[(c,)] = np.concatenate([np.full(CB, -50.0), np.log(rng.dirichlet(np.ones(CB) * 0.7))])
+        for k in t:
+            if len(t[k]) == CB:
+                t[k] = np.concatenate([t[k], np.full(CB, -50.0)])
+        return t
+    tp = tab()
+    tq = tp if same else tab()
+    return table_scorer(tp), table_scorer(tq)
+
+
+def _run_exact(lp, lq, trie, K, runs):
+    slots1, acc_slots, acc_levels, n_slots = [], 0, 0, 0
+    for r in range(runs):
+        rs = Streams((r, 12345), 0)
+        D = draft_exact(lq, trie, [()], [0.0], 2, K, CB, 1.0, rs, 0)
+        log = []
+        verify_exact(lp, lq, trie, [((), 0.0)], [0.0], D, K, L, CB, 1.0, rs, 0, log)
+        lvl1 = [e for e in log if e[0] == "slots" and e[1] == 1][0]
+        slots1.extend(lvl1[2])
+        acc_levels += int(lvl1[3])
+        n_slots += K
+    return slots1, acc_levels
+
+
+def test_exact_slots_follow_target_distribution():
+    trie = Trie(np.array([[a, b] for a in range(CB) for b in range(CB)]))
+    lp, lq = _tables(1)
+    K, runs = 2, 6000
+    paths, logp, _ = level_dist([((), 0.0)], lp, trie, CB, 1.0)
+    _, logq, _ = level_dist([((), 0.0)], lq, trie, CB, 1.0)
+    p, q = np.exp(logp), np.exp(logq)
+    slots1, acc_levels = _run_exact(lp, lq, trie, K, runs)
+    counts = np.array([sum(1 for s in slots1 if s == c) for c in paths], dtype=float)
+    n = counts.sum()
+    chi2 = float(((counts - n * p) ** 2 / (n * p)).sum())
+    # chi-square with 3 dof, alpha = 1e-3: 16.27
+    assert chi2 < 16.27, (counts / n, p)
+    # the draft is not the target: without the correction the slots would follow q
+    chi2_q = float(((counts - n * q) ** 2 / (n * q)).sum())
+    assert chi2_q > 16.27
+    # level acceptance = b^K with b = sum min(p, q) = 1 - TVD (Eq. 6); 99.9% normal interval
+    b = float(np.minimum(p, q).sum())
+    assert abs(b - (1 - 0.5 * np.abs(p - q).sum())) < 1e-12
+    pk = b ** K
+    se = math.sqrt(pk * (1 - pk) / runs)
+    assert abs(acc_levels / runs - pk) < 3.3 * se, (acc_levels / runs, pk)
+
+
+def test_exact_slot_acceptance_rate_is_one_minus_tvd():
+    trie = Trie(np.array([[a, b] for a in range(CB) for b in range(CB)]))
+    lp, lq = _tables(2)
+    paths, logp, _ = level_dist([((), 0.0)], lp, trie, CB, 1.0)
+    _, logq, _ = level_dist([((), 0.0)], lq, trie, CB, 1.0)
+    b = float(np.minimum(np.exp(logp), np.exp(logq)).sum())
+    runs, K, acc = 4000, 3, 0
+    for r in range(runs):
+        rs = Streams((r, 777), 1)
+        D = draft_exact(lq, trie, [()], [0.0], 1, K, CB, 1.0, rs, 0)
+        for k, y in enumerate(D[0]):
+            i = paths.index(y)
+            acc += math.log(rs.u(0, 1, k, 0, 1)) <= logp[i] - logq[i]
+    n = runs * K
+    se = math.sqrt(b * (1 - b) / n)
+    assert abs(acc / n - b) < 3.3 * se, (acc / n, b)
+
+
+def test_identical_draft_accepts_every_level():
+    trie = Trie(np.array([[a, b] for a in range(CB) for b in range(CB)]))
+    lp, _ = _tables(3)
+    for r in range(50):
+        rs = Streams((r, 1), 0)
+        D = draft_exact(lp, trie, [()], [0.0], 2, 3, CB, 1.0, rs, 0)
+        res = verify_exact(lp, lp, trie, [((), 0.0)], [0.0], D, 3, L, CB, 1.0, rs, 0)
+        assert res.accepted == 2 and res.t_after == 2
+        # PAPER mode: with N = K the kept beams are the drafted ones, so pi_p and
+        # pi_q share their candidate sets and q = p accepts every level
+        Dp = draft_paper(lp, trie, [()], [0.0], 2, 2, CB, 1.0, rs, 0)
+        res = verify_paper(lp, lp, trie, [((), 0.0)], [0.0], Dp, 2, L, CB, 1.0, rs, 0)
+        assert res.accepted == 2 and res.t_after == 2
+
+
+def test_paper_mode_outputs_valid_distinct_beams():
+    trie = Trie(np.array([[a, b] for a in range(CB) for b in range(CB) if (a + b) % 3]))
+    lp, lq = _tables(4)
+    for r in range(200):
+        rs = Streams((r, 9), 2)
+        D = draft_paper(lq, trie, [()], [0.0], 2, 3, CB, 1.0, rs, 0)
+        assert all(len(set(p for p, _ in lvl)) == len(lvl) for lvl in D)
+        res = verify_paper(lp, lq, trie, [((), 0.0)], [0.0], D, 2, L, CB, 1.0, rs, 0)
+        paths = [p for p, _ in res.beams]
+        assert len(paths) == len(set(paths)) <= 2
+        assert all(trie.is_prefix(p) for p in paths)
+        assert res.t_after == len(paths[0]) and 0 <= res.accepted <= res.t_after
