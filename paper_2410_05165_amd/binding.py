@@ -115,7 +115,7 @@ class Engine:
 
     def __init__(self, w, target_w: Dict[str, np.ndarray], draft_w: Optional[Dict[str, np.ndarray]],
                  catalog: np.ndarray, max_batch: Optional[int] = None, max_prefix: Optional[int] = None,
-                 device: str = "cuda:0", mode: int = STRICT, stream=None):
+                 device: str = "cuda:0", mode: int = STRICT, stream=None, seed: int = 0):
         import torch
         self.torch = torch
         self.lib = load_library()
@@ -132,7 +132,7 @@ class Engine:
         cfg.L, cfg.codebook, cfg.K, cfg.N, cfg.gamma = w.L, w.codebook, w.K, w.N, w.gamma
         cfg.max_batch = max_batch or w.batch
         cfg.max_prefix = max_prefix or w.prefix_len
-        cfg.mode, cfg.temperature, cfg.seed = mode, w.temperature, 0
+        cfg.mode, cfg.temperature, cfg.seed = mode, w.temperature, seed
         cfg.dtype = BF16 if self.bf16 else FP32
         cfg.stream = self.stream.cuda_stream
         self.cfg = cfg

@@ -111,6 +111,8 @@ struct atspeed_ctx {
   int* acc_tmp = nullptr;
   int* tafter_tmp = nullptr;
   unsigned long long* keys = nullptr;
+  CandBuf cand{};
+  RelaxArgs relax{};
   int B = 0, P = 0;
   bool prefilled = false;
   bool drafted = false;
@@ -193,7 +195,9 @@ atspeed_status check_config(const atspeed_config* cfg) {
   if (c.max_batch < 1 || c.max_batch > 1024) return fail(ATSPEED_E_INVALID, "max_batch must be 1..1024");
   if (c.max_prefix < 1) return fail(ATSPEED_E_INVALID, "max_prefix must be >= 1");
   if (c.dtype != ATSPEED_FP32 && c.dtype != ATSPEED_BF16) return fail(ATSPEED_E_INVALID, "dtype");
-  if (c.mode != ATSPEED_STRICT) return fail(ATSPEED_E_INVALID, "only strict verification is built in this library");
+  if (c.mode != ATSPEED_STRICT && c.mode != ATSPEED_RELAXED_EXACT && c.mode != ATSPEED_RELAXED_PAPER)
+    return fail(ATSPEED_E_INVALID, "mode must be strict, relaxed-exact or relaxed-paper");
+  if (c.mode != ATSPEED_STRICT && !(c.temperature > 0.f)) return fail(ATSPEED_E_INVALID, "temperature must be > 0");
   ST_TRY(check_dims(c.target, c, "target"));
   if (c.draft.n_layers > 0) {
     ST_TRY(check_dims(c.draft, c, "draft"));
@@ -335,6 +339,20 @@ void layout(atspeed_ctx& c, const atspeed_config& cfg, int trie_nodes, Arena& a)
   c.acc_tmp = a.take<int>(B);
   c.tafter_tmp = a.take<int>(B);
   c.keys = a.take<unsigned long long>((size_t)B * c.max_cand);
+  const size_t nc = (size_t)B * c.max_cand;
+  c.cand.path = a.take<uint32_t>(nc);
+  c.cand.par = a.take<int>(nc);
+  c.cand.cidx = a.take<int>(nc);
+  c.cand.sp = a.take<float>(nc);
+  c.cand.sq = a.take<float>(nc);
+  c.relax.mode = cfg.mode;
+  c.relax.tau = cfg.temperature;
+  c.relax.k0 = (uint32_t)(cfg.seed & 0xFFFFFFFFu);
+  c.relax.k1 = (uint32_t)(cfg.seed >> 32);
+  c.relax.N = cfg.N;
+  c.relax.zq = a.take<float>((size_t)B * (L + 1));
+  c.relax.slot_node = a.take<int>((size_t)B * (L + 1) * K);
+  c.relax.keys = c.keys;
 }
 
 atspeed_status bind_weights(ModelRt& r, const atspeed_weights* w, const char* who) {
@@ -562,8 +580,12 @@ atspeed_status atspeed_draft(atspeed_ctx* c) {
   launch_draft_beam_scores(c->state, c->tree, c->dft.lp, c->dft.root, c->nitem, cf.codebook, L, B, c->st);
   HIP_TRY(hipGetLastError());
   for (int j = 1; j <= std::min(cf.gamma, L); ++j) {
-    launch_draft_select(c->state, c->tree, c->trie, c->dft.lp, c->dft.root, c->nitem, cf.target.item_base,
-                        cf.codebook, L, j, cf.N, c->lvl_lo, c->lvl_hi, c->keys, c->max_cand, B, c->st);
+    if (cf.mode == ATSPEED_STRICT)
+      launch_draft_select(c->state, c->tree, c->trie, c->dft.lp, c->dft.root, c->nitem, cf.target.item_base,
+                          cf.codebook, L, j, cf.N, c->lvl_lo, c->lvl_hi, c->keys, c->max_cand, B, c->st);
+    else
+      launch_draft_relaxed(c->state, c->tree, c->trie, c->dft.lp, c->dft.root, c->nitem, cf.target.item_base,
+                           cf.codebook, L, j, c->lvl_lo, c->lvl_hi, c->cand, c->max_cand, c->relax, B, c->st);
     HIP_TRY(hipGetLastError());
     if (j < std::min(cf.gamma, L)) {  // log-probs of the new level feed the next one
       launch_plan_tree(c->tree, c->lvl_lo, c->lvl_hi, B, c->P, c->rows, c->st);
@@ -600,8 +622,15 @@ static atspeed_status accept_on(atspeed_ctx* c, const float* lpt, const float* r
                                 int32_t* t_after) {
   const atspeed_config& cf = c->cfg;
   HIP_TRY(mark(*c, ATSPEED_K_SELECT));
-  launch_verify_strict(c->state, c->tree, c->trie, lpt, roott, c->nitem, cf.codebook, cf.L, c->keys, c->max_cand,
-                       accepted ? accepted : c->acc_tmp, t_after ? t_after : c->tafter_tmp, c->B, c->st);
+  if (cf.mode == ATSPEED_STRICT) {
+    launch_verify_strict(c->state, c->tree, c->trie, lpt, roott, c->nitem, cf.codebook, cf.L, c->keys, c->max_cand,
+                         accepted ? accepted : c->acc_tmp, t_after ? t_after : c->tafter_tmp, c->B, c->st);
+  } else {
+    if (!c->drafted) return fail(ATSPEED_E_STATE, "relaxed verification needs the context's own draft of this step");
+    launch_verify_relaxed(c->state, c->tree, c->trie, lpt, roott, c->dft.lp, c->dft.root, c->nitem, cf.codebook, cf.L,
+                          c->cand, c->max_cand, c->relax, accepted ? accepted : c->acc_tmp,
+                          t_after ? t_after : c->tafter_tmp, c->B, c->st);
+  }
   HIP_TRY(hipGetLastError());
   HIP_TRY(mark(*c, -1));
   return ATSPEED_OK;

@@ -42,6 +42,35 @@ struct TreeDev {
   int* ttrie;       // derived: trie node of each node
 };
 
+// Per-user candidate scratch of the relaxed modes (max_cand entries per user).
+struct CandBuf {
+  uint32_t* path;
+  int* par;
+  int* cidx;
+  float* sp;
+  float* sq;
+  __host__ __device__ CandBuf offset(size_t o) const { return CandBuf{path + o, par + o, cidx + o, sp + o, sq + o}; }
+};
+
+// Relaxed-mode parameters and buffers.
+struct RelaxArgs {
+  int mode;                 // 1 EXACT, 2 PAPER
+  float tau;
+  uint32_t k0, k1;          // Philox key
+  int N;
+  float* zq;                // [B, L+1] draft log-normaliser of each drafted level
+  int* slot_node;           // [B, L+1, K] EXACT: tree slot of every drafted slot
+  unsigned long long* keys; // [B, max_cand]
+};
+
+void launch_draft_relaxed(const StateDev& s, const TreeDev& tr, const TrieDev& trie, const float* lpq,
+                          const float* rootq, int nitem, int item_base, int codebook, int L, int j, int* lvl_lo,
+                          int* lvl_hi, const CandBuf& cb, int max_cand, const RelaxArgs& ra, int B, hipStream_t st);
+void launch_verify_relaxed(const StateDev& s, const TreeDev& tr, const TrieDev& trie, const float* lpt,
+                           const float* roott, const float* lpq, const float* rootq, int nitem, int codebook, int L,
+                           const CandBuf& cb, int max_cand, const RelaxArgs& ra, int* accepted, int* t_after, int B,
+                           hipStream_t st);
+
 void launch_tree_from_beams(const StateDev& s, const TreeDev& tr, const TrieDev& trie, int B, int item_base,
                             int codebook, int L, hipStream_t st);
 void launch_tree_index(const TreeDev& tr, const TrieDev& trie, const StateDev& s, int B, int item_base, int codebook,
