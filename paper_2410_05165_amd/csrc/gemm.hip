@@ -81,29 +81,50 @@ __device__ __forceinline__ void load_stage(unsigned char* stage, int wave, const
                                      (lds_void_t*)(stage + a_bytes + (wave * NB + j) * 1024), 16, 0, 0);
 }
 
+// One LDS stage (64 columns of k) through the MFMAs.  Fragments of k-step kk+1
+// are read into a second register set while the MFMAs of step kk issue, so the
+// LDS latency hides behind matrix work instead of stalling every step.
 template <int WM, int WN, int TM, int TN>
 __device__ __forceinline__ void mma_stage(const unsigned char* stage, int wave_m, int wave_n, int fr, int fc,
                                           f32x16_t (&acc)[TM][TN], int a_bytes) {
-#pragma unroll
-  for (int kk = 0; kk < 4; ++kk) {
-    bf16x8_t af[TM], bfr[TN];
+  bf16x8_t af[2][TM], bfr[2][TN];
+  auto read = [&](int kk, bf16x8_t (&a)[TM], bf16x8_t (&b)[TN]) {
     const int ch = kk * 2 + fc;
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
       const int r = wave_m * TM * 32 + i * 32 + fr;
-      af[i] = *reinterpret_cast<const bf16x8_t*>(stage + r * 128 + ((ch ^ (r & 7)) << 4));
+      a[i] = *reinterpret_cast<const bf16x8_t*>(stage + r * 128 + ((ch ^ (r & 7)) << 4));
     }
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
       const int r = wave_n * TN * 32 + j * 32 + fr;
-      bfr[j] = *reinterpret_cast<const bf16x8_t*>(stage + a_bytes + r * 128 + ((ch ^ (r & 7)) << 4));
+      b[j] = *reinterpret_cast<const bf16x8_t*>(stage + a_bytes + r * 128 + ((ch ^ (r & 7)) << 4));
     }
+  };
+  read(0, af[0], bfr[0]);
+  // the scheduling groups below describe the whole stage in order: these reads,
+  // then per k-step an MFMA / next-step-read alternation (mask 0x008 = MFMA,
+  // 0x100 = DS read), then the last step's MFMAs
+  __builtin_amdgcn_sched_group_barrier(0x100, TM + TN, 0);
+  static_for<4>([&](auto KK) {
+    constexpr int kk = decltype(KK)::value;
+    constexpr int cur = kk & 1, nxt = cur ^ 1;
+    if constexpr (kk + 1 < 4) read(kk + 1, af[nxt], bfr[nxt]);
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-  }
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0);
+    if constexpr (kk + 1 < 4) {
+      static_for<TM + TN>([&](auto) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      });
+      __builtin_amdgcn_sched_group_barrier(0x008, TM * TN - (TM + TN), 0);
+    } else {
+      __builtin_amdgcn_sched_group_barrier(0x008, TM * TN, 0);
+    }
+  });
 }
 
 template <int WM, int WN, int TM, int TN, int BMAP, int EPI, int NS>
@@ -111,9 +132,10 @@ __global__ void __launch_bounds__(64 * WM * WN)
 gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ Mdev, int Mt, int N, int K,
                  BArgs b, EpiArgs e) {
   using T = Tile<WM, WN, TM, TN>;
-  static_assert(WM * WN == 4, "four waves");
-  constexpr int NA = T::BM / 32;   // wave instructions per stage for A (8 rows each, 4 waves)
-  constexpr int NB = T::BN / 32;
+  constexpr int NW = WM * WN;
+  static_assert(NW == 4 || NW == 8, "four or eight waves");
+  constexpr int NA = T::BM / (8 * NW);   // wave instructions per stage for A (8 rows of 128 B each)
+  constexpr int NB = T::BN / (8 * NW);
   static_assert(NS == 2 || NS == 3, "two or three LDS stages");
   __shared__ __align__(1024) unsigned char st0[T::STAGE];
   __shared__ __align__(1024) unsigned char st1[T::STAGE];
@@ -261,16 +283,18 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
     // buffers are free now), then written out in 16-byte chunks along rows.
     constexpr int OUTC = EPI == EPI_GU ? T::BN / 2 : T::BN;  // output columns of the tile
     constexpr int OROW = OUTC * 2;                            // bytes per LDS row
-    constexpr int HROWS = T::BM / 2;  // rows of wave row 0 go to st0, of wave row 1 to st1
-    static_assert(HROWS * OROW <= T::STAGE && WM == 2, "each half of the output tile fits a stage buffer");
-    bf16_t* ob = reinterpret_cast<bf16_t*>(wave_m == 0 ? st0 : st1);
+    constexpr int HROWS = T::BM / 2;  // the first half of the tile rows goes to st0, the second to st1
+    constexpr int WMH = WM / 2;       // wave rows per half
+    static_assert(HROWS * OROW <= T::STAGE && WM % 2 == 0, "each half of the output tile fits a stage buffer");
+    bf16_t* ob = reinterpret_cast<bf16_t*>(wave_m < WMH ? st0 : st1);
+    const int hrow0 = (wave_m % WMH) * TM * 32;
     if constexpr (EPI == EPI_GU) {
       constexpr int half = TN / 2;
       static_for<TM>([&](auto I) {
         constexpr int i = decltype(I)::value;
         static_for<16>([&](auto R) {
           constexpr int r = decltype(R)::value;
-          const int hr = i * 32 + (r >> 2) * 8 + fc * 4 + (r & 3);  // row within this half
+          const int hr = hrow0 + i * 32 + (r >> 2) * 8 + fc * 4 + (r & 3);  // row within this half
 #pragma unroll
           for (int j = 0; j < half; ++j) {
             const int lc = wave_n * (half * 32) + j * 32 + fr;
@@ -286,8 +310,8 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
         constexpr int i = decltype(I)::value;
         static_for<16>([&](auto R) {
           constexpr int r = decltype(R)::value;
-          const int hr = i * 32 + (r >> 2) * 8 + fc * 4 + (r & 3);  // row within this half
-          const int row = m0 + wave_m * HROWS + hr;
+          const int hr = hrow0 + i * 32 + (r >> 2) * 8 + fc * 4 + (r & 3);  // row within this half
+          const int row = m0 + (wave_m < WMH ? 0 : HROWS) + hr;
           const int pos = e.rows.pos[row < M ? row : M - 1];
           const float* cb = e.cosT + pos * halfdh;
           const float* sb = e.sinT + pos * halfdh;
@@ -429,12 +453,21 @@ __global__ void epi_f32_kernel(const float* __restrict__ C, const int* __restric
 }
 
 // ------------------------------------------------------------------ launchers
+// 256x256 tiles for q/k/v and gate/up: 8 waves of 64x128 (two waves per SIMD,
+// so one wave's LDS and barrier waits hide behind the other's MFMAs).
+constexpr int kWideWM = 4, kWideTM = 2;
+#ifndef NARROW_WM
+#define NARROW_WM 4   // o / down / output head: 256x128 tiles of 8 waves (64x64 each), 3 LDS stages
+#define NARROW_WN 2
+#define NARROW_TM 2
+#define NARROW_TN 2
+#endif
 // 256x256 tiles (4 waves of 128x128) for the wide projections (q/k/v, gate/up);
 // 128x256 tiles for the d_model-wide ones (o, down, output head), which keeps
 // their tile count near the CU count at a few thousand rows without split-K.
-template <int BMAP, int EPI, int TMW, int NS>
+template <int BMAP, int EPI, int WMW, int WNW, int TMW, int TNW, int NS>
 static hipError_t launch_bf16(const GemmCall& g, hipStream_t st) {
-  using T = Tile<2, 2, TMW, 4>;
+  using T = Tile<WMW, WNW, TMW, TNW>;
   BArgs b{(const bf16_t*)g.w0, (const bf16_t*)g.w1, (const bf16_t*)g.w2, g.split};
   EpiArgs e{};
   e.out = g.out; e.ldo = g.ldo; e.hout = (bf16_t*)g.hout;
@@ -444,7 +477,7 @@ static hipError_t launch_bf16(const GemmCall& g, hipStream_t st) {
   const int Mt = (g.Mmax + T::BM - 1) / T::BM, Nt = (g.N + T::BN - 1) / T::BN;
   const int per = (Mt * Nt + 7) / 8;
   dim3 grid(8 * per);
-  auto kern = gemm_bf16_kernel<2, 2, TMW, 4, BMAP, EPI, NS>;
+  auto kern = gemm_bf16_kernel<WMW, WNW, TMW, TNW, BMAP, EPI, NS>;
   hipLaunchKernelGGL(kern, grid, dim3(T::NT), 0, st, (const bf16_t*)g.A, g.lda, g.Mdev, Mt, g.N, g.K, b, e);
   return hipGetLastError();
 }
@@ -452,10 +485,10 @@ static hipError_t launch_bf16(const GemmCall& g, hipStream_t st) {
 hipError_t gemm(const GemmCall& g, hipStream_t st) {
   if (g.bf16) {
     switch (g.kind) {
-      case GEMM_QKV: return launch_bf16<BMAP_QKV, EPI_QKV, 4, 2>(g, st);
-      case GEMM_GU: return launch_bf16<BMAP_GU, EPI_GU, 4, 2>(g, st);
-      case GEMM_RESID: return launch_bf16<BMAP_PLAIN, EPI_RESID, 2, 3>(g, st);
-      default: return launch_bf16<BMAP_PLAIN, EPI_STORE, 2, 3>(g, st);
+      case GEMM_QKV: return launch_bf16<BMAP_QKV, EPI_QKV, kWideWM, 2, kWideTM, 4, 2>(g, st);
+      case GEMM_GU: return launch_bf16<BMAP_GU, EPI_GU, kWideWM, 2, kWideTM, 4, 2>(g, st);
+      case GEMM_RESID: return launch_bf16<BMAP_PLAIN, EPI_RESID, NARROW_WM, NARROW_WN, NARROW_TM, NARROW_TN, 3>(g, st);
+      default: return launch_bf16<BMAP_PLAIN, EPI_STORE, NARROW_WM, NARROW_WN, NARROW_TM, NARROW_TN, 3>(g, st);
     }
   }
   // fp32: raw product into g.scratch (or straight into the logits), then the
