@@ -161,6 +161,49 @@ def cpu_baseline(w, tw, pre, cat, tree_paths):
                        f"accepted={res.accepted}, host cpus={os.cpu_count()}"), res
 
 
+def bench_decode(args, w, eng, pre, dev):
+    """Relaxed workloads: a step is one whole decode (prefill, sampled drafting and
+    relaxed verification until every user holds L-token items); the replay-tree
+    step of the strict workload does not apply (relaxed verification consumes
+    the context's own sampled draft)."""
+    import numpy as np
+    import torch
+    from paper_2410_05165_amd.binding import Stats
+    B, K, L = w.batch, w.K, w.L
+    prefix = torch.from_numpy(pre).to(dev)
+    items = torch.zeros((B, K, L), dtype=torch.int32, device=dev)
+    scores = torch.zeros((B, K), dtype=torch.float32, device=dev)
+    n = torch.zeros(B, dtype=torch.int32, device=dev)
+    for _ in range(args.warmup):
+        eng.atspeed_decode_topk(prefix, items, scores, n, None)
+    torch.cuda.synchronize()
+    eng.atspeed_set_timing(True)
+    acc = np.zeros((L, B), np.int32)
+    st = Stats()
+    import ctypes as C
+    st.accepted = acc.ctypes.data_as(C.POINTER(C.c_int32))
+    a = time.perf_counter()
+    for _ in range(args.steps):
+        eng.atspeed_decode_topk(prefix, items, scores, n, st)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - a
+    kt = eng.atspeed_get_timing()
+    value = B * args.steps / elapsed
+    log(f"decode {1e3 * elapsed / args.steps:.1f} ms -> {value:.0f} lists/s; last decode steps {st.n_steps}")
+    out = {"metric": "top-K lists/sec/GPU (relaxed sampling verification, whole decode)", "value": round(value, 2),
+           "unit": "lists/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "ms_per_step": round(1e3 * elapsed / args.steps, 3), "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+           "config": {"workload": f"{w.name}: whole decode with {w.mode}, B={B}, P={w.prefix_len}, K={K}, N={w.N}, "
+                                  f"gamma={w.gamma}, tau={w.temperature}", "global_batch": B, "seq_len": w.prefix_len,
+                      "parallelism": "none (1 GPU)"},
+           "kernels": {k: dict(ms_per_step=v[0] / args.steps, launches_per_step=v[1] / args.steps)
+                       for k, v in kt.items() if v[1]},
+           "accepted_levels_last_decode": acc[:st.n_steps].tolist()}
+    print(json.dumps(out), flush=True)
+    eng.close()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -191,8 +234,13 @@ def main():
     tw = make_weights(w, "target")
     log(f"target weights {sum(a.nbytes for a in tw.values()) / 2**30:.1f} GiB ({time.time() - t0:.1f}s)")
     dw = make_weights(w, "draft")
-    eng = Engine(w, tw, dw, cat)
+    relaxed = w.mode != "strict"
+    mode = {"strict": 0, "relaxed_exact": 1, "relaxed_paper": 2}[w.mode]
+    key = [int(x) for x in __import__("synth").philox_key(w)]
+    eng = Engine(w, tw, dw, cat, mode=mode, seed=key[0] | (key[1] << 32))
     log(f"engine ready, workspace {eng.ws.numel() / 2**30:.2f} GiB ({time.time() - t0:.1f}s)")
+    if relaxed:
+        return bench_decode(args, w, eng, pre, dev)
     kids = catalog_children(cat)
     prefix = torch.from_numpy(pre).to(dev)
     B, K, L = w.batch, w.K, w.L

@@ -31,9 +31,9 @@ attn_kernel(const T* __restrict__ q, const T* __restrict__ pk, const T* __restri
   __shared__ int nctx_s[AQ], anc_s[AQ][4], nanc_s[AQ];
   __shared__ int kmax_s;
 
-  const int u = blockIdx.z, h = blockIdx.y;
+  const int u = blockIdx.y, h = blockIdx.x;
   const int ubeg = rows.user_off[u], uend = rows.user_off[u + 1];
-  const int r0 = ubeg + blockIdx.x * AQ;
+  const int r0 = ubeg + blockIdx.z * AQ;
   if (r0 >= uend) return;
   const int nq = min(AQ, uend - r0);
   const int tid = threadIdx.x;
@@ -209,7 +209,7 @@ attn_kernel(const T* __restrict__ q, const T* __restrict__ pk, const T* __restri
 }
 
 // ---------------------------------------------------------------- bf16 MFMA kernel
-// Per workgroup: (user, head, 64 query rows); wave w owns queries 16w..16w+15.
+// Per workgroup: (head, user, 64 query rows); wave w owns queries 16w..16w+15.
 // S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (A = K rows from LDS, B = Q from
 // registers): lane l holds S^T[key 4g+i][query l%16] (g = l/16) of each 16-key
 // block, so the probabilities of its query sit in registers in exactly the
@@ -230,9 +230,9 @@ attn_mfma_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ pk, co
   __shared__ __align__(16) bf16_t Vt[DH * KT];
   __shared__ int kmax_s;
 
-  const int u = blockIdx.z, h = blockIdx.y;
+  const int u = blockIdx.y, h = blockIdx.x;
   const int ubeg = rows.user_off[u], uend = rows.user_off[u + 1];
-  const int r0 = ubeg + blockIdx.x * 64;
+  const int r0 = ubeg + blockIdx.z * 64;
   if (r0 >= uend) return;
   const int nq = min(64, uend - r0);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -261,26 +261,51 @@ attn_mfma_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ pk, co
   const int kmax = kmax_s;
   const size_t kvbase = ((size_t)u * H + h) * Pmax * DH;
 
-  for (int k0 = 0; k0 < kmax; k0 += KT) {
+  // Tile staging: K rows as 16-byte chunks (NKC per thread); V transposed, each
+  // thread taking 4 consecutive keys x 8 dims so that it writes 8-byte runs of
+  // 4 keys per dim.  The next tile's global loads are issued into registers
+  // before the current tile's matrix work, so their latency hides behind it.
+  constexpr int NKC = KT * CPR / 256;
+  const bool vthr = tid < 16 * CPR;
+  const int vkg = tid / CPR, vj = tid % CPR;
+  u32x4_t kreg[NKC], vreg[4];
+  auto fetch = [&](int k0) {
     const int nk = min(KT, kmax - k0);
-    // stage K (swizzled rows) and V^T (swizzled 4-key chunks)
 #pragma unroll
-    for (int c = tid; c < KT * CPR; c += 256) {
-      const int key = c / CPR, j = c % CPR;
-      u32x4_t kv = {0u, 0u, 0u, 0u}, vv = {0u, 0u, 0u, 0u};
-      if (key < nk) {
-        kv = *reinterpret_cast<const u32x4_t*>(pk + kvbase + (size_t)(k0 + key) * DH + j * 8);
-        vv = *reinterpret_cast<const u32x4_t*>(pv + kvbase + (size_t)(k0 + key) * DH + j * 8);
-      }
-      *reinterpret_cast<u32x4_t*>(Ks + key * DH + ((j ^ (key & (CPR - 1))) * 8)) = kv;
-      const bf16_t* ve = reinterpret_cast<const bf16_t*>(&vv);
+    for (int c = 0; c < NKC; ++c) {
+      const int idx = tid + c * 256, key = idx / CPR, j = idx % CPR;
+      kreg[c] = key < nk ? *reinterpret_cast<const u32x4_t*>(pk + kvbase + (size_t)(k0 + key) * DH + j * 8)
+                         : u32x4_t{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int key = 4 * vkg + i;
+      vreg[i] = vthr && key < nk ? *reinterpret_cast<const u32x4_t*>(pv + kvbase + (size_t)(k0 + key) * DH + vj * 8)
+                                 : u32x4_t{0u, 0u, 0u, 0u};
+    }
+  };
+  auto stash = [&]() {
+#pragma unroll
+    for (int c = 0; c < NKC; ++c) {
+      const int idx = tid + c * 256, key = idx / CPR, j = idx % CPR;
+      *reinterpret_cast<u32x4_t*>(Ks + key * DH + ((j ^ (key & (CPR - 1))) * 8)) = kreg[c];
+    }
+    if (vthr) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const int dim = j * 8 + e;
-        Vt[dim * KT + ((((key >> 2) ^ (dim & 15)) << 2)) + (key & 3)] = ve[e];
+        const int dim = vj * 8 + e, sh = (e & 1) * 16;
+        uint2 w;
+        w.x = ((vreg[0][e >> 1] >> sh) & 0xffffu) | (((vreg[1][e >> 1] >> sh) & 0xffffu) << 16);
+        w.y = ((vreg[2][e >> 1] >> sh) & 0xffffu) | (((vreg[3][e >> 1] >> sh) & 0xffffu) << 16);
+        *reinterpret_cast<uint2*>(Vt + dim * KT + ((vkg ^ (dim & 15)) << 2)) = w;
       }
     }
+  };
+  if (kmax > 0) fetch(0);
+  for (int k0 = 0; k0 < kmax; k0 += KT) {
+    stash();
     __syncthreads();
+    if (k0 + KT < kmax) fetch(k0 + KT);
     // S^T for 4 blocks of 16 keys
     f32x4_t sc[4];
 #pragma unroll
@@ -350,12 +375,15 @@ attn_mfma_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ pk, co
 
   if (tk != nullptr && valid) {  // tree keys: ancestors and self
     const int na = rows.nanc[row];
+    int slot[4];
+#pragma unroll
+    for (int a = 0; a < 4; ++a) slot[a] = a < na ? rows.anc[row * 4 + a] : 0;
     float sa[4];
 #pragma unroll
     for (int a = 0; a < 4; ++a) {
       float part = 0.f;
       if (a < na) {
-        const bf16_t* kp = tk + (size_t)rows.anc[row * 4 + a] * d + h * DH;
+        const bf16_t* kp = tk + (size_t)slot[a] * d + h * DH;
 #pragma unroll
         for (int ks = 0; ks < NKS; ++ks) {
           const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(kp + ks * 32 + g * 8);
@@ -378,15 +406,24 @@ attn_mfma_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ pk, co
     }
     lsum = lsum * alpha + (g == 0 ? ps : 0.f);
     m = mnew;
+    // lane (query, g) holds dims db*16 + 4g .. +3 of O: one 8-byte load per
+    // (ancestor, block), the blocks of one ancestor issued together
 #pragma unroll
-    for (int db = 0; db < NDB; ++db) {
-      o[db] *= alpha;
+    for (int db = 0; db < NDB; ++db) o[db] *= alpha;
 #pragma unroll
-      for (int a = 0; a < 4; ++a) {
-        if (a < na) {
-          const bf16_t* vp = tv + (size_t)rows.anc[row * 4 + a] * d + h * DH + db * 16 + g * 4;
+    for (int a = 0; a < 4; ++a) {
+      if (a < na) {
+        const bf16_t* vp = tv + (size_t)slot[a] * d + h * DH + g * 4;
+        uint2 vw[NDB];
 #pragma unroll
-          for (int i = 0; i < 4; ++i) o[db][i] += sa[a] * bf2f(vp[i]);
+        for (int db = 0; db < NDB; ++db) vw[db] = *reinterpret_cast<const uint2*>(vp + db * 16);
+        const float p = sa[a];
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+          o[db][0] += p * __uint_as_float(vw[db].x << 16);
+          o[db][1] += p * __uint_as_float(vw[db].x & 0xffff0000u);
+          o[db][2] += p * __uint_as_float(vw[db].y << 16);
+          o[db][3] += p * __uint_as_float(vw[db].y & 0xffff0000u);
         }
       }
     }
@@ -396,16 +433,22 @@ attn_mfma_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ pk, co
   if (valid) {
     const float inv = 1.f / lsum;
 #pragma unroll
-    for (int db = 0; db < NDB; ++db)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) out[(size_t)row * d + h * DH + db * 16 + g * 4 + i] = f2bf(o[db][i] * inv);
+    for (int db = 0; db < NDB; ++db) {
+      uint2 w;
+      w.x = (uint32_t)f2bf(o[db][0] * inv) | ((uint32_t)f2bf(o[db][1] * inv) << 16);
+      w.y = (uint32_t)f2bf(o[db][2] * inv) | ((uint32_t)f2bf(o[db][3] * inv) << 16);
+      *reinterpret_cast<uint2*>(out + (size_t)row * d + h * DH + db * 16 + g * 4) = w;
+    }
   }
 }
 
 template <int DH>
 static hipError_t launch_attn_mfma(const AttnCall& a, hipStream_t st) {
   const float qscale = 1.4426950408889634f / sqrtf((float)DH);
-  dim3 grid((a.Tq + 63) / 64, a.H, a.B);
+  // query blocks vary slowest: workgroups are dealt to the XCDs round-robin by
+  // linear index, and the blocks past a user's rows exit at once, so the busy
+  // ones must form one contiguous run of linear indices to spread over all XCDs
+  dim3 grid(a.H, a.B, (a.Tq + 63) / 64);
   hipLaunchKernelGGL(attn_mfma_kernel<DH>, grid, dim3(256), 0, st, (const bf16_t*)a.q, (const bf16_t*)a.pk,
                      (const bf16_t*)a.pv, (const bf16_t*)a.tk, (const bf16_t*)a.tv, (bf16_t*)a.out, a.rows, a.H,
                      a.Pmax, qscale);
@@ -424,7 +467,7 @@ static hipError_t launch_attn(const AttnCall& a, hipStream_t st) {
     attr = true;
   }
   const float qscale = 1.4426950408889634f / sqrtf((float)DH);  // log2(e) / sqrt(d_head)
-  dim3 grid((a.Tq + AQ - 1) / AQ, a.H, a.B);
+  dim3 grid(a.H, a.B, (a.Tq + AQ - 1) / AQ);  // query blocks slowest, as in the MFMA kernel
   hipLaunchKernelGGL(kern, grid, dim3(256), smem, st, (const T*)a.q, (const T*)a.pk, (const T*)a.pv,
                      (const T*)a.tk, (const T*)a.tv, (T*)a.out, a.rows, a.H, a.Pmax, qscale);
   return hipGetLastError();
