@@ -262,19 +262,42 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
   const int row0 = m0 + wave_m * TM * 32;
   const int col0 = tile_n * T::BN + wave_n * TN * 32;
   if constexpr (EPI == EPI_STORE || EPI == EPI_RESID) {
+    // Branch-free: the accesses go through a buffer resource spanning this
+    // tile's valid rows, so the hardware drops stores past it (rows >= M, and
+    // columns >= N, which get an out-of-range offset) and returns 0 for such
+    // loads.  Guarding each access with a branch instead makes the compiler
+    // wait for every store before the next one.  RESID loads all TN x 16
+    // residual values of a 32-row block before it adds and stores them.
+    const int mrows = M - m0 < T::BM ? M - m0 : T::BM;
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        e.out + (size_t)m0 * e.ldo, 0, mrows * e.ldo * (int)sizeof(float), 0x00020000);
+    const int lrow0 = wave_m * TM * 32;
     static_for<TM>([&](auto I) {
       constexpr int i = decltype(I)::value;
+      int off[TN][16];
       static_for<16>([&](auto R) {
         constexpr int r = decltype(R)::value;
-        const int row = row0 + i * 32 + (r >> 2) * 8 + fc * 4 + (r & 3);
+        const int lrow = lrow0 + i * 32 + (r >> 2) * 8 + fc * 4 + (r & 3);
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
           const int col = col0 + j * 32 + fr;
-          if (row < M && col < N) {
-            float* p = e.out + (size_t)row * e.ldo + col;
-            if (EPI == EPI_STORE) *p = acc[i][j][r];
-            else *p += acc[i][j][r];
-          }
+          off[j][r] = col < N ? (lrow * e.ldo + col) * (int)sizeof(float) : 0x7fffffff;
+        }
+      });
+      float old[TN][16];
+      if constexpr (EPI == EPI_RESID) {
+        static_for<16>([&](auto R) {
+          constexpr int r = decltype(R)::value;
+#pragma unroll
+          for (int j = 0; j < TN; ++j) old[j][r] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, off[j][r], 0, 0));
+        });
+      }
+      static_for<16>([&](auto R) {
+        constexpr int r = decltype(R)::value;
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const float v = EPI == EPI_RESID ? old[j][r] + acc[i][j][r] : acc[i][j][r];
+          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), rs, off[j][r], 0, 0);
         }
       });
     });
