@@ -55,8 +55,10 @@ typedef enum {
 
 typedef enum { ATSPEED_FP32 = 0, ATSPEED_BF16 = 1 } atspeed_dtype;
 
-/* LLaMA-style decoder dimensions.  d_model % n_heads == 0, d_head in {32, 64, 128},
- * d_model and d_ffn multiples of 64. */
+/* LLaMA-style decoder dimensions.  d_model % n_heads == 0 and d_model <= 8192;
+ * bf16: d_head 64 or 128, d_model % 256 == 0, d_ffn % 128 == 0;
+ * fp32: d_head 32, 64 or 128, d_model and d_ffn multiples of 16.
+ * Violations make atspeed_create return ATSPEED_E_SHAPE. */
 typedef struct {
   int32_t n_layers, d_model, n_heads, d_ffn, vocab, item_base;
 } atspeed_model_dims;

@@ -42,25 +42,61 @@ __device__ __forceinline__ float block_max256(float v, float* red) {
 }
 
 // out[r] = g * x[src] / sqrt(mean(x[src]^2) + eps), src = row_index ? row_index[r] : r.
+// One workgroup per row; the row is read once in 16-byte loads and held in
+// registers (up to 256 * 4 * VMAX columns) between the sum of squares and the
+// scaled write.
+constexpr int kNormVmax = 8;
+
+template <class T>
+__device__ __forceinline__ void store4(T* p, float a, float b, float c, float e);
+template <>
+__device__ __forceinline__ void store4<float>(float* p, float a, float b, float c, float e) {
+  *reinterpret_cast<float4*>(p) = make_float4(a, b, c, e);
+}
+template <>
+__device__ __forceinline__ void store4<bf16_t>(bf16_t* p, float a, float b, float c, float e) {
+  uint2 w;
+  w.x = (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
+  w.y = (uint32_t)f2bf(c) | ((uint32_t)f2bf(e) << 16);
+  *reinterpret_cast<uint2*>(p) = w;
+}
+
 template <class T>
 __global__ void __launch_bounds__(256)
 rmsnorm_kernel(const float* __restrict__ x, const int* __restrict__ Mdev, int d, const float* __restrict__ g,
                T* __restrict__ out, const int* __restrict__ row_index) {
   __shared__ float red[4];
   const int M = *Mdev;
+  const int n4 = d >> 2;
   for (int r = blockIdx.x; r < M; r += gridDim.x) {
     const int src = row_index ? row_index[r] : r;
-    const float* xr = x + (size_t)src * d;
+    const float4* xr = reinterpret_cast<const float4*>(x + (size_t)src * d);
+    float4 v[kNormVmax];
     float ss = 0.f;
-    for (int c = threadIdx.x; c < d; c += 256) ss += xr[c] * xr[c];
+#pragma unroll
+    for (int k = 0; k < kNormVmax; ++k) {
+      const int c = threadIdx.x + k * 256;
+      v[k] = c < n4 ? xr[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+      ss += v[k].x * v[k].x + v[k].y * v[k].y + v[k].z * v[k].z + v[k].w * v[k].w;
+    }
     ss = block_sum256(ss, red);
     const float inv = rsqrtf(ss / (float)d + 1e-6f);
-    for (int c = threadIdx.x; c < d; c += 256) St<T>::st(out + (size_t)r * d + c, xr[c] * inv * g[c]);
+    const float4* g4 = reinterpret_cast<const float4*>(g);
+#pragma unroll
+    for (int k = 0; k < kNormVmax; ++k) {
+      const int c = threadIdx.x + k * 256;
+      if (c < n4) {
+        const float4 gg = g4[c];
+        store4<T>(out + (size_t)r * d + 4 * c, v[k].x * inv * gg.x, v[k].y * inv * gg.y, v[k].z * inv * gg.z,
+                  v[k].w * inv * gg.w);
+      }
+    }
   }
 }
 
 hipError_t rmsnorm(bool bf16, const float* x, const int* Mdev, int Mmax, int d, const float* g, void* out,
                    const int* row_index, hipStream_t st) {
+  if (d % 4 != 0 || d > 1024 * kNormVmax) return hipErrorInvalidValue;
   int blocks = std::max(1, std::min(Mmax, 8192));
   if (bf16) hipLaunchKernelGGL(rmsnorm_kernel<bf16_t>, dim3(blocks), dim3(256), 0, st, x, Mdev, d, g, (bf16_t*)out, row_index);
   else hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(blocks), dim3(256), 0, st, x, Mdev, d, g, (float*)out, row_index);

@@ -179,6 +179,7 @@ atspeed_status check_dims(const atspeed_model_dims& m, const atspeed_config& c, 
     if (dh != 32 && dh != 64 && dh != 128) return fail(ATSPEED_E_SHAPE, w + ": d_head must be 32, 64 or 128");
     if (m.d_model % 16 || m.d_ffn % 16) return fail(ATSPEED_E_SHAPE, w + ": d_model, d_ffn must be multiples of 16");
   }
+  if (m.d_model > 8192) return fail(ATSPEED_E_SHAPE, w + ": d_model above 8192 (row kernels hold a row in registers)");
   if (m.item_base < 0 || m.vocab < m.item_base + c.L * c.codebook)
     return fail(ATSPEED_E_SHAPE, w + ": vocab must hold item_base + L*codebook tokens");
   return ATSPEED_OK;
