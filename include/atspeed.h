@@ -183,7 +183,12 @@ ATSPEED_API atspeed_status atspeed_get_tree(atspeed_ctx* ctx, atspeed_tree* out)
  * (t, beams, scores).  accepted_dev / t_after_dev: [B] int32 (device, nullable).
  * logits_dev (nullable): [B, max_nodes, L*codebook] fp32 target item logits of
  * every forwarded node by slot.  Synchronises the stream (reads back one status
- * word): ATSPEED_E_INVALID if the tree is malformed (state then unchanged). */
+ * word): ATSPEED_E_INVALID if the tree is malformed (state then unchanged).  The
+ * tree is validated on the device before the forward: n_nodes within 0..max_nodes,
+ * level order, depths 1..L, each parent an earlier node one level up (-1 at depth
+ * 1), tokens the item tokens of their level, every path in the catalog, and (t > 0)
+ * every beam of Y_t a node of depth t.  A user whose tree fails any check forwards
+ * no rows, so a malformed tree never sends a kernel outside its buffers. */
 ATSPEED_API atspeed_status atspeed_verify(atspeed_ctx* ctx, int32_t* accepted_dev, int32_t* t_after_dev,
                               float* logits_dev);
 

@@ -65,11 +65,17 @@ __global__ void tree_index_kernel(TreeDev tr, TrieDev trie, StateDev s, int item
   const int u = blockIdx.x;
   const size_t tb = (size_t)u * tr.max_nodes;
   const int n = s.t[u] >= L ? 0 : tr.n_nodes[u];
-  __shared__ int nfwd;
-  if (threadIdx.x == 0) nfwd = n;
+  __shared__ int nfwd, bad;
+  if (threadIdx.x == 0) {
+    nfwd = n;
+    bad = 0;
+  }
   __syncthreads();
   if (n < 0 || n > tr.max_nodes) {
-    if (threadIdx.x == 0) atomicOr(err, 1);
+    if (threadIdx.x == 0) {
+      atomicOr(err, 1);
+      s.nfwd[u] = 0;   // nothing of this user is forwarded
+    }
     return;
   }
   for (int i = threadIdx.x; i < n; i += blockDim.x) {
@@ -91,13 +97,20 @@ __global__ void tree_index_kernel(TreeDev tr, TrieDev trie, StateDev s, int item
       if (node < 0) { ok = 0; break; }
       path = path_with(path, l - 1, code);
     }
-    if (!ok) { atomicOr(err, 1); continue; }
+    if (!ok) {
+      atomicOr(err, 1);
+      bad = 1;
+      continue;
+    }
     tr.tpath[tb + i] = path;
     tr.ttrie[tb + i] = node;
     if (dep == L) atomicMin(&nfwd, i);
   }
   __syncthreads();
-  if (threadIdx.x == 0) s.nfwd[u] = nfwd;
+  // A user whose tree has any malformed node forwards nothing: the row planner
+  // walks parents, depths and tokens of the forwarded nodes, and only
+  // validated ones keep those walks inside the tree and the tables.
+  if (threadIdx.x == 0) s.nfwd[u] = bad ? 0 : nfwd;
 }
 
 // Beam slots of Y_t in a caller tree (verify): every beam path must be a node of depth t.
@@ -107,6 +120,7 @@ __global__ void find_beam_slots_kernel(TreeDev tr, StateDev s, int L, int* err) 
   if (t <= 0 || t >= L) return;
   const size_t tb = (size_t)u * tr.max_nodes;
   const int n = tr.n_nodes[u];
+  if (n < 0 || n > tr.max_nodes) return;   // flagged by tree_index_kernel
   for (int k = threadIdx.x; k < s.nb[u]; k += blockDim.x) {
     const uint32_t p = s.path[u * s.K + k];
     int found = -1;
