@@ -63,10 +63,17 @@ struct Tile {
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
+// LDS swizzle of the 128-byte tile rows: logical 16-byte chunk c of row r sits
+// at physical chunk c ^ swz(r).  A fragment read has 16 lanes on 16 consecutive
+// rows in one LDS cycle, and a row covers half of the 64 banks, so the 8 even
+// rows must use 8 distinct chunks and so must the 8 odd ones: (r >> 1) & 7
+// does that (r & 7 would put rows r and r + 8 on the same banks).
+__device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
+
 // One k-tile (64 columns of A and W) into an LDS stage with direct global->LDS
 // DMA (global_load_lds_dwordx4): each wave instruction fills 1 KB = 8 rows of
 // 128 B; lane i lands at byte 16*i, i.e. row i/8, physical chunk i%8, and so
-// fetches logical chunk (i%8) ^ (row & 7) -- the XOR swizzle the fragment reads
+// fetches logical chunk (i%8) ^ swz(row) -- the XOR swizzle the fragment reads
 // undo.  No VGPRs hold the tile.
 template <int NA, int NB>
 __device__ __forceinline__ void load_stage(unsigned char* stage, int wave, const bf16_t* A, const int* a_off,
@@ -93,12 +100,12 @@ __device__ __forceinline__ void mma_stage(const unsigned char* stage, int wave_m
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
       const int r = wave_m * TM * 32 + i * 32 + fr;
-      a[i] = *reinterpret_cast<const bf16x8_t*>(stage + r * 128 + ((ch ^ (r & 7)) << 4));
+      a[i] = *reinterpret_cast<const bf16x8_t*>(stage + r * 128 + ((ch ^ swz(r)) << 4));
     }
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
       const int r = wave_n * TN * 32 + j * 32 + fr;
-      b[j] = *reinterpret_cast<const bf16x8_t*>(stage + a_bytes + r * 128 + ((ch ^ (r & 7)) << 4));
+      b[j] = *reinterpret_cast<const bf16x8_t*>(stage + a_bytes + r * 128 + ((ch ^ swz(r)) << 4));
     }
   };
   read(0, af[0], bfr[0]);
@@ -154,7 +161,7 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
   if (m0 >= M) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wave_m = wave / WN, wave_n = wave % WN;
-  const int lrow = lane >> 3, lchunk = (lane & 7) ^ (lrow & 7);
+  const int lrow = lane >> 3;
 
   // per-lane element offsets of the 16-byte chunks this lane fetches
   int a_off[NA], b_off[NB];
@@ -164,7 +171,7 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
     int r = (wave * NA + j) * 8 + lrow;
     int gr = m0 + r;
     gr = gr < M ? gr : M - 1;
-    a_off[j] = gr * lda + lchunk * 8;
+    a_off[j] = gr * lda + ((lane & 7) ^ swz(r)) * 8;
   }
   const bf16_t* B0;
   const bf16_t* B1 = nullptr;
@@ -191,7 +198,7 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
       row = row < N ? row : N - 1;
       if (BMAP == BMAP_QKV) row -= (tile_n * T::BN / b.split) * b.split;
     }
-    b_off[j] = row * K + lchunk * 8;
+    b_off[j] = row * K + ((lane & 7) ^ swz(r)) * 8;
   }
 
   f32x16_t acc[TM][TN];
