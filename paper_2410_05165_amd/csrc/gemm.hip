@@ -227,12 +227,17 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
     load_stage<NA, NB>(st0, wave, A, a_off, B0, B1, b_off, b_hi, 0, T::A_BYTES);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
+    // sched_barrier(0) after each DMA issue: left free, the scheduler sinks the
+    // DMA below the stage's MFMAs, right before the wait that ends the stage,
+    // and the load latency is exposed instead of hidden
     for (int kt = 0; kt < nk; kt += 2) {
       load_stage<NA, NB>(st1, wave, A, a_off, B0, B1, b_off, b_hi, (kt + 1) * 64, T::A_BYTES);
+      __builtin_amdgcn_sched_barrier(0);
       mma_stage<WM, WN, TM, TN>(st0, wave_m, wave_n, fr, fc, acc, T::A_BYTES);
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
       if (kt + 2 < nk) load_stage<NA, NB>(st0, wave, A, a_off, B0, B1, b_off, b_hi, (kt + 2) * 64, T::A_BYTES);
+      __builtin_amdgcn_sched_barrier(0);
       mma_stage<WM, WN, TM, TN>(st1, wave_m, wave_n, fr, fc, acc, T::A_BYTES);
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
@@ -252,6 +257,7 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
         if (kt + NS - 1 < nk)
           load_stage<NA, NB>(stage(std::integral_constant<int, s_ + NS - 1>{}), wave, A, a_off, B0, B1, b_off, b_hi,
                              (kt + NS - 1) * 64, T::A_BYTES);
+        __builtin_amdgcn_sched_barrier(0);
         mma_stage<WM, WN, TM, TN>(stage(S), wave_m, wave_n, fr, fc, acc, T::A_BYTES);
         // Own DMA of the next stage landed (only the newest stage may still be in
         // flight); the fragment reads of this stage were consumed by the MFMAs.
