@@ -262,9 +262,13 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
         // Own DMA of the next stage landed (only the newest stage may still be in
         // flight); the fragment reads of this stage were consumed by the MFMAs.
         // A bare barrier then orders both for every wave (a fenced __syncthreads
-        // would drain the newest stage's DMA too).
+        // would drain the newest stage's DMA too).  The barrier intrinsic does
+        // not order memory for the compiler, so empty asm with a memory clobber
+        // on both sides keeps the next stage's fragment reads and DMA below it.
+        asm volatile("" ::: "memory");
         __builtin_amdgcn_s_waitcnt(WAITCNT);
         __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
       }
     });
   }
