@@ -70,8 +70,10 @@ typedef struct {
   int32_t K;            /* target beam size (recommended items)                     */
   int32_t N;            /* draft beam size, N >= K                                  */
   int32_t gamma;        /* drafted levels per speculative step, >= 1                */
-  int32_t max_batch;    /* users per call                                           */
-  int32_t max_prefix;   /* prefix (history) tokens per user                         */
+  int32_t max_batch;    /* users per call, 1..1024                                  */
+  int32_t max_prefix;   /* prefix (history) tokens per user; max_batch x max(max_prefix,
+                           K*(L-1) + gamma*N) x max(d_model, d_ffn, L*codebook) must stay
+                           below 2^31 (ATSPEED_E_SHAPE otherwise)                    */
   int32_t mode;         /* atspeed_mode                                             */
   float temperature;    /* sampling temperature of the relaxed modes (> 0)          */
   uint64_t seed;        /* Philox key of the relaxed modes                          */

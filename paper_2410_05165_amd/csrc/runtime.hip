@@ -204,6 +204,13 @@ atspeed_status check_config(const atspeed_config* cfg) {
     ST_TRY(check_dims(c.draft, c, "draft"));
     if (c.draft.item_base != c.target.item_base) return fail(ATSPEED_E_SHAPE, "draft and target item_base differ");
   }
+  // Row offsets inside an activation matrix are 32-bit in the kernels: rows x
+  // widest row must stay below 2^31 elements.
+  const long long tmax = (long long)c.K * (c.L - 1) + (long long)c.gamma * c.N;
+  const long long rows = (long long)c.max_batch * std::max<long long>(c.max_prefix, tmax);
+  const long long width = std::max({c.target.d_model, c.target.d_ffn, c.draft.d_model, c.draft.d_ffn, 4 * c.codebook});
+  if (rows * width >= (1LL << 31))
+    return fail(ATSPEED_E_SHAPE, "max_batch x max(max_prefix, tree rows) x widest activation row must be below 2^31");
   return ATSPEED_OK;
 }
 

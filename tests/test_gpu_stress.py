@@ -1,0 +1,132 @@
+"""The stress workload at full size through the C ABI: 7B-shaped target, 1M
+catalog items, 128 users with 1,024-token prefixes, K = 50, N = 100.
+
+The oracle cannot forward this model at this size, so the test checks what
+holds at any size:
+* every user gets K decoded lists, each a catalog item, distinct, in
+  non-increasing score order;
+* losslessness on the device: the speculative decode returns bitwise the lists
+  of the GPU's own target-only beam search (verify on trees holding only Y_t);
+* batch invariance: the first 4 users decoded as a batch of 4 get bitwise the
+  lists they got in the batch of 128;
+* selection and acceptance on the GPU's t = 0 logits equal the oracle's
+  Algorithm 1 for sampled users (up to ties inside SEL_TIE).
+The model path at this width is checked against the oracle by the 7B test, and
+1,024-token prefixes by the 'longctx' variant.
+"""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+from _gpu_common import SEL_TIE, logit_table, upload_tree  # noqa: E402
+from synth import get_workload, make_catalog, make_prefixes, make_weights  # noqa: E402
+from oracle.search import verify_strict  # noqa: E402
+from oracle.trie import Trie  # noqa: E402
+
+DEV = "cuda:0"
+
+
+@pytest.fixture(scope="module")
+def stress():
+    from paper_2410_05165_amd.binding import Engine
+    w = get_workload("stress")
+    cat = make_catalog(w)
+    pre = make_prefixes(w, cat)
+    print(f"[stress] {len(cat)} items, prefixes {pre.shape}; generating weights", flush=True)
+    tw, dw = make_weights(w, "target"), make_weights(w, "draft")
+    eng = Engine(w, tw, dw, cat)
+    print(f"[stress] engine ready, workspace {eng.ws.numel() / 2**30:.1f} GiB", flush=True)
+    del tw, dw
+    yield dict(w=w, cat=cat, pre=pre, eng=eng)
+    eng.close()
+
+
+def _decode(eng, w, pre):
+    B = pre.shape[0]
+    prefix = torch.from_numpy(pre).to(DEV)
+    items = torch.zeros((B, w.K, w.L), dtype=torch.int32, device=DEV)
+    scores = torch.zeros((B, w.K), dtype=torch.float32, device=DEV)
+    n = torch.zeros(B, dtype=torch.int32, device=DEV)
+    eng.atspeed_decode_topk(prefix, items, scores, n, None)
+    torch.cuda.synchronize()
+    return items.cpu().numpy(), scores.cpu().numpy(), n.cpu().numpy()
+
+
+def _paths(tn, tt, tp, td, u, w):
+    paths = []
+    for i in range(tn[u]):
+        code = tt[u, i] - w.target.item_base - w.codebook * (td[u, i] - 1)
+        paths.append((paths[tp[u, i]] if tp[u, i] >= 0 else ()) + (int(code),))
+    return paths
+
+
+def test_stress_decode_lossless_and_batch_invariant(stress):
+    w, eng, pre, cat = stress["w"], stress["eng"], stress["pre"], stress["cat"]
+    print(f"[stress] decode_topk B={w.batch} P={w.prefix_len} K={w.K} N={w.N}", flush=True)
+    it, sc, nn = _decode(eng, w, pre)
+    catalog = set(map(tuple, cat.tolist()))
+    assert (nn == w.K).all(), nn
+    for u in range(w.batch):
+        lists = [tuple(int(c) for c in it[u, k]) for k in range(nn[u])]
+        assert len(set(lists)) == len(lists) and all(p in catalog for p in lists), u
+        assert (np.diff(sc[u, :nn[u]]) <= 0).all(), u
+    # GPU target-only beam search
+    print("[stress] target-only beam search on the GPU", flush=True)
+    eng.atspeed_prefill(torch.from_numpy(pre).to(DEV))
+    for _ in range(w.L):
+        t, nb, paths, _ = eng.atspeed_get_state(w.batch)
+        trees = [[tuple(int(c) for c in paths[u, k, :t[u]]) for k in range(nb[u])] if t[u] > 0 else []
+                 for u in range(w.batch)]
+        upload_tree(eng, trees, w.batch)
+        eng.atspeed_verify()
+    t, nb, paths, bsc = eng.atspeed_get_state(w.batch)
+    assert (t == w.L).all()
+    np.testing.assert_array_equal(nb, nn)
+    for u in range(w.batch):
+        np.testing.assert_array_equal(paths[u, :nb[u]], it[u, :nn[u]])
+        np.testing.assert_array_equal(bsc[u, :nb[u]], sc[u, :nn[u]])
+    # the first 4 users as a batch of their own
+    print("[stress] batch of 4", flush=True)
+    it4, sc4, nn4 = _decode(eng, w, pre[:4])
+    np.testing.assert_array_equal(nn4, nn[:4])
+    np.testing.assert_array_equal(it4, it[:4])
+    np.testing.assert_array_equal(sc4, sc[:4])
+
+
+def test_stress_selection_matches_algorithm_1(stress):
+    w, eng, pre, cat = stress["w"], stress["eng"], stress["pre"], stress["cat"]
+    root = torch.zeros((w.batch, w.n_item_tokens), dtype=torch.float32, device=DEV)
+    print("[stress] prefill + draft + tree logits", flush=True)
+    eng.atspeed_prefill(torch.from_numpy(pre).to(DEV), root)
+    eng.atspeed_draft()
+    logits = torch.zeros((w.batch, eng.max_nodes, w.n_item_tokens), dtype=torch.float32, device=DEV)
+    eng.atspeed_tree_logits(logits)
+    acc = torch.zeros(w.batch, dtype=torch.int32, device=DEV)
+    ta = torch.zeros(w.batch, dtype=torch.int32, device=DEV)
+    eng.atspeed_accept(logits, root, acc, ta)
+    torch.cuda.synchronize()
+    tn, tt, tp, td, _ = (x.cpu().numpy() for x in eng.tree_tensors(w.batch))
+    t, nb, sp, ssc = eng.atspeed_get_state(w.batch)
+    lg, r = logits.cpu().numpy(), root.cpu().numpy()
+    acc, ta = acc.cpu().numpy(), ta.cpu().numpy()
+    assert (tn == min(w.gamma, w.L) * w.N).all(), tn
+    print("[stress] oracle trie of 1M items", flush=True)
+    trie = Trie(cat)
+    ties = 0
+    for u in (0, 63, 127):
+        nodes = _paths(tn, tt, tp, td, u, w)
+        lp = logit_table(nodes, lg[u], r[u])
+        D = [[p for p in nodes if len(p) == d] for d in range(1, w.L + 1)]
+        log = []
+        res = verify_strict(lp, trie, [((), 0.0)], D, w.K, w.L, w.codebook, log)
+        got = [tuple(int(c) for c in sp[u, k, :t[u]]) for k in range(nb[u])]
+        print(f"[stress] user {u}: accepted {acc[u]} (oracle {res.accepted}), t -> {ta[u]}")
+        if got != [p for p, _ in res.beams] or acc[u] != res.accepted or ta[u] != res.t_after:
+            assert min(d.margin for d in log) < SEL_TIE
+            ties += 1
+            continue
+        np.testing.assert_allclose(ssc[u, :nb[u]], [s for _, s in res.beams], rtol=0, atol=1e-4)
+    assert ties < 3

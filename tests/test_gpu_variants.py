@@ -1,6 +1,6 @@
 """GPU parity on shape variants that the named workloads do not cover at small
 size: d_head 128 with a text-token prompt before the history (as the 7B shape
-has), several layers, a ragged tree."""
+has), several layers, a ragged tree, and 1,024-token prefixes."""
 import numpy as np
 import pytest
 
@@ -21,6 +21,10 @@ VARIANTS = {
     # 32 layers at d 1024: how the bf16 discrepancy grows with depth
     "deep": dict(target=ModelDims(32, 1024, 8, 2816, 2048, 1024), draft=ModelDims(2, 256, 4, 1024, 2048, 1024),
                  batch=2, prompt_len=16, hist_items=10, K=10, N=20, n_items=5000),
+    # 1,024-token prefixes (64-token prompt + 240 items, as the stress workload has) at d 256, d_head 128:
+    # 16 key tiles per attention workgroup, 16 causal query blocks in prefill
+    "longctx": dict(target=ModelDims(2, 256, 2, 512, 2048, 1024), draft=ModelDims(1, 256, 2, 512, 2048, 1024),
+                    batch=2, prompt_len=64, hist_items=240, K=10, N=20, n_items=5000),
 }
 
 
@@ -60,5 +64,5 @@ def test_variant_logits(var):
               f"(logit std {caches[u].last_logits.std():.3f})")
         worst = max(worst, e_root, e_tree)
     eng.close()
-    if var == "dh128":
+    if var in ("dh128", "longctx"):
         assert worst <= LOGIT_TOL["bf16"]
