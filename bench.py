@@ -161,6 +161,38 @@ def cpu_baseline(w, tw, pre, cat, tree_paths):
                        f"accepted={res.accepted}, host cpus={os.cpu_count()}"), res
 
 
+def decode_bound_probe(eng, w, prefix, levels, steps):
+    """Target-only beam step at t = 1 (the K beams of every user forwarded, K*B
+    rows): the weights and the prefix KV cache stream once per step with little
+    arithmetic per byte, so it is HBM-bound; reports its algorithmic bytes/s."""
+    import torch
+    B, K, L = w.batch, w.K, w.L
+    eng.atspeed_prefill(prefix)
+    t1, nb1, p1, s1 = levels[0]
+    upload_tree(eng, [[tuple(int(c) for c in p1[u, k, :1]) for k in range(nb1[u])] for u in range(B)], B)
+    rows = int(nb1.sum())
+
+    def step():
+        eng.atspeed_set_state(t1, nb1, p1, s1)
+        eng.atspeed_verify()
+    for _ in range(2):
+        step()
+    torch.cuda.synchronize()
+    a = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    ms = 1e3 * (time.perf_counter() - a) / steps
+    m = w.target
+    weights = m.n_layers * (4 * m.d_model ** 2 + 3 * m.d_model * m.d_ffn) * 2 + w.n_item_tokens * m.d_model * 2
+    kv = m.n_layers * 2 * B * w.prefix_len * m.d_model * 2
+    gbs = (weights + kv) / (ms * 1e-3) / 1e9
+    log(f"decode-bound probe: {rows} rows, {ms:.2f} ms/step, {gbs:.0f} GB/s ({gbs / PEAK_HBM_GBS:.1%} of HBM)")
+    return dict(rows=rows, ms_per_step=round(ms, 3), bytes=weights + kv, gbs=round(gbs, 1),
+                hbm_frac=round(gbs / PEAK_HBM_GBS, 4),
+                what="target-only beam step at t=1: target weights + prefix KV read once per step")
+
+
 def bench_decode(args, w, eng, pre, dev):
     """Relaxed workloads: a step is one whole decode (prefill, sampled drafting and
     relaxed verification until every user holds L-token items); the replay-tree
@@ -332,6 +364,8 @@ def main():
                     frac=round(gu["tflops"] / PEAK_BF16_TFLOPS, 4), traffic=gemm_traffic("gate/up GEMM"),
                     per_launch_flops=flops["gu"], avg_launch_ms=round(gu["avg_launch_ms"], 4))
 
+    probe = decode_bound_probe(eng, w, prefix, levels, max(3, args.steps // 2))
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu, _ = cpu_baseline(w, tw, pre, cat, trees[0])
@@ -361,6 +395,7 @@ def main():
                             mfma_frac=gemm_flops / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
                             ms_per_step=gemm_ms),
         "e2e_decode": e2e,
+        "decode_bound": probe,
     }
     print(json.dumps(out), flush=True)
     eng.close()

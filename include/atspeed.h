@@ -184,8 +184,10 @@ ATSPEED_API atspeed_status atspeed_get_tree(atspeed_ctx* ctx, atspeed_tree* out)
  * Algorithm 1; relaxed: Algorithm 2 per the configured mode).  Updates the state
  * (t, beams, scores).  accepted_dev / t_after_dev: [B] int32 (device, nullable).
  * logits_dev (nullable): [B, max_nodes, L*codebook] fp32 target item logits of
- * every forwarded node by slot.  Synchronises the stream (reads back one status
- * word): ATSPEED_E_INVALID if the tree is malformed (state then unchanged).  The
+ * every forwarded node by slot.  Synchronises the stream once, after tree
+ * planning and before the forward (reads back the validity word and the row
+ * counts that size the forward's launches): ATSPEED_E_INVALID if the tree is
+ * malformed (no forward runs; state unchanged).  The
  * tree is validated on the device before the forward: n_nodes within 0..max_nodes,
  * level order, depths 1..L, each parent an earlier node one level up (-1 at depth
  * 1), tokens the item tokens of their level, every path in the catalog, and (t > 0)

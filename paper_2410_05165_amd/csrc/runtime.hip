@@ -107,6 +107,7 @@ struct atspeed_ctx {
   int* row_last = nullptr;
   int* Mb = nullptr;         // [1] = B (rows of the last-position head in prefill)
   int* Mall = nullptr;       // [1] = B * Tmax (every tree slot)
+  int* plan_max = nullptr;   // [1] largest per-user row count of the last tree plan
   int* err = nullptr;
   int* acc_tmp = nullptr;
   int* tafter_tmp = nullptr;
@@ -343,6 +344,7 @@ void layout(atspeed_ctx& c, const atspeed_config& cfg, int trie_nodes, Arena& a)
   c.row_last = a.take<int>(B);
   c.Mb = a.take<int>(1);
   c.Mall = a.take<int>(1);
+  c.plan_max = a.take<int>(1);
   c.err = a.take<int>(1);
   c.acc_tmp = a.take<int>(B);
   c.tafter_tmp = a.take<int>(B);
@@ -474,9 +476,18 @@ atspeed_status tree_forward(atspeed_ctx& c, float* dbg_logits) {
   MARK(ATSPEED_K_SELECT);
   launch_tree_index(c.tree, c.trie, c.state, c.B, c.cfg.target.item_base, c.cfg.codebook, c.cfg.L, c.err, c.st);
   HIP_TRY(hipGetLastError());
-  launch_plan_tree(c.tree, c.lo, c.state.nfwd, c.B, c.P, c.rows, c.st);
+  launch_plan_tree(c.tree, c.lo, c.state.nfwd, c.B, c.P, c.rows, c.plan_max, c.st);
   HIP_TRY(hipGetLastError());
-  ST_TRY(forward(c, c.tgt, false, c.B * c.Tmax, c.Tmax, dbg_logits));
+  // One read-back per forward: the validity word, the row count and the largest
+  // per-user row count, so a malformed tree never reaches the forward and every
+  // launch of the forward is sized to the rows it has.
+  int info[3] = {0, 0, 0};
+  HIP_TRY(hipMemcpyAsync(&info[0], c.err, sizeof(int), hipMemcpyDeviceToHost, c.st));
+  HIP_TRY(hipMemcpyAsync(&info[1], c.rows.M, sizeof(int), hipMemcpyDeviceToHost, c.st));
+  HIP_TRY(hipMemcpyAsync(&info[2], c.plan_max, sizeof(int), hipMemcpyDeviceToHost, c.st));
+  HIP_TRY(hipStreamSynchronize(c.st));
+  if (info[0]) return fail(ATSPEED_E_INVALID, "malformed tree (code " + std::to_string(info[0]) + ")");
+  if (info[1] > 0) ST_TRY(forward(c, c.tgt, false, info[1], info[2], dbg_logits));
   return ATSPEED_OK;
 }
 
@@ -582,7 +593,7 @@ atspeed_status atspeed_draft(atspeed_ctx* c) {
   HIP_TRY(hipGetLastError());
   // draft log-probs along the Y_t paths (none at t = 0), then the beams' draft scores
   HIP_TRY(hipMemsetAsync(c->lo, 0, sizeof(int) * B, c->st));
-  launch_plan_tree(c->tree, c->lo, c->state.npath, B, c->P, c->rows, c->st);
+  launch_plan_tree(c->tree, c->lo, c->state.npath, B, c->P, c->rows, nullptr, c->st);
   HIP_TRY(hipGetLastError());
   ST_TRY(forward(*c, c->dft, false, B * c->Tmax, c->Tmax, nullptr));
   launch_draft_beam_scores(c->state, c->tree, c->dft.lp, c->dft.root, c->nitem, cf.codebook, L, B, c->st);
@@ -596,7 +607,7 @@ atspeed_status atspeed_draft(atspeed_ctx* c) {
                            cf.codebook, L, j, c->lvl_lo, c->lvl_hi, c->cand, c->max_cand, c->relax, B, c->st);
     HIP_TRY(hipGetLastError());
     if (j < std::min(cf.gamma, L)) {  // log-probs of the new level feed the next one
-      launch_plan_tree(c->tree, c->lvl_lo, c->lvl_hi, B, c->P, c->rows, c->st);
+      launch_plan_tree(c->tree, c->lvl_lo, c->lvl_hi, B, c->P, c->rows, nullptr, c->st);
       HIP_TRY(hipGetLastError());
       ST_TRY(forward(*c, c->dft, false, B * c->Tmax, c->Tmax, nullptr));
     }
@@ -620,9 +631,7 @@ atspeed_status atspeed_tree_logits(atspeed_ctx* c, float* logits) {
   if (!c || !logits) return fail(ATSPEED_E_INVALID, "null argument");
   if (!c->prefilled) return fail(ATSPEED_E_STATE, "tree_logits before prefill");
   ST_TRY(tree_forward(*c, logits));
-  int err = 0;
-  ST_TRY(read_err(*c, &err));
-  if (err) return fail(ATSPEED_E_INVALID, "malformed tree (code " + std::to_string(err) + ")");
+  HIP_TRY(hipStreamSynchronize(c->st));
   return ATSPEED_OK;
 }
 
@@ -648,9 +657,6 @@ atspeed_status atspeed_verify(atspeed_ctx* c, int32_t* accepted, int32_t* t_afte
   if (!c) return fail(ATSPEED_E_INVALID, "ctx is null");
   if (!c->prefilled) return fail(ATSPEED_E_STATE, "verify before prefill");
   ST_TRY(tree_forward(*c, logits));
-  int err = 0;
-  ST_TRY(read_err(*c, &err));
-  if (err) return fail(ATSPEED_E_INVALID, "malformed tree (code " + std::to_string(err) + ")");
   ST_TRY(accept_on(c, c->tgt.lp, c->tgt.root, accepted, t_after));
   c->drafted = false;
   return ATSPEED_OK;

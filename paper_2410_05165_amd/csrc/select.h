@@ -75,7 +75,10 @@ void launch_tree_from_beams(const StateDev& s, const TreeDev& tr, const TrieDev&
                             int codebook, int L, hipStream_t st);
 void launch_tree_index(const TreeDev& tr, const TrieDev& trie, const StateDev& s, int B, int item_base, int codebook,
                        int L, int* err, hipStream_t st);
-void launch_plan_tree(const TreeDev& tr, const int* lo, const int* hi, int B, int P, const Rows& rows, hipStream_t st);
+// Row plan of one forward: nodes with slot in [lo[u], hi[u]) of every user, users
+// in order; writes rows.M and (if maxrows) the largest per-user row count.
+void launch_plan_tree(const TreeDev& tr, const int* lo, const int* hi, int B, int P, const Rows& rows, int* maxrows,
+                      hipStream_t st);
 void launch_plan_prefix(const int* prefix, int B, int P, const Rows& rows, hipStream_t st);
 void launch_draft_beam_scores(const StateDev& s, const TreeDev& tr, const float* lpq, const float* rootq, int nitem,
                               int codebook, int L, int B, hipStream_t st);

@@ -132,18 +132,22 @@ __global__ void find_beam_slots_kernel(TreeDev tr, StateDev s, int L, int* err) 
 }
 
 // Rows of one forward: nodes with slot in [lo[u], hi[u]) of every user, users in order.
-__global__ void plan_tree_rows_kernel(TreeDev tr, const int* lo, const int* hi, int B, int P, Rows rows) {
+__global__ void plan_tree_rows_kernel(TreeDev tr, const int* lo, const int* hi, int B, int P, Rows rows,
+                                      int* maxrows) {
   __shared__ int off[1025];
   if (threadIdx.x == 0) {
-    int acc = 0;
+    int acc = 0, mx = 0;
     for (int u = 0; u < B; ++u) {
       off[u] = acc;
       rows.user_off[u] = acc;
-      acc += max(0, hi[u] - lo[u]);
+      const int n = max(0, hi[u] - lo[u]);
+      acc += n;
+      mx = max(mx, n);
     }
     off[B] = acc;
     rows.user_off[B] = acc;
     *rows.M = acc;
+    if (maxrows) *maxrows = mx;
   }
   __syncthreads();
   for (int u = 0; u < B; ++u) {
@@ -374,8 +378,9 @@ void launch_tree_index(const TreeDev& tr, const TrieDev& trie, const StateDev& s
   hipLaunchKernelGGL(tree_index_kernel, dim3(B), dim3(256), 0, st, tr, trie, s, item_base, codebook, L, err);
   hipLaunchKernelGGL(find_beam_slots_kernel, dim3(B), dim3(64), 0, st, tr, s, L, err);
 }
-void launch_plan_tree(const TreeDev& tr, const int* lo, const int* hi, int B, int P, const Rows& rows, hipStream_t st) {
-  hipLaunchKernelGGL(plan_tree_rows_kernel, dim3(1), dim3(1024), 0, st, tr, lo, hi, B, P, rows);
+void launch_plan_tree(const TreeDev& tr, const int* lo, const int* hi, int B, int P, const Rows& rows, int* maxrows,
+                      hipStream_t st) {
+  hipLaunchKernelGGL(plan_tree_rows_kernel, dim3(1), dim3(1024), 0, st, tr, lo, hi, B, P, rows, maxrows);
 }
 void launch_plan_prefix(const int* prefix, int B, int P, const Rows& rows, hipStream_t st) {
   int blocks = std::max(1, std::min(1024, (B * P + 255) / 256));
