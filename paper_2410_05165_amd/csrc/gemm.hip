@@ -1,8 +1,9 @@
 // Dense projections of the decoder block: Y[M, N] = X[M, K] · W[N, K]^T.
 //
 // bf16 path: MFMA v_mfma_f32_32x32x16_bf16 (fp32 accumulate), block tile
-// BM x BN x 64 fetched by direct global->LDS DMA into two LDS stages
-// (XOR-swizzled 16-byte chunks), wave tile TM x TN blocks of 32x32.  Epilogues are fused:
+// BM x BN x 64 fetched by direct global->LDS DMA into two or three LDS stages
+// (XOR-swizzled 16-byte chunks), wave tile TM x TN blocks of 32x32, tile shape
+// chosen by the row count.  Epilogues are fused:
 //   QKV   rotary embedding on q and k (rotate-half pairs sit in registers of the
 //         same lane: partner block tn ^ (d_head/64)), rounding to bf16, q to its
 //         row buffer, k/v scattered into the prefix cache or the tree KV buffer;
@@ -10,8 +11,8 @@
 //         blocks), out = bf16(SiLU(gate) * up);
 //   RESID residual stream x += acc (fp32);
 //   STORE fp32 logits.
-// M is read from device memory (the tree size is only known on the device);
-// tiles past it exit at once.
+// M is read from device memory; the grid covers the caller's row count or
+// bound (GemmCall::Mmax), and tiles past M exit at once.
 //
 // fp32 path (fp32 workloads): plain LDS-tiled FMA GEMM to a scratch matrix,
 // then an elementwise epilogue kernel with the same semantics.
@@ -140,7 +141,7 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
                  BArgs b, EpiArgs e) {
   using T = Tile<WM, WN, TM, TN>;
   constexpr int NW = WM * WN;
-  static_assert(NW == 4 || NW == 8, "four or eight waves");
+  static_assert(NW == 2 || NW == 4 || NW == 8, "two, four or eight waves");
   constexpr int NA = T::BM / (8 * NW);   // wave instructions per stage for A (8 rows of 128 B each)
   constexpr int NB = T::BN / (8 * NW);
   static_assert(NS == 2 || NS == 3, "two or three LDS stages");
@@ -222,6 +223,7 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
   constexpr int NLOADS = NA + NB;                 // DMA instructions per stage per lane
   constexpr int ALLOW = NLOADS * (NS - 2);        // loads that may stay in flight at a stage boundary
   constexpr int WAITCNT = (ALLOW & 0xF) | (((ALLOW >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8);
+  constexpr int WAITALL = (0x7 << 4) | (0xF << 8);  // vmcnt(0): every DMA of this wave landed
   if constexpr (NS == 2) {
     // nk is even (K % 128 == 0 is checked on the host): stages alternate st0, st1
     load_stage<NA, NB>(st0, wave, A, a_off, B0, B1, b_off, b_hi, 0, T::A_BYTES);
@@ -247,7 +249,10 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
     constexpr int s_ = decltype(S)::value;
     if (s_ < nk) load_stage<NA, NB>(stage(S), wave, A, a_off, B0, B1, b_off, b_hi, s_ * 64, T::A_BYTES);
   });
-  __builtin_amdgcn_s_waitcnt(WAITCNT);
+  // Stage 0 must have landed.  Leaving ALLOW loads in flight is only right when
+  // the later stages' loads were issued behind it; otherwise wait for all.
+  if (NS - 2 < nk) __builtin_amdgcn_s_waitcnt(WAITCNT);
+  else __builtin_amdgcn_s_waitcnt(WAITALL);
   __syncthreads();
   for (int kt0 = 0; kt0 < nk; kt0 += NS) {
     static_for<NS>([&](auto S) {
@@ -265,8 +270,11 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
         // would drain the newest stage's DMA too).  The barrier intrinsic does
         // not order memory for the compiler, so empty asm with a memory clobber
         // on both sides keeps the next stage's fragment reads and DMA below it.
+        // Near the end of k no newer stage was issued: then the next stage's DMA
+        // is the newest in flight and must be waited for in full.
         asm volatile("" ::: "memory");
-        __builtin_amdgcn_s_waitcnt(WAITCNT);
+        if (kt + NS - 1 < nk) __builtin_amdgcn_s_waitcnt(WAITCNT);
+        else __builtin_amdgcn_s_waitcnt(WAITALL);
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
       }
@@ -323,9 +331,12 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
     // buffers are free now), then written out in 16-byte chunks along rows.
     constexpr int OUTC = EPI == EPI_GU ? T::BN / 2 : T::BN;  // output columns of the tile
     constexpr int OROW = OUTC * 2;                            // bytes per LDS row
-    constexpr int HROWS = T::BM / 2;  // the first half of the tile rows goes to st0, the second to st1
-    constexpr int WMH = WM / 2;       // wave rows per half
-    static_assert(HROWS * OROW <= T::STAGE && WM % 2 == 0, "each half of the output tile fits a stage buffer");
+    // The whole output tile in st0 when it fits a stage buffer; otherwise its
+    // first half of rows in st0 and the second in st1.
+    constexpr bool ONEBUF = T::BM * OROW <= T::STAGE;
+    constexpr int HROWS = ONEBUF ? T::BM : T::BM / 2;
+    constexpr int WMH = ONEBUF ? WM : WM / 2;       // wave rows per buffer
+    static_assert(ONEBUF || (HROWS * OROW <= T::STAGE && WM % 2 == 0), "each half of the output tile fits a stage");
     bf16_t* ob = reinterpret_cast<bf16_t*>(wave_m < WMH ? st0 : st1);
     const int hrow0 = (wave_m % WMH) * TM * 32;
     if constexpr (EPI == EPI_GU) {
@@ -493,18 +504,17 @@ __global__ void epi_f32_kernel(const float* __restrict__ C, const int* __restric
 }
 
 // ------------------------------------------------------------------ launchers
-// 256x256 tiles for q/k/v and gate/up: 8 waves of 64x128 (two waves per SIMD,
-// so one wave's LDS and barrier waits hide behind the other's MFMAs).
+// Large batches: 256x256 tiles of 8 waves (64x128 each, two waves per SIMD, so
+// one wave's LDS and barrier waits hide behind the other's MFMAs) for the wide
+// projections (q/k/v, gate/up), 256x128 tiles of 8 waves (64x64) with three LDS
+// stages for the d_model-wide ones (o, down) and the output head.
 constexpr int kWideWM = 4, kWideTM = 2;
 #ifndef NARROW_WM
-#define NARROW_WM 4   // o / down / output head: 256x128 tiles of 8 waves (64x64 each), 3 LDS stages
+#define NARROW_WM 4
 #define NARROW_WN 2
 #define NARROW_TM 2
 #define NARROW_TN 2
 #endif
-// 256x256 tiles (4 waves of 128x128) for the wide projections (q/k/v, gate/up);
-// 128x256 tiles for the d_model-wide ones (o, down, output head), which keeps
-// their tile count near the CU count at a few thousand rows without split-K.
 template <int BMAP, int EPI, int WMW, int WNW, int TMW, int TNW, int NS>
 static hipError_t launch_bf16(const GemmCall& g, hipStream_t st) {
   using T = Tile<WMW, WNW, TMW, TNW>;
@@ -522,13 +532,32 @@ static hipError_t launch_bf16(const GemmCall& g, hipStream_t st) {
   return hipGetLastError();
 }
 
+// Tile shape by row count (measured on the 7B projections): few rows leave a
+// 256-row tile mostly empty and too few tiles for 256 CUs, so small batches take
+// 64-row tiles of two waves (and 64-wide ones for the d_model-wide products),
+// medium ones 128x128 tiles of four waves.  The shape does not change any
+// element's k-order, so results do not depend on it.  g.Mmax is the row count
+// of the call when the caller knows it, else an upper bound.
+constexpr int kSmallM = 512, kMidM = 1280;
+
 hipError_t gemm(const GemmCall& g, hipStream_t st) {
   if (g.bf16) {
+    const bool small = g.Mmax <= kSmallM, mid = g.Mmax <= kMidM;
     switch (g.kind) {
-      case GEMM_QKV: return launch_bf16<BMAP_QKV, EPI_QKV, kWideWM, 2, kWideTM, 4, 2>(g, st);
-      case GEMM_GU: return launch_bf16<BMAP_GU, EPI_GU, kWideWM, 2, kWideTM, 4, 2>(g, st);
-      case GEMM_RESID: return launch_bf16<BMAP_PLAIN, EPI_RESID, NARROW_WM, NARROW_WN, NARROW_TM, NARROW_TN, 3>(g, st);
-      default: return launch_bf16<BMAP_PLAIN, EPI_STORE, NARROW_WM, NARROW_WN, NARROW_TM, NARROW_TN, 3>(g, st);
+      case GEMM_QKV:
+        return small ? launch_bf16<BMAP_QKV, EPI_QKV, 1, 2, 2, 4, 3>(g, st)
+                     : launch_bf16<BMAP_QKV, EPI_QKV, kWideWM, 2, kWideTM, 4, 2>(g, st);
+      case GEMM_GU:
+        return small ? launch_bf16<BMAP_GU, EPI_GU, 1, 2, 2, 4, 2>(g, st)
+                     : launch_bf16<BMAP_GU, EPI_GU, kWideWM, 2, kWideTM, 4, 2>(g, st);
+      case GEMM_RESID:
+        return small ? launch_bf16<BMAP_PLAIN, EPI_RESID, 1, 2, 2, 1, 3>(g, st)
+             : mid   ? launch_bf16<BMAP_PLAIN, EPI_RESID, 2, 2, 2, 2, 3>(g, st)
+                     : launch_bf16<BMAP_PLAIN, EPI_RESID, NARROW_WM, NARROW_WN, NARROW_TM, NARROW_TN, 3>(g, st);
+      default:
+        return small ? launch_bf16<BMAP_PLAIN, EPI_STORE, 1, 2, 2, 1, 3>(g, st)
+             : mid   ? launch_bf16<BMAP_PLAIN, EPI_STORE, 2, 2, 2, 2, 3>(g, st)
+                     : launch_bf16<BMAP_PLAIN, EPI_STORE, NARROW_WM, NARROW_WN, NARROW_TM, NARROW_TN, 3>(g, st);
     }
   }
   // fp32: raw product into g.scratch (or straight into the logits), then the
