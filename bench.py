@@ -244,6 +244,7 @@ def main():
     ap.add_argument("--workload", default="b7")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-e2e", action="store_true")
+    ap.add_argument("--no-probe", action="store_true", help="skip the decode-bound probe (profiling runs)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one plain device copy of this size (HBM counter calibration)")
     args = ap.parse_args()
@@ -364,7 +365,7 @@ def main():
                     frac=round(gu["tflops"] / PEAK_BF16_TFLOPS, 4), traffic=gemm_traffic("gate/up GEMM"),
                     per_launch_flops=flops["gu"], avg_launch_ms=round(gu["avg_launch_ms"], 4))
 
-    probe = decode_bound_probe(eng, w, prefix, levels, max(3, args.steps // 2))
+    probe = None if args.no_probe else decode_bound_probe(eng, w, prefix, levels, max(3, args.steps // 2))
 
     cpu = None
     if not args.no_cpu_baseline:
