@@ -532,32 +532,61 @@ static hipError_t launch_bf16(const GemmCall& g, hipStream_t st) {
   return hipGetLastError();
 }
 
-// Tile shape by row count (measured on the 7B projections): few rows leave a
-// 256-row tile mostly empty and too few tiles for 256 CUs, so small batches take
-// 64-row tiles of two waves (and 64-wide ones for the d_model-wide products),
-// medium ones 128x128 tiles of four waves.  The shape does not change any
-// element's k-order, so results do not depend on it.  g.Mmax is the row count
-// of the call when the caller knows it, else an upper bound.
-constexpr int kSmallM = 512, kMidM = 1280;
+// Tile shape by row count.  A shape's cost is modelled as the number of rounds
+// of its tiles over the 256 CUs times the time of one round (per 4096 of k),
+// measured on MI355X at the 7B projections: few rows leave a 256-row tile
+// mostly empty and give too few tiles to fill the CUs, many rows favour the
+// large tiles' higher MFMA rate.  The shape does not change any element's
+// k-order, so results do not depend on it.  g.Mmax is the row count of the call
+// when the caller knows it, else an upper bound.
+namespace {
+constexpr int kCUs = 256;
+struct Shape { int bm, bn; float t_round; };
+// q/k/v, gate/up: 256x256 (8 waves) or 64x256 (2 waves)
+constexpr Shape kQkvShapes[] = {{256, 256, 124.f}, {64, 256, 50.f}};
+constexpr Shape kGuShapes[] = {{256, 256, 106.f}, {64, 256, 36.f}};
+// o, down, output head: 256x256, 256x128 (8 waves), 128x128 (4 waves), 64x64 (2 waves)
+constexpr Shape kRowShapes[] = {{256, 256, 101.f}, {256, 128, 72.f}, {128, 128, 44.5f}, {64, 64, 15.5f}};
+
+template <int NSH>
+int pick_shape(const Shape (&sh)[NSH], int M, int N, int K) {
+  int best = 0;
+  float best_cost = 0.f;
+  for (int i = 0; i < NSH; ++i) {
+    const long tiles = (long)((M + sh[i].bm - 1) / sh[i].bm) * ((N + sh[i].bn - 1) / sh[i].bn);
+    const float cost = (float)((tiles + kCUs - 1) / kCUs) * sh[i].t_round * (float)K / 4096.f;
+    if (i == 0 || cost < best_cost) { best = i; best_cost = cost; }
+  }
+  return best;
+}
+}  // namespace
 
 hipError_t gemm(const GemmCall& g, hipStream_t st) {
   if (g.bf16) {
-    const bool small = g.Mmax <= kSmallM, mid = g.Mmax <= kMidM;
+    const int M = g.Mmax > 0 ? g.Mmax : 1;
     switch (g.kind) {
       case GEMM_QKV:
-        return small ? launch_bf16<BMAP_QKV, EPI_QKV, 1, 2, 2, 4, 3>(g, st)
-                     : launch_bf16<BMAP_QKV, EPI_QKV, kWideWM, 2, kWideTM, 4, 2>(g, st);
+        return pick_shape(kQkvShapes, M, g.N, g.K) == 0
+                   ? launch_bf16<BMAP_QKV, EPI_QKV, kWideWM, 2, kWideTM, 4, 2>(g, st)
+                   : launch_bf16<BMAP_QKV, EPI_QKV, 1, 2, 2, 4, 2>(g, st);
       case GEMM_GU:
-        return small ? launch_bf16<BMAP_GU, EPI_GU, 1, 2, 2, 4, 2>(g, st)
-                     : launch_bf16<BMAP_GU, EPI_GU, kWideWM, 2, kWideTM, 4, 2>(g, st);
+        return pick_shape(kGuShapes, M, g.N, g.K) == 0
+                   ? launch_bf16<BMAP_GU, EPI_GU, kWideWM, 2, kWideTM, 4, 2>(g, st)
+                   : launch_bf16<BMAP_GU, EPI_GU, 1, 2, 2, 4, 2>(g, st);
       case GEMM_RESID:
-        return small ? launch_bf16<BMAP_PLAIN, EPI_RESID, 1, 2, 2, 1, 3>(g, st)
-             : mid   ? launch_bf16<BMAP_PLAIN, EPI_RESID, 2, 2, 2, 2, 3>(g, st)
-                     : launch_bf16<BMAP_PLAIN, EPI_RESID, NARROW_WM, NARROW_WN, NARROW_TM, NARROW_TN, 3>(g, st);
+        switch (pick_shape(kRowShapes, M, g.N, g.K)) {
+          case 0: return launch_bf16<BMAP_PLAIN, EPI_RESID, kWideWM, 2, kWideTM, 4, 2>(g, st);
+          case 1: return launch_bf16<BMAP_PLAIN, EPI_RESID, NARROW_WM, NARROW_WN, NARROW_TM, NARROW_TN, 3>(g, st);
+          case 2: return launch_bf16<BMAP_PLAIN, EPI_RESID, 2, 2, 2, 2, 3>(g, st);
+          default: return launch_bf16<BMAP_PLAIN, EPI_RESID, 1, 2, 2, 1, 3>(g, st);
+        }
       default:
-        return small ? launch_bf16<BMAP_PLAIN, EPI_STORE, 1, 2, 2, 1, 3>(g, st)
-             : mid   ? launch_bf16<BMAP_PLAIN, EPI_STORE, 2, 2, 2, 2, 3>(g, st)
-                     : launch_bf16<BMAP_PLAIN, EPI_STORE, NARROW_WM, NARROW_WN, NARROW_TM, NARROW_TN, 3>(g, st);
+        switch (pick_shape(kRowShapes, M, g.N, g.K)) {
+          case 0: return launch_bf16<BMAP_PLAIN, EPI_STORE, kWideWM, 2, kWideTM, 4, 2>(g, st);
+          case 1: return launch_bf16<BMAP_PLAIN, EPI_STORE, NARROW_WM, NARROW_WN, NARROW_TM, NARROW_TN, 3>(g, st);
+          case 2: return launch_bf16<BMAP_PLAIN, EPI_STORE, 2, 2, 2, 2, 3>(g, st);
+          default: return launch_bf16<BMAP_PLAIN, EPI_STORE, 1, 2, 2, 1, 3>(g, st);
+        }
     }
   }
   // fp32: raw product into g.scratch (or straight into the logits), then the
