@@ -357,30 +357,49 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
       const int halfdh = e.dh >> 1;
       const bool pair1 = halfdh == 32;       // partner block j^1 (d_head 64) or j^2 (d_head 128)
       const bool rot = col0 / e.d < 2;
+      // column j*32+fr of the wave's head-aligned span has rotary index (j*32+fr) mod halfdh
+      const int ci0 = fr & (halfdh - 1), ci1 = (32 + fr) & (halfdh - 1);
       static_for<TM>([&](auto I) {
         constexpr int i = decltype(I)::value;
-        static_for<16>([&](auto R) {
-          constexpr int r = decltype(R)::value;
-          const int hr = hrow0 + i * 32 + (r >> 2) * 8 + fc * 4 + (r & 3);  // row within this half
-          const int row = m0 + (wave_m < WMH ? 0 : HROWS) + hr;
-          const int pos = e.rows.pos[row < M ? row : M - 1];
-          const float* cb = e.cosT + pos * halfdh;
-          const float* sb = e.sinT + pos * halfdh;
-          // column j*32+fr of the wave's head-aligned span; its rotary index is (j*32+fr) mod halfdh
-          const float c0 = cb[fr & (halfdh - 1)], s0 = sb[fr & (halfdh - 1)];
-          const float c1 = cb[(32 + fr) & (halfdh - 1)], s1 = sb[(32 + fr) & (halfdh - 1)];
-#pragma unroll
-          for (int j = 0; j < TN; ++j) {
-            float v = acc[i][j][r];
-            if (rot) {
-              const float pv = pair1 ? acc[i][j ^ 1][r] : acc[i][j ^ 2][r];
-              const bool odd = (j & 1) != 0;
-              const float c = (pair1 || !odd) ? c0 : c1, sn = (pair1 || !odd) ? s0 : s1;
+        // rows in groups of 4: positions, then the cos/sin of the group, all issued
+        // before any is used (one memory latency per group, not per row); v
+        // columns take cos 1, sin 0 without a branch
+        static_for<4>([&](auto Q) {
+          constexpr int qg = decltype(Q)::value;
+          int pos[4];
+          static_for<4>([&](auto R) {
+            constexpr int r = decltype(R)::value;
+            const int hr = hrow0 + i * 32 + qg * 8 + fc * 4 + r;
+            const int row = m0 + (wave_m < WMH ? 0 : HROWS) + hr;
+            pos[r] = e.rows.pos[row < M ? row : M - 1];
+          });
+          float c0[4], s0[4], c1[4], s1[4];
+          static_for<4>([&](auto R) {
+            constexpr int r = decltype(R)::value;
+            const int base = rot ? pos[r] * halfdh : 0;
+            c0[r] = e.cosT[base + ci0]; s0[r] = e.sinT[base + ci0];
+            c1[r] = e.cosT[base + ci1]; s1[r] = e.sinT[base + ci1];
+          });
+          static_for<4>([&](auto R) {
+            constexpr int r = decltype(R)::value;
+            constexpr int ra = qg * 4 + r;     // accumulator register of this row
+            const int hr = hrow0 + i * 32 + qg * 8 + fc * 4 + r;
+            const float cc0 = rot ? c0[r] : 1.f, ss0 = rot ? s0[r] : 0.f;
+            const float cc1 = rot ? c1[r] : 1.f, ss1 = rot ? s1[r] : 0.f;
+            static_for<TN>([&](auto J) {
+              constexpr int j = decltype(J)::value;
+              constexpr bool odd = (j & 1) != 0;
+              const float v = acc[i][j][ra];
+              const float pv = pair1 ? acc[i][j ^ 1][ra] : acc[i][j ^ 2][ra];
+              const float c = (pair1 || !odd) ? cc0 : cc1, sn = (pair1 || !odd) ? ss0 : ss1;
               const bool lo = pair1 ? !odd : j < 2;   // first half of the head
-              v = lo ? v * c - pv * sn : v * c + pv * sn;
-            }
-            ob[hr * OUTC + wave_n * TN * 32 + j * 32 + fr] = f2bf(v);
-          }
+              // explicit fma of a rounded product: the same arithmetic in every
+              // tile shape (free contraction may differ between instantiations,
+              // and rows must not depend on the shape their batch got)
+              const float ps = pv * sn;
+              ob[hr * OUTC + wave_n * TN * 32 + j * 32 + fr] = f2bf(__builtin_fmaf(v, c, lo ? -ps : ps));
+            });
+          });
         });
       });
     }
