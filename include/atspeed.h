@@ -162,7 +162,10 @@ ATSPEED_API const char* atspeed_last_error(void);
 
 /* Prefill: one causal forward of the target (and draft) over B prefixes of P
  * tokens each (prefix_dev [B, P] int32, device), filling the prefix KV caches and
- * the root log-probs (logits at the last prefix position).  Resets every user to
+ * the root log-probs (logits at the last prefix position).  Positions that all
+ * users share with user 0 (a common prompt; found on the device, one read-back)
+ * are forwarded once and their K/V copied to the other users: the results are
+ * those of forwarding every position.  Resets every user to
  * item level t = 0 with the empty beam.  root_logits_dev (nullable): [B, L*codebook]
  * fp32 item logits of the target at the last prefix position.  Asynchronous. */
 ATSPEED_API atspeed_status atspeed_prefill(atspeed_ctx* ctx, int32_t B, int32_t P, const int32_t* prefix_dev,

@@ -107,7 +107,8 @@ struct atspeed_ctx {
   int* row_last = nullptr;
   int* Mb = nullptr;         // [1] = B (rows of the last-position head in prefill)
   int* Mall = nullptr;       // [1] = B * Tmax (every tree slot)
-  int* plan_max = nullptr;   // [1] largest per-user row count of the last tree plan
+  int* plan_max = nullptr;   // [1] largest per-user row count of the last tree plan (scratch word)
+  int shared_prefix = 0;     // prefix positions the users of the last prefill shared
   int* err = nullptr;
   int* acc_tmp = nullptr;
   int* tafter_tmp = nullptr;
@@ -397,7 +398,7 @@ atspeed_status upload_rope(atspeed_ctx& c, ModelRt& r) {
 // One decoder forward over the planned rows.  prefill: K/V into the prefix cache,
 // log-probs at each user's last position into r.root; else K/V into the tree
 // buffer and log-probs into r.lp by tree slot (logits copied to dbg if given).
-atspeed_status forward(atspeed_ctx& c, ModelRt& r, bool prefill, int Mmax, int Tq, float* dbg) {
+atspeed_status forward(atspeed_ctx& c, ModelRt& r, bool prefill, int Mmax, int Tq, float* dbg, int shared = 0) {
   const atspeed_model_dims& m = r.dims;
   const int d = m.d_model, f = m.d_ffn, H = m.n_heads, dh = r.dh();
   const int B = c.B, P = c.P;
@@ -425,6 +426,10 @@ atspeed_status forward(atspeed_ctx& c, ModelRt& r, bool prefill, int Mmax, int T
     g.vdst = prefill ? (void*)pv : (void*)tv;
     MARK(ATSPEED_K_QKV);
     HIP_TRY(gemm(g, st));
+    if (prefill && shared > 0 && B > 1) {  // users 1..B-1 take user 0's K/V of the shared positions
+      launch_broadcast_prefix_kv(pk, pv, B, H, (size_t)c.cfg.max_prefix * dh * es, (size_t)shared * dh * es, st);
+      HIP_TRY(hipGetLastError());
+    }
     AttnCall at{};
     at.bf16 = c.bf16; at.q = c.q; at.pk = pk; at.pv = pv;
     at.tk = prefill ? nullptr : tk; at.tv = prefill ? nullptr : tv;
@@ -563,15 +568,30 @@ atspeed_status atspeed_prefill(atspeed_ctx* c, int32_t B, int32_t P, const int32
   if (P < 1 || P > c->cfg.max_prefix) return fail(ATSPEED_E_SHAPE, "P out of range");
   c->B = B;
   c->P = P;
+  // Positions every user shares with user 0 (a common prompt) are forwarded
+  // once: user 0 computes them, the others copy its K/V.  Their hidden states
+  // depend only on those tokens, and a row's results do not depend on its batch,
+  // so the caches and logits are the same as with every row forwarded.  Each
+  // user keeps at least its last position (its root logits).
+  int S = 0;
+  if (B > 1) {
+    launch_common_prefix(prefix, B, P, c->plan_max, c->st);
+    HIP_TRY(hipGetLastError());
+    HIP_TRY(hipMemcpyAsync(&S, c->plan_max, sizeof(int), hipMemcpyDeviceToHost, c->st));
+    HIP_TRY(hipStreamSynchronize(c->st));
+    S = std::min(S, P - 1);
+  }
+  const int M = P + (B - 1) * (P - S);
   std::vector<int> last(B), sizes{B, B * c->Tmax};
-  for (int u = 0; u < B; ++u) last[u] = u * P + P - 1;
+  for (int u = 0; u < B; ++u) last[u] = u == 0 ? P - 1 : P + u * (P - S) - 1;
   HIP_TRY(hipMemcpyAsync(c->row_last, last.data(), B * 4, hipMemcpyHostToDevice, c->st));
   HIP_TRY(hipMemcpyAsync(c->Mb, &sizes[0], 4, hipMemcpyHostToDevice, c->st));
   HIP_TRY(hipMemcpyAsync(c->Mall, &sizes[1], 4, hipMemcpyHostToDevice, c->st));
-  launch_plan_prefix(prefix, B, P, c->rows, c->st);
+  launch_plan_prefix(prefix, B, P, S, c->rows, c->st);
   HIP_TRY(hipGetLastError());
-  ST_TRY(forward(*c, c->tgt, true, B * P, P, root_logits));
-  if (c->dft.present) ST_TRY(forward(*c, c->dft, true, B * P, P, nullptr));
+  ST_TRY(forward(*c, c->tgt, true, M, P, root_logits, S));
+  if (c->dft.present) ST_TRY(forward(*c, c->dft, true, M, P, nullptr, S));
+  c->shared_prefix = S;
   HIP_TRY(hipMemsetAsync(c->state.t, 0, sizeof(int) * B, c->st));
   HIP_TRY(hipMemsetAsync(c->state.steps, 0, sizeof(int) * B, c->st));
   std::vector<int> ones(B, 1);

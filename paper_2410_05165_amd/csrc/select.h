@@ -79,7 +79,14 @@ void launch_tree_index(const TreeDev& tr, const TrieDev& trie, const StateDev& s
 // in order; writes rows.M and (if maxrows) the largest per-user row count.
 void launch_plan_tree(const TreeDev& tr, const int* lo, const int* hi, int B, int P, const Rows& rows, int* maxrows,
                       hipStream_t st);
-void launch_plan_prefix(const int* prefix, int B, int P, const Rows& rows, hipStream_t st);
+// Prefill rows sharing the first S positions: the longest prefix all users have
+// in common is computed on the device (launch_common_prefix); user 0 forwards all
+// P positions, the others P - S, and their first S K/V rows are user 0's
+// (launch_broadcast_prefix_kv, once per layer after the K/V projection).
+void launch_common_prefix(const int* prefix, int B, int P, int* out, hipStream_t st);
+void launch_plan_prefix(const int* prefix, int B, int P, int S, const Rows& rows, hipStream_t st);
+void launch_broadcast_prefix_kv(void* pk, void* pv, int B, int H, size_t head_bytes, size_t shared_bytes,
+                                hipStream_t st);
 void launch_draft_beam_scores(const StateDev& s, const TreeDev& tr, const float* lpq, const float* rootq, int nitem,
                               int codebook, int L, int B, hipStream_t st);
 void launch_draft_select(const StateDev& s, const TreeDev& tr, const TrieDev& trie, const float* lpq,

@@ -172,19 +172,65 @@ __global__ void plan_tree_rows_kernel(TreeDev tr, const int* lo, const int* hi, 
   }
 }
 
-// Rows of the prefill: B users x P positions.
-__global__ void plan_prefix_rows_kernel(const int* prefix, int B, int P, Rows rows) {
-  const int total = B * P;
+// Length of the prefix every user shares with user 0 (tokens equal at every
+// position before it), at most P.
+__global__ void common_prefix_kernel(const int* prefix, int B, int P, int* out) {
+  __shared__ int len;
+  if (threadIdx.x == 0) len = P;
+  __syncthreads();
+  const int total = (B - 1) * P;
+  for (int i = threadIdx.x; i < total; i += blockDim.x) {
+    const int u = 1 + i / P, p = i % P;
+    if (prefix[u * P + p] != prefix[p]) atomicMin(&len, p);
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) *out = len;
+}
+
+// Rows of the prefill: user 0 forwards positions 0..P-1, every other user only
+// S..P-1 (its first S positions are user 0's, whose K/V it copies).
+__global__ void plan_prefix_rows_kernel(const int* prefix, int B, int P, int S, Rows rows) {
+  const int own = P - S;
+  const int total = P + (B - 1) * own;
   for (int r = blockIdx.x * blockDim.x + threadIdx.x; r < total; r += gridDim.x * blockDim.x) {
-    const int u = r / P, p = r % P;
+    int u, p;
+    if (r < P) {
+      u = 0;
+      p = r;
+    } else {
+      const int q = r - P;
+      u = 1 + q / own;
+      p = S + q % own;
+    }
     rows.user[r] = u;
-    rows.token[r] = prefix[r];
+    rows.token[r] = prefix[u * P + p];
     rows.pos[r] = p;
     rows.slot[r] = -1;
     rows.nctx[r] = p + 1;
     rows.nanc[r] = 0;
-    if (p == 0) rows.user_off[u] = r;
-    if (r == 0) { rows.user_off[B] = total; *rows.M = total; }
+    if (r == 0) {
+      for (int v = 0; v < B; ++v) rows.user_off[v] = v == 0 ? 0 : P + (v - 1) * own;
+      rows.user_off[B] = total;
+      *rows.M = total;
+    }
+  }
+}
+
+// K/V of the first S positions of user 0 to users 1..B-1, one layer of the
+// prefix cache [user][head][Pmax][d_head] (16-byte chunks).
+__global__ void broadcast_prefix_kv_kernel(unsigned char* pk, unsigned char* pv, int B, int H, size_t head_bytes,
+                                           size_t shared_bytes) {
+  const size_t chunks = shared_bytes / 16;
+  const size_t per_user = (size_t)H * chunks;
+  const size_t total = (size_t)(B - 1) * per_user * 2;
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < total; i += (size_t)gridDim.x * blockDim.x) {
+    const size_t kv = i / ((size_t)(B - 1) * per_user), rest = i % ((size_t)(B - 1) * per_user);
+    const size_t u = 1 + rest / per_user, hc = rest % per_user;
+    const size_t h = hc / chunks, c = hc % chunks;
+    unsigned char* base = kv == 0 ? pk : pv;
+    const u32x4_t* src = reinterpret_cast<const u32x4_t*>(base + h * head_bytes) + c;
+    u32x4_t* dst = reinterpret_cast<u32x4_t*>(base + (u * H + h) * head_bytes) + c;
+    *dst = *src;
   }
 }
 
@@ -382,9 +428,20 @@ void launch_plan_tree(const TreeDev& tr, const int* lo, const int* hi, int B, in
                       hipStream_t st) {
   hipLaunchKernelGGL(plan_tree_rows_kernel, dim3(1), dim3(1024), 0, st, tr, lo, hi, B, P, rows, maxrows);
 }
-void launch_plan_prefix(const int* prefix, int B, int P, const Rows& rows, hipStream_t st) {
-  int blocks = std::max(1, std::min(1024, (B * P + 255) / 256));
-  hipLaunchKernelGGL(plan_prefix_rows_kernel, dim3(blocks), dim3(256), 0, st, prefix, B, P, rows);
+void launch_common_prefix(const int* prefix, int B, int P, int* out, hipStream_t st) {
+  hipLaunchKernelGGL(common_prefix_kernel, dim3(1), dim3(1024), 0, st, prefix, B, P, out);
+}
+void launch_plan_prefix(const int* prefix, int B, int P, int S, const Rows& rows, hipStream_t st) {
+  const int total = P + (B - 1) * (P - S);
+  int blocks = std::max(1, std::min(1024, (total + 255) / 256));
+  hipLaunchKernelGGL(plan_prefix_rows_kernel, dim3(blocks), dim3(256), 0, st, prefix, B, P, S, rows);
+}
+void launch_broadcast_prefix_kv(void* pk, void* pv, int B, int H, size_t head_bytes, size_t shared_bytes,
+                                hipStream_t st) {
+  const size_t total = (size_t)(B - 1) * H * (shared_bytes / 16) * 2;
+  const int blocks = (int)std::max<size_t>(1, std::min<size_t>(4096, (total + 255) / 256));
+  hipLaunchKernelGGL(broadcast_prefix_kv_kernel, dim3(blocks), dim3(256), 0, st, (unsigned char*)pk,
+                     (unsigned char*)pv, B, H, head_bytes, shared_bytes);
 }
 void launch_draft_beam_scores(const StateDev& s, const TreeDev& tr, const float* lpq, const float* rootq, int nitem,
                               int codebook, int L, int B, hipStream_t st) {

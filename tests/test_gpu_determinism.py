@@ -73,3 +73,32 @@ def test_reproducible_after_other_context():
             eng.close()
     finally:
         other.close()
+
+
+def test_shared_prompt_prefill_is_exact():
+    """Users that share a prompt forward it once (user 0) and copy its K/V; the
+    root logits must equal bitwise those of each user prefilled alone."""
+    from paper_2410_05165_amd.binding import Engine
+    from synth import ModelDims, get_workload, make_catalog, make_prefixes, make_weights
+    # text tokens below item_base 1024 form the shared prompt
+    w = get_workload("small").with_(name="small_prompt", target=ModelDims(2, 512, 4, 1024, 2048, 1024),
+                                    draft=ModelDims(1, 256, 2, 512, 2048, 1024), batch=4, prompt_len=24,
+                                    hist_items=10, n_items=5000)
+    cat = make_catalog(w)
+    pre = make_prefixes(w, cat)
+    assert (pre[:, :w.prompt_len] == pre[0, :w.prompt_len]).all()
+    eng = Engine(w, make_weights(w, "target"), make_weights(w, "draft"), cat)
+    try:
+        root = torch.zeros((w.batch, w.n_item_tokens), dtype=torch.float32, device=DEV)
+        eng.atspeed_prefill(torch.from_numpy(pre).to(DEV), root)
+        torch.cuda.synchronize()
+        together = root.cpu().numpy()
+        for u in range(w.batch):
+            one = torch.zeros((1, w.n_item_tokens), dtype=torch.float32, device=DEV)
+            eng.atspeed_prefill(torch.from_numpy(pre[u:u + 1].copy()).to(DEV), one)
+            torch.cuda.synchronize()
+            print(f"[det] user {u}: shared-prompt prefill vs alone, max|diff| "
+                  f"{np.abs(together[u] - one.cpu().numpy()[0]).max():.1e}", flush=True)
+            np.testing.assert_array_equal(together[u], one.cpu().numpy()[0])
+    finally:
+        eng.close()
