@@ -27,6 +27,7 @@ enum { BMAP_PLAIN = 0, BMAP_QKV = 1, BMAP_GU = 2 };
 struct EpiArgs {
   float* out;        // STORE: [M, ldo] fp32; RESID: residual [M, ldo] fp32
   int ldo;
+  float* part;       // RESID split in k: the second half's product [M, ldo] fp32 (null: no split)
   bf16_t* hout;      // GU: [M, f] bf16
   // QKV
   bf16_t* q;         // [M, d]
@@ -152,11 +153,18 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
   // XCD-aware tile order: workgroup L is dispatched to XCD L % 8; XCD x owns the
   // contiguous range x*per .. x*per+per-1 of the tiles in N-major order, so the
   // M-tiles that share a weight tile run together on one XCD and share its L2.
+  // A RESID call with e.part splits k in two halves at K/2 for every row count
+  // (so a row's arithmetic never depends on the batch): workgroups of the
+  // first half add their product into the residual, those of the second store
+  // theirs into e.part, and the next row kernel adds the two.
+  const int kparts = (EPI == EPI_RESID && e.part != nullptr) ? 2 : 1;
   const int Nt = (N + T::BN - 1) / T::BN;
-  const int ntiles = Mt * Nt, per = (ntiles + 7) >> 3;
+  const int tiles1 = Mt * Nt, ntiles = tiles1 * kparts, per = (ntiles + 7) >> 3;
   const int L = blockIdx.x;
-  const int t = (L & 7) * per + (L >> 3);
-  if (t >= ntiles) return;
+  const int tk = (L & 7) * per + (L >> 3);
+  if (tk >= ntiles) return;
+  const int ks = tk / tiles1, t = tk - ks * tiles1;
+  const int kbase = ks * (K / kparts);
   const int tile_n = t / Mt, tile_m = t - tile_n * Mt;
   const int m0 = tile_m * T::BM;
   if (m0 >= M) return;
@@ -172,7 +180,7 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
     int r = (wave * NA + j) * 8 + lrow;
     int gr = m0 + r;
     gr = gr < M ? gr : M - 1;
-    a_off[j] = gr * lda + ((lane & 7) ^ swz(r)) * 8;
+    a_off[j] = gr * lda + kbase + ((lane & 7) ^ swz(r)) * 8;
   }
   const bf16_t* B0;
   const bf16_t* B1 = nullptr;
@@ -199,7 +207,7 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
       row = row < N ? row : N - 1;
       if (BMAP == BMAP_QKV) row -= (tile_n * T::BN / b.split) * b.split;
     }
-    b_off[j] = row * K + ((lane & 7) ^ swz(r)) * 8;
+    b_off[j] = row * K + kbase + ((lane & 7) ^ swz(r)) * 8;
   }
 
   f32x16_t acc[TM][TN];
@@ -210,7 +218,7 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  const int nk = K / T::BK;
+  const int nk = K / kparts / T::BK;
   const int fr = lane & 31, fc = lane >> 5;
   // NS-stage pipeline: stage s of round kt0 computes k-tile kt0+s while the
   // DMA of k-tile kt0+s+NS-1 is in flight; each stage is its own LDS array and
@@ -294,36 +302,46 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
     // wait for every store before the next one.  RESID loads all TN x 16
     // residual values of a 32-row block before it adds and stores them.
     const int mrows = M - m0 < T::BM ? M - m0 : T::BM;
+    const bool add_old = EPI == EPI_RESID && ks == 0;   // the k-split's second half stores its product alone
     const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-        e.out + (size_t)m0 * e.ldo, 0, mrows * e.ldo * (int)sizeof(float), 0x00020000);
+        (ks == 0 ? e.out : e.part) + (size_t)m0 * e.ldo, 0, mrows * e.ldo * (int)sizeof(float), 0x00020000);
     const int lrow0 = wave_m * TM * 32;
+    // byte offset = row part + column part; a column >= N gets a 1 GiB column
+    // part, past the range of any tile's rows
+    int coff[TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int col = col0 + j * 32 + fr;
+      coff[j] = col < N ? col * (int)sizeof(float) : (1 << 30);
+    }
     static_for<TM>([&](auto I) {
       constexpr int i = decltype(I)::value;
-      int off[TN][16];
+      int roff[16];
       static_for<16>([&](auto R) {
         constexpr int r = decltype(R)::value;
-        const int lrow = lrow0 + i * 32 + (r >> 2) * 8 + fc * 4 + (r & 3);
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          const int col = col0 + j * 32 + fr;
-          off[j][r] = col < N ? (lrow * e.ldo + col) * (int)sizeof(float) : 0x7fffffff;
-        }
+        roff[r] = (lrow0 + i * 32 + (r >> 2) * 8 + fc * 4 + (r & 3)) * e.ldo * (int)sizeof(float);
       });
-      float old[TN][16];
-      if constexpr (EPI == EPI_RESID) {
-        static_for<16>([&](auto R) {
+      // residual values loaded for half a 32-row block at a time, all issued
+      // before any is used
+      static_for<2>([&](auto Hh) {
+        constexpr int h0 = decltype(Hh)::value * 8;
+        float old[TN][8];
+        if (add_old) {
+          static_for<8>([&](auto R) {
+            constexpr int r = decltype(R)::value;
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+              old[j][r] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, roff[h0 + r] + coff[j], 0, 0));
+          });
+        }
+        static_for<8>([&](auto R) {
           constexpr int r = decltype(R)::value;
 #pragma unroll
-          for (int j = 0; j < TN; ++j) old[j][r] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, off[j][r], 0, 0));
+          for (int j = 0; j < TN; ++j) {
+            const float v = add_old ? old[j][r] + acc[i][j][h0 + r] : acc[i][j][h0 + r];
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), rs, roff[h0 + r] + coff[j], 0, 0);
+          }
         });
-      }
-      static_for<16>([&](auto R) {
-        constexpr int r = decltype(R)::value;
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          const float v = EPI == EPI_RESID ? old[j][r] + acc[i][j][r] : acc[i][j][r];
-          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), rs, off[j][r], 0, 0);
-        }
       });
     });
   } else {
@@ -540,11 +558,15 @@ static hipError_t launch_bf16(const GemmCall& g, hipStream_t st) {
   BArgs b{(const bf16_t*)g.w0, (const bf16_t*)g.w1, (const bf16_t*)g.w2, g.split};
   EpiArgs e{};
   e.out = g.out; e.ldo = g.ldo; e.hout = (bf16_t*)g.hout;
+  e.part = EPI == EPI_RESID ? g.part : nullptr;
   e.q = (bf16_t*)g.q; e.kdst = (bf16_t*)g.kdst; e.vdst = (bf16_t*)g.vdst;
   e.cosT = g.cosT; e.sinT = g.sinT; e.rows = g.rows; e.kv_mode = g.kv_mode; e.Pmax = g.Pmax;
   e.d = g.d; e.dh = g.dh; e.H = g.H;
+  const int kparts = e.part ? 2 : 1;
+  // each k-range is whole k-tiles of 64, an even number of them for two stages
+  if (g.K % (kparts * 64 * (NS == 2 ? 2 : 1)) != 0) return hipErrorInvalidValue;
   const int Mt = (g.Mmax + T::BM - 1) / T::BM, Nt = (g.N + T::BN - 1) / T::BN;
-  const int per = (Mt * Nt + 7) / 8;
+  const int per = (kparts * Mt * Nt + 7) / 8;
   dim3 grid(8 * per);
   auto kern = gemm_bf16_kernel<WMW, WNW, TMW, TNW, BMAP, EPI, NS>;
   hipLaunchKernelGGL(kern, grid, dim3(T::NT), 0, st, (const bf16_t*)g.A, g.lda, g.Mdev, Mt, g.N, g.K, b, e);
@@ -552,28 +574,32 @@ static hipError_t launch_bf16(const GemmCall& g, hipStream_t st) {
 }
 
 // Tile shape by row count.  A shape's cost is modelled as the number of rounds
-// of its tiles over the 256 CUs times the time of one round (per 4096 of k),
-// measured on MI355X at the 7B projections: few rows leave a 256-row tile
-// mostly empty and give too few tiles to fill the CUs, many rows favour the
-// large tiles' higher MFMA rate.  The shape does not change any element's
-// k-order, so results do not depend on it.  g.Mmax is the row count of the call
-// when the caller knows it, else an upper bound.
+// of its tiles over the CUs (256 x the workgroups of that shape one CU holds)
+// times the time of one round, t0 + t4k x (k per workgroup) / 4096, fitted to
+// measurements on MI355X at the 7B projections for 320 to 2,236 rows: few rows
+// leave a 256-row tile mostly empty and give too few tiles to fill the CUs,
+// many rows favour the large tiles' higher MFMA rate, and in between the
+// better shape is the one whose last round is fuller.  The shape does not
+// change any element's k-order, so results do not depend on it.  g.Mmax is
+// the row count of the call when the caller knows it, else an upper bound.
 namespace {
 constexpr int kCUs = 256;
-struct Shape { int bm, bn; float t_round; };
-// q/k/v, gate/up: 256x256 (8 waves) or 64x256 (2 waves)
-constexpr Shape kQkvShapes[] = {{256, 256, 124.f}, {64, 256, 50.f}};
-constexpr Shape kGuShapes[] = {{256, 256, 106.f}, {64, 256, 36.f}};
+struct Shape { int bm, bn, per_cu; float t0, t4k; };
+// q/k/v, gate/up: 256x256 (8 waves), 128x256 (8 waves), 64x256 (2 waves, two per CU)
+constexpr Shape kQkvShapes[] = {{256, 256, 1, 0.f, 120.f}, {128, 256, 1, 0.f, 70.f}, {64, 256, 2, 0.f, 72.f}};
+constexpr Shape kGuShapes[] = {{256, 256, 1, 0.f, 102.f}, {128, 256, 1, 0.f, 63.f}, {64, 256, 2, 0.f, 66.f}};
 // o, down, output head: 256x256, 256x128 (8 waves), 128x128 (4 waves), 64x64 (2 waves)
-constexpr Shape kRowShapes[] = {{256, 256, 101.f}, {256, 128, 72.f}, {128, 128, 44.5f}, {64, 64, 15.5f}};
+constexpr Shape kRowShapes[] = {
+    {256, 256, 1, 19.8f, 98.4f}, {256, 128, 1, 10.6f, 62.8f}, {128, 128, 1, 5.3f, 41.7f}, {64, 64, 1, 2.f, 14.f}};
 
 template <int NSH>
-int pick_shape(const Shape (&sh)[NSH], int M, int N, int K) {
+int pick_shape(const Shape (&sh)[NSH], int M, int N, int K, int kparts = 1) {
   int best = 0;
   float best_cost = 0.f;
   for (int i = 0; i < NSH; ++i) {
-    const long tiles = (long)((M + sh[i].bm - 1) / sh[i].bm) * ((N + sh[i].bn - 1) / sh[i].bn);
-    const float cost = (float)((tiles + kCUs - 1) / kCUs) * sh[i].t_round * (float)K / 4096.f;
+    const long tiles = kparts * (long)((M + sh[i].bm - 1) / sh[i].bm) * ((N + sh[i].bn - 1) / sh[i].bn);
+    const long slots = (long)kCUs * sh[i].per_cu;
+    const float cost = (float)((tiles + slots - 1) / slots) * (sh[i].t0 + sh[i].t4k * (float)K / kparts / 4096.f);
     if (i == 0 || cost < best_cost) { best = i; best_cost = cost; }
   }
   return best;
@@ -585,15 +611,19 @@ hipError_t gemm(const GemmCall& g, hipStream_t st) {
     const int M = g.Mmax > 0 ? g.Mmax : 1;
     switch (g.kind) {
       case GEMM_QKV:
-        return pick_shape(kQkvShapes, M, g.N, g.K) == 0
-                   ? launch_bf16<BMAP_QKV, EPI_QKV, kWideWM, 2, kWideTM, 4, 2>(g, st)
-                   : launch_bf16<BMAP_QKV, EPI_QKV, 1, 2, 2, 4, 2>(g, st);
+        switch (pick_shape(kQkvShapes, M, g.N, g.K)) {
+          case 0: return launch_bf16<BMAP_QKV, EPI_QKV, kWideWM, 2, kWideTM, 4, 2>(g, st);
+          case 1: return launch_bf16<BMAP_QKV, EPI_QKV, 4, 2, 1, 4, 2>(g, st);
+          default: return launch_bf16<BMAP_QKV, EPI_QKV, 1, 2, 2, 4, 2>(g, st);
+        }
       case GEMM_GU:
-        return pick_shape(kGuShapes, M, g.N, g.K) == 0
-                   ? launch_bf16<BMAP_GU, EPI_GU, kWideWM, 2, kWideTM, 4, 2>(g, st)
-                   : launch_bf16<BMAP_GU, EPI_GU, 1, 2, 2, 4, 2>(g, st);
+        switch (pick_shape(kGuShapes, M, g.N, g.K)) {
+          case 0: return launch_bf16<BMAP_GU, EPI_GU, kWideWM, 2, kWideTM, 4, 2>(g, st);
+          case 1: return launch_bf16<BMAP_GU, EPI_GU, 4, 2, 1, 4, 2>(g, st);
+          default: return launch_bf16<BMAP_GU, EPI_GU, 1, 2, 2, 4, 2>(g, st);
+        }
       case GEMM_RESID:
-        switch (pick_shape(kRowShapes, M, g.N, g.K)) {
+        switch (pick_shape(kRowShapes, M, g.N, g.K, g.part ? 2 : 1)) {
           case 0: return launch_bf16<BMAP_PLAIN, EPI_RESID, kWideWM, 2, kWideTM, 4, 2>(g, st);
           case 1: return launch_bf16<BMAP_PLAIN, EPI_RESID, NARROW_WM, NARROW_WN, NARROW_TM, NARROW_TN, 3>(g, st);
           case 2: return launch_bf16<BMAP_PLAIN, EPI_RESID, 2, 2, 2, 2, 3>(g, st);

@@ -16,6 +16,7 @@ struct GemmCall {
   const void* w0; const void* w1; const void* w2;
   int split;                 // QKV: d_model; GU: d_ffn
   float* out; int ldo;       // STORE / RESID
+  float* part;               // bf16 RESID: k split at K/2; the second half's product [Mmax, ldo] fp32 goes here
   void* hout;                // GU output [M, f]
   void* q; void* kdst; void* vdst;
   const float* cosT; const float* sinT;
@@ -40,7 +41,9 @@ hipError_t attention(const AttnCall& a, hipStream_t st);
 
 // Misc
 hipError_t embed(bool bf16, const void* emb, const Rows& rows, int Mmax, int d, float* x, hipStream_t st);
-hipError_t rmsnorm(bool bf16, const float* x, const int* Mdev, int Mmax, int d, const float* g, void* out,
+// add (may be null): a k-split GEMM's second partial product, added to x first;
+// the sum is written back to x when row_index is null.
+hipError_t rmsnorm(bool bf16, float* x, const float* add, const int* Mdev, int Mmax, int d, const float* g, void* out,
                    const int* row_index, hipStream_t st);
 hipError_t log_softmax_rows(const float* logits, const int* Mdev, int Mmax, int n, const int* dst_index,
                             float* lp, float* logits_copy, hipStream_t st);

@@ -42,9 +42,11 @@ __device__ __forceinline__ float block_max256(float v, float* red) {
 }
 
 // out[r] = g * x[src] / sqrt(mean(x[src]^2) + eps), src = row_index ? row_index[r] : r.
-// One workgroup per row; the row is read once in 16-byte loads and held in
-// registers (up to 256 * 4 * VMAX columns) between the sum of squares and the
-// scaled write.
+// With add: x[src] + add[src] takes the place of x[src] (the second partial
+// product of a GEMM split in k), and without row_index that sum is written
+// back to x.  One workgroup per row; the row is read once in 16-byte loads and
+// held in registers (up to 256 * 4 * VMAX columns) between the sum of squares
+// and the scaled write.
 constexpr int kNormVmax = 8;
 
 template <class T>
@@ -63,20 +65,25 @@ __device__ __forceinline__ void store4<bf16_t>(bf16_t* p, float a, float b, floa
 
 template <class T>
 __global__ void __launch_bounds__(256)
-rmsnorm_kernel(const float* __restrict__ x, const int* __restrict__ Mdev, int d, const float* __restrict__ g,
-               T* __restrict__ out, const int* __restrict__ row_index) {
+rmsnorm_kernel(float* __restrict__ x, const float* __restrict__ add, const int* __restrict__ Mdev, int d,
+               const float* __restrict__ g, T* __restrict__ out, const int* __restrict__ row_index) {
   __shared__ float red[4];
   const int M = *Mdev;
   const int n4 = d >> 2;
   for (int r = blockIdx.x; r < M; r += gridDim.x) {
     const int src = row_index ? row_index[r] : r;
-    const float4* xr = reinterpret_cast<const float4*>(x + (size_t)src * d);
+    const float4* xr = reinterpret_cast<const float4*>(x + (size_t)src * d);  // read once, before any write-back
     float4 v[kNormVmax];
     float ss = 0.f;
 #pragma unroll
     for (int k = 0; k < kNormVmax; ++k) {
       const int c = threadIdx.x + k * 256;
       v[k] = c < n4 ? xr[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+      if (add && c < n4) {
+        const float4 p = reinterpret_cast<const float4*>(add + (size_t)src * d)[c];
+        v[k].x += p.x; v[k].y += p.y; v[k].z += p.z; v[k].w += p.w;
+        if (!row_index) reinterpret_cast<float4*>(x + (size_t)src * d)[c] = v[k];
+      }
       ss += v[k].x * v[k].x + v[k].y * v[k].y + v[k].z * v[k].z + v[k].w * v[k].w;
     }
     ss = block_sum256(ss, red);
@@ -94,12 +101,14 @@ rmsnorm_kernel(const float* __restrict__ x, const int* __restrict__ Mdev, int d,
   }
 }
 
-hipError_t rmsnorm(bool bf16, const float* x, const int* Mdev, int Mmax, int d, const float* g, void* out,
+hipError_t rmsnorm(bool bf16, float* x, const float* add, const int* Mdev, int Mmax, int d, const float* g, void* out,
                    const int* row_index, hipStream_t st) {
   if (d % 4 != 0 || d > 1024 * kNormVmax) return hipErrorInvalidValue;
   int blocks = std::max(1, std::min(Mmax, 8192));
-  if (bf16) hipLaunchKernelGGL(rmsnorm_kernel<bf16_t>, dim3(blocks), dim3(256), 0, st, x, Mdev, d, g, (bf16_t*)out, row_index);
-  else hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(blocks), dim3(256), 0, st, x, Mdev, d, g, (float*)out, row_index);
+  if (bf16)
+    hipLaunchKernelGGL(rmsnorm_kernel<bf16_t>, dim3(blocks), dim3(256), 0, st, x, add, Mdev, d, g, (bf16_t*)out, row_index);
+  else
+    hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(blocks), dim3(256), 0, st, x, add, Mdev, d, g, (float*)out, row_index);
   return hipGetLastError();
 }
 

@@ -100,6 +100,7 @@ struct atspeed_ctx {
   void* h = nullptr;
   float* logits = nullptr;
   float* scratch = nullptr;
+  float* part = nullptr;      // bf16: second k-half of the o / down product [Mmax, d] fp32
   int* lo = nullptr;
   int* hi = nullptr;
   int* lvl_lo = nullptr;
@@ -308,6 +309,7 @@ void layout(atspeed_ctx& c, const atspeed_config& cfg, int trie_nodes, Arena& a)
   c.h = a.take<char>(M * fmax * es);
   c.logits = a.take<float>(M * c.nitem);
   c.scratch = c.bf16 ? nullptr : a.take<float>(M * std::max(3 * dmax, 2 * fmax));
+  c.part = c.bf16 ? a.take<float>(M * dmax) : nullptr;
   c.rows.M = a.take<int>(1);
   c.rows.user = a.take<int>(M);
   c.rows.token = a.take<int>(M);
@@ -406,10 +408,18 @@ atspeed_status forward(atspeed_ctx& c, ModelRt& r, bool prefill, int Mmax, int T
   hipStream_t st = c.st;
   MARK(ATSPEED_K_ROW);
   HIP_TRY(embed(c.bf16, r.emb, c.rows, Mmax, d, c.x, st));
+  // bf16: the o and down projections split k at its midpoint (whole even
+  // numbers of 64-column k-tiles), so 256x256 tiles fill the CUs at these
+  // widths; the first half adds into x, the second goes to c.part, and the
+  // next RMSNorm adds it and writes x back.  The split does not depend on the
+  // row count, so neither does any row's arithmetic.
+  float* part_o = c.bf16 && d % 256 == 0 ? c.part : nullptr;
+  float* part_down = c.bf16 && f % 256 == 0 ? c.part : nullptr;
   for (int l = 0; l < m.n_layers; ++l) {
     const void* const* w = &r.layers[(size_t)l * 9];
     MARK(ATSPEED_K_ROW);
-    HIP_TRY(rmsnorm(c.bf16, c.x, c.rows.M, Mmax, d, (const float*)w[0], c.xn, nullptr, st));
+    HIP_TRY(rmsnorm(c.bf16, c.x, l > 0 ? part_down : nullptr, c.rows.M, Mmax, d, (const float*)w[0], c.xn, nullptr,
+                    st));
     GemmCall g{};
     g.bf16 = c.bf16;
     g.Mmax = Mmax; g.Mdev = c.rows.M; g.scratch = c.scratch; g.rows = c.rows;
@@ -438,14 +448,16 @@ atspeed_status forward(atspeed_ctx& c, ModelRt& r, bool prefill, int Mmax, int T
     MARK(ATSPEED_K_ATTN);
     HIP_TRY(attention(at, st));
     g.kind = GEMM_RESID; g.A = c.ao; g.lda = d; g.N = d; g.K = d; g.w0 = w[4]; g.out = c.x; g.ldo = d;
+    g.part = part_o;
     MARK(ATSPEED_K_O);
     HIP_TRY(gemm(g, st));
     MARK(ATSPEED_K_ROW);
-    HIP_TRY(rmsnorm(c.bf16, c.x, c.rows.M, Mmax, d, (const float*)w[5], c.xn, nullptr, st));
+    HIP_TRY(rmsnorm(c.bf16, c.x, part_o, c.rows.M, Mmax, d, (const float*)w[5], c.xn, nullptr, st));
     g.kind = GEMM_GU; g.A = c.xn; g.lda = d; g.N = 2 * f; g.K = d; g.w0 = w[6]; g.w1 = w[7]; g.split = f; g.hout = c.h;
     MARK(ATSPEED_K_GU);
     HIP_TRY(gemm(g, st));
     g.kind = GEMM_RESID; g.A = c.h; g.lda = f; g.N = d; g.K = f; g.w0 = w[8]; g.out = c.x; g.ldo = d;
+    g.part = part_down;
     MARK(ATSPEED_K_DOWN);
     HIP_TRY(gemm(g, st));
   }
@@ -453,7 +465,7 @@ atspeed_status forward(atspeed_ctx& c, ModelRt& r, bool prefill, int Mmax, int T
   const int* Mfin = prefill ? c.Mb : c.rows.M;
   const int Mmf = prefill ? B : Mmax;
   MARK(ATSPEED_K_ROW);
-  HIP_TRY(rmsnorm(c.bf16, c.x, Mfin, Mmf, d, r.final_norm, c.xn, prefill ? c.row_last : nullptr, st));
+  HIP_TRY(rmsnorm(c.bf16, c.x, part_down, Mfin, Mmf, d, r.final_norm, c.xn, prefill ? c.row_last : nullptr, st));
   GemmCall g{};
   g.kind = GEMM_STORE; g.bf16 = c.bf16; g.A = c.xn; g.lda = d; g.Mmax = Mmf; g.Mdev = Mfin;
   g.N = c.nitem; g.K = d; g.w0 = r.lm_head; g.out = c.logits; g.ldo = c.nitem; g.scratch = c.scratch;
