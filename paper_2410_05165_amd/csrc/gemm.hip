@@ -9,7 +9,11 @@
 //         row buffer, k/v scattered into the prefix cache or the tree KV buffer;
 //   GU    gate and up columns share a tile (first/second half of each wave's
 //         blocks), out = bf16(SiLU(gate) * up);
-//   RESID residual stream x += acc (fp32);
+//   RESID residual stream x += acc (fp32); with a partial buffer the k range
+//         is split at K/2 into two workgroups per tile, the first adding its
+//         product into x and the second storing its own into the buffer (the
+//         following RMSNorm adds it), so the o and down projections fill the
+//         CUs with 256x256 tiles;
 //   STORE fp32 logits.
 // M is read from device memory; the grid covers the caller's row count or
 // bound (GemmCall::Mmax), and tiles past M exit at once.
