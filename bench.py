@@ -209,7 +209,6 @@ def bench_decode(args, w, eng, pre, dev):
     for _ in range(args.warmup):
         eng.atspeed_decode_topk(prefix, items, scores, n, None)
     torch.cuda.synchronize()
-    eng.atspeed_set_timing(True)
     acc = np.zeros((L, B), np.int32)
     st = Stats()
     import ctypes as C
@@ -219,7 +218,13 @@ def bench_decode(args, w, eng, pre, dev):
         eng.atspeed_decode_topk(prefix, items, scores, n, st)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - a
+    # breakdown by kernel class: a separate pass with every launch bracketed
+    steps_kt = max(1, args.steps // 2)
+    eng.atspeed_set_timing(True)
+    for _ in range(steps_kt):
+        eng.atspeed_decode_topk(prefix, items, scores, n, None)
     kt = eng.atspeed_get_timing()
+    eng.atspeed_set_timing(False)
     value = B * args.steps / elapsed
     log(f"decode {1e3 * elapsed / args.steps:.1f} ms -> {value:.0f} lists/s; last decode steps {st.n_steps}")
     out = {"metric": "top-K lists/sec/GPU (relaxed sampling verification, whole decode)", "value": round(value, 2),
@@ -229,7 +234,7 @@ def bench_decode(args, w, eng, pre, dev):
            "config": {"workload": f"{w.name}: whole decode with {w.mode}, B={B}, P={w.prefix_len}, K={K}, N={w.N}, "
                                   f"gamma={w.gamma}, tau={w.temperature}", "global_batch": B, "seq_len": w.prefix_len,
                       "parallelism": "none (1 GPU)"},
-           "kernels": {k: dict(ms_per_step=v[0] / args.steps, launches_per_step=v[1] / args.steps)
+           "kernels": {k: dict(ms_per_step=v[0] / steps_kt, launches_per_step=v[1] / steps_kt)
                        for k, v in kt.items() if v[1]},
            "accepted_levels_last_decode": acc[:st.n_steps].tolist()}
     print(json.dumps(out), flush=True)
@@ -324,18 +329,27 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    eng.atspeed_set_timing(True)
+    # Timed region: HIP events bracket only the gate/up launches (the roofline
+    # kernel), since every event adds stream time.
+    eng.atspeed_set_timing(["gu"])
     torch.cuda.synchronize()
     a = time.perf_counter()
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - a
-    kt = eng.atspeed_get_timing()
+    kt_gu = eng.atspeed_get_timing()["gu"]
     eng.atspeed_set_timing(False)
     ms_step = 1e3 * elapsed / args.steps
     value = B * args.steps / elapsed
     log(f"verify step {ms_step:.2f} ms -> {value:.0f} lists/s")
+    # Breakdown by kernel class: a separate pass with every launch bracketed.
+    steps_kt = max(3, args.steps // 2)
+    eng.atspeed_set_timing(True)
+    for _ in range(steps_kt):
+        step()
+    kt = eng.atspeed_get_timing()
+    eng.atspeed_set_timing(False)
 
     # ---- roofline of the dominant kernel (gate/up GEMM) and of the other classes
     M, d, f, H = n_fwd, w.target.d_model, w.target.d_ffn, w.target.n_heads
@@ -347,7 +361,7 @@ def main():
         if nlaunch == 0:
             continue
         avg = ms / nlaunch
-        ent = dict(ms_per_step=ms / args.steps, launches_per_step=nlaunch / args.steps, avg_launch_ms=avg)
+        ent = dict(ms_per_step=ms / steps_kt, launches_per_step=nlaunch / steps_kt, avg_launch_ms=avg)
         if k in flops:
             ent["tflops"] = flops[k] / (avg * 1e-3) / 1e12
             ent["mfma_frac"] = ent["tflops"] / PEAK_BF16_TFLOPS
@@ -357,13 +371,15 @@ def main():
             ent["gbs"] = (kv + tree) / (avg * 1e-3) / 1e9
             ent["hbm_frac"] = ent["gbs"] / PEAK_HBM_GBS
         classes[k] = ent
-    gemm_ms = sum(kt[k][0] for k in flops) / args.steps
+    gemm_ms = sum(kt[k][0] for k in flops) / steps_kt
     gemm_flops = nl * sum(flops[k] for k in ("qkv", "o", "gu", "down")) + flops["lm_head"]
-    gu = classes["gu"]
+    gu_avg = kt_gu[0] / kt_gu[1]                        # ms per gate/up launch in the timed region
+    gu_tflops = flops["gu"] / (gu_avg * 1e-3) / 1e12
     roofline = dict(bound="mfma", kernel="gemm_bf16 gate/up (SiLU*up epilogue)",
-                    achieved=round(gu["tflops"], 2), peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
-                    frac=round(gu["tflops"] / PEAK_BF16_TFLOPS, 4), traffic=gemm_traffic("gate/up GEMM"),
-                    per_launch_flops=flops["gu"], avg_launch_ms=round(gu["avg_launch_ms"], 4))
+                    achieved=round(gu_tflops, 2), peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
+                    frac=round(gu_tflops / PEAK_BF16_TFLOPS, 4), traffic=gemm_traffic("gate/up GEMM"),
+                    per_launch_flops=flops["gu"], avg_launch_ms=round(gu_avg, 4),
+                    launches_timed=int(kt_gu[1]))
 
     probe = None if args.no_probe else decode_bound_probe(eng, w, prefix, levels, max(3, args.steps // 2))
 
@@ -391,7 +407,7 @@ def main():
                    "global_batch": B, "seq_len": P, "parallelism": "none (1 GPU)"},
         "roofline": roofline,
         "cpu_baseline": cpu,
-        "kernels": classes,
+        "kernels": classes,            # separate pass, every launch bracketed by events
         "verify_gemm": dict(tflops=gemm_flops / (gemm_ms * 1e-3) / 1e12,
                             mfma_frac=gemm_flops / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
                             ms_per_step=gemm_ms),

@@ -225,10 +225,15 @@ ATSPEED_API atspeed_status atspeed_get_state(atspeed_ctx* ctx, int32_t B, int32_
 ATSPEED_API atspeed_status atspeed_set_state(atspeed_ctx* ctx, int32_t B, const int32_t* t, const int32_t* nbeams,
                                  const int32_t* paths, const float* scores);
 
-/* Kernel timing (instrumentation for measurement).  enable != 0 starts recording
- * one HIP event before every launch (and one after the last) on the context's
- * stream and clears the totals; 0 stops.  atspeed_get_timing synchronises the
- * stream, folds the recorded intervals into out (totals since enabling). */
+/* Kernel timing (instrumentation for measurement).  enable is a bit mask of the
+ * kernel classes to time (bit ATSPEED_K_x; ATSPEED_TIME_ALL for every class):
+ * a HIP event is recorded on the context's stream before each launch of a
+ * selected class and before the launch that follows it, and the totals are
+ * cleared; 0 stops.  Each event adds a little stream time, so timing only the
+ * classes of interest perturbs a measurement least.  atspeed_get_timing
+ * synchronises the stream, folds the recorded intervals into out (totals since
+ * enabling). */
+#define ATSPEED_TIME_ALL ((1 << ATSPEED_K_COUNT) - 1)
 ATSPEED_API atspeed_status atspeed_set_timing(atspeed_ctx* ctx, int32_t enable);
 ATSPEED_API atspeed_status atspeed_get_timing(atspeed_ctx* ctx, atspeed_kernel_times* out);
 

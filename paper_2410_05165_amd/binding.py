@@ -237,8 +237,16 @@ class Engine:
         self._check(self.lib.atspeed_set_state(self.ctx, len(t), _np_ptr(t, C.c_int32), _np_ptr(nb, C.c_int32),
                                                _np_ptr(paths, C.c_int32), _np_ptr(scores, C.c_float)))
 
-    def atspeed_set_timing(self, enable: bool):
-        self._check(self.lib.atspeed_set_timing(self.ctx, 1 if enable else 0))
+    def atspeed_set_timing(self, enable=True):
+        """enable: True (every kernel class), False (off), or an iterable of
+        class names from KERNEL_CLASSES (only those launches are bracketed)."""
+        if enable is True:
+            mask = (1 << len(KERNEL_CLASSES)) - 1
+        elif not enable:
+            mask = 0
+        else:
+            mask = sum(1 << KERNEL_CLASSES.index(k) for k in set(enable))
+        self._check(self.lib.atspeed_set_timing(self.ctx, mask))
 
     def atspeed_get_timing(self) -> Dict[str, tuple]:
         kt = KernelTimes()

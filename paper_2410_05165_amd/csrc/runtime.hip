@@ -120,7 +120,7 @@ struct atspeed_ctx {
   bool prefilled = false;
   bool drafted = false;
   // timing instrumentation
-  bool timing = false;
+  uint32_t timing_mask = 0;   // kernel classes whose launches are bracketed by events
   std::vector<hipEvent_t> ev_pool;
   std::vector<int> ev_kind;   // kind of the interval that starts at event i (-1: end marker)
   size_t ev_used = 0;
@@ -138,7 +138,12 @@ size_t esize(const atspeed_ctx& c) { return c.bf16 ? 2 : 4; }
 // Marks the start of a launch of class `kind` (or, with kind -1, the end of the
 // previous one) when timing is on.
 hipError_t mark(atspeed_ctx& c, int kind) {
-  if (!c.timing) return hipSuccess;
+  if (!c.timing_mask) return hipSuccess;
+  // An event opens a span before a launch of a selected class; the next mark
+  // closes it (and opens a new span if its class is selected too).
+  const bool want = kind >= 0 && ((c.timing_mask >> kind) & 1u);
+  const bool open = c.ev_used > 0 && c.ev_kind[c.ev_used - 1] >= 0;
+  if (!want && !open) return hipSuccess;
   if (c.ev_used == c.ev_pool.size()) {
     hipEvent_t e;
     hipError_t err = hipEventCreate(&e);
@@ -146,7 +151,7 @@ hipError_t mark(atspeed_ctx& c, int kind) {
     c.ev_pool.push_back(e);
     c.ev_kind.push_back(-1);
   }
-  c.ev_kind[c.ev_used] = kind;
+  c.ev_kind[c.ev_used] = want ? kind : -1;
   return hipEventRecord(c.ev_pool[c.ev_used++], c.st);
 }
 
@@ -823,7 +828,7 @@ atspeed_status atspeed_decode_topk(atspeed_ctx* c, int32_t B, int32_t P, const i
 atspeed_status atspeed_set_timing(atspeed_ctx* c, int32_t enable) {
   if (!c) return fail(ATSPEED_E_INVALID, "ctx is null");
   HIP_TRY(fold_timing(*c));
-  c->timing = enable != 0;
+  c->timing_mask = (uint32_t)enable & ATSPEED_TIME_ALL;
   for (int k = 0; k < ATSPEED_K_COUNT; ++k) { c->t_ms[k] = 0; c->t_n[k] = 0; }
   return ATSPEED_OK;
 }
