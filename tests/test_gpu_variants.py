@@ -1,6 +1,7 @@
 """GPU parity on shape variants that the named workloads do not cover at small
 size: d_head 128 with a text-token prompt before the history (as the 7B shape
-has), several layers, a ragged tree, and 1,024-token prefixes."""
+has), several layers, a ragged tree, 1,024-token prefixes, and an FFN width
+whose down projection is not split in k."""
 import numpy as np
 import pytest
 
@@ -25,6 +26,10 @@ VARIANTS = {
     # 16 key tiles per attention workgroup, 16 causal query blocks in prefill
     "longctx": dict(target=ModelDims(2, 256, 2, 512, 2048, 1024), draft=ModelDims(1, 256, 2, 512, 2048, 1024),
                     batch=2, prompt_len=64, hist_items=240, K=10, N=20, n_items=5000),
+    # d_ffn an odd multiple of 128 (11 x 128): the down projection takes its k range whole (no split at
+    # K/2, which needs whole even numbers of 64-column k-tiles in each half) while o is still split
+    "oddffn": dict(target=ModelDims(2, 512, 4, 1408, 2048, 1024), draft=ModelDims(1, 256, 2, 640, 2048, 1024),
+                   batch=4, prompt_len=16, hist_items=10, K=10, N=20, n_items=5000),
 }
 
 
@@ -64,5 +69,5 @@ def test_variant_logits(var):
               f"(logit std {caches[u].last_logits.std():.3f})")
         worst = max(worst, e_root, e_tree)
     eng.close()
-    if var in ("dh128", "longctx"):
+    if var in ("dh128", "longctx", "oddffn"):
         assert worst <= LOGIT_TOL["bf16"]
