@@ -60,10 +60,10 @@ def catalog_children(cat):
     return {k: sorted(v) for k, v in kids.items()}
 
 
-def upload_tree(eng, trees, B):
-    """Write per-user path lists into the context's tree (level-ordered, deduplicated)."""
+def tree_arrays(eng, trees, B):
+    """Per-user path lists as the context's tree arrays (level-ordered, deduplicated):
+    n_nodes [B], token, parent, depth [B, T] int32."""
     import numpy as np
-    import torch
     w = eng.w
     T = eng.max_nodes
     n = np.zeros(B, np.int32)
@@ -82,6 +82,13 @@ def upload_tree(eng, trees, B):
             tok[u, i] = w.target.item_base + w.codebook * (len(q) - 1) + q[-1]
             par[u, i] = index[q[:-1]] if len(q) > 1 else -1
             dep[u, i] = len(q)
+    return n, tok, par, dep
+
+
+def upload_tree(eng, trees, B):
+    """Write per-user path lists into the context's tree (level-ordered, deduplicated)."""
+    import torch
+    n, tok, par, dep = tree_arrays(eng, trees, B)
     tn, tt, tp, td, tq = eng.tree_tensors(B)
     tn.copy_(torch.from_numpy(n))
     tt.copy_(torch.from_numpy(tok))
@@ -116,6 +123,112 @@ def replay_all_accept_tree(eng, kids, w, levels):
             prev = lvl
         trees.append(nodes)
     return trees
+
+
+# Continuation probability of the forced-acceptance profile: accepted levels per
+# step a ~ P(a >= j) = ALPHA^j truncated at the L - t levels left, so that at
+# t = 0 (four levels) E[a] = 0.675 + 0.675^2 + 0.675^3 + 0.675^4 = 1.64, the
+# acceptance steps AtSpeed-S reaches at K = 10 on Amazon Beauty (Table 2).
+AS_ALPHA = 0.675
+
+
+def replay_as_steps(kids, w, levels, seed):
+    """Trees of one decode under forced acceptance.  At state t a user draws a
+    accepted levels; drafted levels t+1..t+a hold the target's TopK of that level
+    (padded to N as in the replay-all-accept tree), level t+a+1 holds N other
+    valid extensions (none of the target's TopK, so strict verification rejects
+    there and takes the target's level as the bonus), and t moves to t+a+1.
+    Returns [(trees, accepted, t_after)] per step; finished users get []."""
+    import numpy as np
+    rng = np.random.default_rng(seed)
+    B, L, N = w.batch, w.L, w.N
+    t = [0] * B
+    steps = []
+
+    def top(u, depth):
+        _, nb, paths, _ = levels[depth - 1]
+        return [tuple(int(c) for c in paths[u, k, :depth]) for k in range(nb[u])]
+
+    while any(tu < L for tu in t):
+        trees, acc, after = [], [], []
+        for u in range(B):
+            if t[u] >= L:
+                trees.append([]); acc.append(-1); after.append(L)
+                continue
+            a = 0
+            while a < L - t[u] and rng.random() < AS_ALPHA:
+                a += 1
+            prev = top(u, t[u]) if t[u] > 0 else [()]
+            nodes = [p for p in prev if p]
+            for depth in range(t[u] + 1, min(t[u] + a + 1, L) + 1):
+                tp = top(u, depth)
+                seen = set(tp)
+                if depth <= t[u] + a:           # accepted level: the target's TopK, padded
+                    lvl = list(tp)
+                else:                           # the rejected level: other extensions only
+                    lvl = []
+                for p in prev:
+                    if len(lvl) >= N:
+                        break
+                    for c in kids.get(p, []):
+                        q = p + (c,)
+                        if q not in seen:
+                            lvl.append(q)
+                            seen.add(q)
+                            if len(lvl) >= N:
+                                break
+                nodes.extend(lvl)
+                prev = lvl
+            trees.append(nodes)
+            acc.append(a)
+            t[u] = min(L, t[u] + a + 1)
+            after.append(t[u])
+        steps.append((trees, acc, after))
+    return steps
+
+
+def decode_replay_as(eng, w, prefix, levels, kids, reps, seed=1):
+    """Whole decode (prefill, then per step the device draft and a verify of the
+    forced-acceptance tree, copied device-to-device over the drafted one) under
+    the replay-paper-AS profile.  Returns the profile's figures."""
+    import numpy as np
+    import torch
+    B = w.batch
+    steps = replay_as_steps(kids, w, levels, seed)
+    dev_trees = [tuple(torch.from_numpy(a).to(prefix.device) for a in tree_arrays(eng, tr, B)) for tr, _, _ in steps]
+    tn, tt, tp, td, tq = eng.tree_tensors(B)
+    acc = torch.zeros(B, dtype=torch.int32, device=prefix.device)
+    ta = torch.zeros(B, dtype=torch.int32, device=prefix.device)
+
+    def decode(check):
+        eng.atspeed_prefill(prefix)
+        for s, (n, tok, par, dep) in enumerate(dev_trees):
+            eng.atspeed_draft()
+            tn.copy_(n); tt.copy_(tok); tp.copy_(par); td.copy_(dep); tq.zero_()
+            eng.atspeed_verify(acc, ta)
+            if check:
+                a_exp, t_exp = steps[s][1], steps[s][2]
+                got_a, got_t = acc.cpu().numpy(), ta.cpu().numpy()
+                for u in range(B):
+                    if a_exp[u] >= 0:
+                        assert got_a[u] == a_exp[u] and got_t[u] == t_exp[u], (s, u, got_a[u], a_exp[u])
+
+    decode(True)                                # the library accepts exactly the forced levels
+    final = eng.atspeed_get_state(B)
+    assert (final[2] == levels[-1][2]).all(), "replayed decode differs from target beam search"
+    torch.cuda.synchronize()
+    tt_ = []
+    for _ in range(reps):
+        a = time.perf_counter()
+        decode(False)
+        torch.cuda.synchronize()
+        tt_.append(time.perf_counter() - a)
+    ms = 1e3 * float(np.median(tt_))
+    first = [a for a in steps[0][1] if a >= 0]
+    return dict(lists_per_s=B / (ms * 1e-3), ms_per_decode=ms, steps=len(steps),
+                accepted_first_step_mean=float(np.mean(first)),
+                accepted_mean=float(np.mean([a for _, acc_, _ in steps for a in acc_ if a >= 0])),
+                profile="replay-paper-AS (first rejection forced; AS@10 = 1.64 at t = 0)")
 
 
 def gpu_target_beam_search(eng, w, prefix, upload_tree):
@@ -306,6 +419,12 @@ def main():
 
     # ---- replay-all-accept tree from the GPU's own target beam search
     levels = gpu_target_beam_search(eng, w, prefix, upload_tree)
+    e2e_as = None
+    if not args.no_e2e:
+        e2e_as = decode_replay_as(eng, w, prefix, levels, kids, reps=3)
+        log(f"e2e decode, replay-paper-AS: {e2e_as['ms_per_decode']:.1f} ms ({e2e_as['lists_per_s']:.0f} lists/s), "
+            f"{e2e_as['steps']} steps, accepted levels per step {e2e_as['accepted_mean']:.2f} "
+            f"(first step {e2e_as['accepted_first_step_mean']:.2f})")
     trees = replay_all_accept_tree(eng, kids, w, levels)
     final = levels[-1]
     eng.atspeed_prefill(prefix)
@@ -412,6 +531,7 @@ def main():
                             mfma_frac=gemm_flops / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
                             ms_per_step=gemm_ms),
         "e2e_decode": e2e,
+        "e2e_decode_paper_as": e2e_as,
         "decode_bound": probe,
     }
     print(json.dumps(out), flush=True)
