@@ -128,7 +128,7 @@ def replay_all_accept_tree(eng, kids, w, levels):
 # Continuation probability of the forced-acceptance profile: accepted levels per
 # step a ~ P(a >= j) = ALPHA^j truncated at the L - t levels left, so that at
 # t = 0 (four levels) E[a] = 0.675 + 0.675^2 + 0.675^3 + 0.675^4 = 1.64, the
-# acceptance steps AtSpeed-S reaches at K = 10 on Amazon Beauty (Table 2).
+# acceptance steps AtSpeed-S reaches at K = 10 on Amazon Beauty (Table 1).
 AS_ALPHA = 0.675
 
 
