@@ -397,25 +397,35 @@ def main():
     B, K, L = w.batch, w.K, w.L
 
     # ---- end-to-end decode (natural acceptance)
-    e2e = None
-    if not args.no_e2e:
+    def e2e_natural(engine, label):
         items = torch.zeros((B, K, L), dtype=torch.int32, device=dev)
         scores = torch.zeros((B, K), dtype=torch.float32, device=dev)
         n = torch.zeros(B, dtype=torch.int32, device=dev)
         st = Stats()
-        eng.atspeed_decode_topk(prefix, items, scores, n, None)
+        engine.atspeed_decode_topk(prefix, items, scores, n, None)
         torch.cuda.synchronize()
         reps, tt = 3, []
         for _ in range(reps):
             torch.cuda.synchronize()
             a = time.perf_counter()
-            eng.atspeed_decode_topk(prefix, items, scores, n, st)
+            engine.atspeed_decode_topk(prefix, items, scores, n, st)
             torch.cuda.synchronize()
             tt.append(time.perf_counter() - a)
-        e2e = dict(lists_per_s=B / float(np.median(tt)), ms_per_decode=1e3 * float(np.median(tt)),
-                   steps=int(st.n_steps), ms_prefill=st.ms_prefill, ms_draft=st.ms_draft, ms_verify=st.ms_verify,
-                   lists_per_s_decode_only=B / ((st.ms_draft + st.ms_verify) / 1e3), profile="natural")
-        log(f"e2e decode: {e2e['ms_per_decode']:.1f} ms ({e2e['lists_per_s']:.0f} lists/s), steps {st.n_steps}")
+        r = dict(lists_per_s=B / float(np.median(tt)), ms_per_decode=1e3 * float(np.median(tt)),
+                 steps=int(st.n_steps), ms_prefill=st.ms_prefill, ms_draft=st.ms_draft, ms_verify=st.ms_verify,
+                 lists_per_s_decode_only=B / ((st.ms_draft + st.ms_verify) / 1e3), profile=label)
+        log(f"e2e decode ({label}): {r['ms_per_decode']:.1f} ms ({r['lists_per_s']:.0f} lists/s), steps {st.n_steps}")
+        return r, (items.cpu().numpy(), scores.cpu().numpy(), n.cpu().numpy())
+
+    e2e = e2e_l1 = None
+    if not args.no_e2e:
+        e2e, out0 = e2e_natural(eng, "natural")
+        # the level-1 start: level 1 from the prefill, speculation from t = 1
+        eng1 = Engine(w, tw, dw, cat, mode=mode, seed=key[0] | (key[1] << 32), sd_start_level=1)
+        e2e_l1, out1 = e2e_natural(eng1, "natural, level-1 start")
+        eng1.close()
+        for x, y in zip(out0, out1):
+            assert (x == y).all(), "level-1 start changed the lists"
 
     # ---- replay-all-accept tree from the GPU's own target beam search
     levels = gpu_target_beam_search(eng, w, prefix, upload_tree)
@@ -531,6 +541,7 @@ def main():
                             mfma_frac=gemm_flops / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
                             ms_per_step=gemm_ms),
         "e2e_decode": e2e,
+        "e2e_decode_level1_start": e2e_l1,
         "e2e_decode_paper_as": e2e_as,
         "decode_bound": probe,
     }

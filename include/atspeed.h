@@ -78,6 +78,11 @@ typedef struct {
   float temperature;    /* sampling temperature of the relaxed modes (> 0)          */
   uint64_t seed;        /* Philox key of the relaxed modes                          */
   int32_t dtype;        /* atspeed_dtype of weights, activations and KV caches      */
+  int32_t sd_start_level; /* atspeed_decode_topk schedule: 0 speculates from t = 0, as
+                           Algorithm 1 does; 1 first takes level 1 from the prefill's
+                           root log-probs (a verify with no drafted levels, no forward)
+                           and speculates from t = 1, so no drafted level 1 is wasted.
+                           The lists are the same either way.                       */
   void* stream;         /* hipStream_t                                              */
 } atspeed_config;
 

@@ -35,7 +35,7 @@ class Config(C.Structure):
     _fields_ = [("target", Dims), ("draft", Dims), ("L", C.c_int32), ("codebook", C.c_int32),
                 ("K", C.c_int32), ("N", C.c_int32), ("gamma", C.c_int32), ("max_batch", C.c_int32),
                 ("max_prefix", C.c_int32), ("mode", C.c_int32), ("temperature", C.c_float),
-                ("seed", C.c_uint64), ("dtype", C.c_int32), ("stream", C.c_void_p)]
+                ("seed", C.c_uint64), ("dtype", C.c_int32), ("sd_start_level", C.c_int32), ("stream", C.c_void_p)]
 
 
 class Weights(C.Structure):
@@ -115,7 +115,7 @@ class Engine:
 
     def __init__(self, w, target_w: Dict[str, np.ndarray], draft_w: Optional[Dict[str, np.ndarray]],
                  catalog: np.ndarray, max_batch: Optional[int] = None, max_prefix: Optional[int] = None,
-                 device: str = "cuda:0", mode: int = STRICT, stream=None, seed: int = 0):
+                 device: str = "cuda:0", mode: int = STRICT, stream=None, seed: int = 0, sd_start_level: int = 0):
         import torch
         self.torch = torch
         self.lib = load_library()
@@ -134,6 +134,7 @@ class Engine:
         cfg.max_prefix = max_prefix or w.prefix_len
         cfg.mode, cfg.temperature, cfg.seed = mode, w.temperature, seed
         cfg.dtype = BF16 if self.bf16 else FP32
+        cfg.sd_start_level = sd_start_level
         cfg.stream = self.stream.cuda_stream
         self.cfg = cfg
         self._keep = []

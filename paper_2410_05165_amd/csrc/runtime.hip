@@ -201,6 +201,7 @@ atspeed_status check_config(const atspeed_config* cfg) {
   if (c.K < 1 || c.K > kMaxSel) return fail(ATSPEED_E_INVALID, "K must be 1..128");
   if (c.N < c.K || c.N > kMaxSel) return fail(ATSPEED_E_INVALID, "N must be K..128");
   if (c.gamma < 1) return fail(ATSPEED_E_INVALID, "gamma must be >= 1");
+  if (c.sd_start_level != 0 && c.sd_start_level != 1) return fail(ATSPEED_E_INVALID, "sd_start_level must be 0 or 1");
   if (c.max_batch < 1 || c.max_batch > 1024) return fail(ATSPEED_E_INVALID, "max_batch must be 1..1024");
   if (c.max_prefix < 1) return fail(ATSPEED_E_INVALID, "max_prefix must be >= 1");
   if (c.dtype != ATSPEED_FP32 && c.dtype != ATSPEED_BF16) return fail(ATSPEED_E_INVALID, "dtype");
@@ -795,8 +796,14 @@ atspeed_status atspeed_decode_topk(atspeed_ctx* c, int32_t B, int32_t P, const i
   const int L = c->cfg.L;
   std::vector<int> acc(B), ta(B);
   for (int step = 0; step < L; ++step) {
-    ST_TRY(atspeed_draft(c));
-    ST_TRY(lap(timing ? &stats->ms_draft : nullptr));
+    if (step == 0 && c->cfg.sd_start_level == 1) {
+      // level 1 from the prefill: a verify over a tree with no nodes selects the
+      // target's level from the root log-probs (the bonus level of zero accepted)
+      HIP_TRY(hipMemsetAsync(c->tree.n_nodes, 0, sizeof(int) * B, c->st));
+    } else {
+      ST_TRY(atspeed_draft(c));
+      ST_TRY(lap(timing ? &stats->ms_draft : nullptr));
+    }
     ST_TRY(atspeed_verify(c, c->acc_tmp, c->tafter_tmp, nullptr));
     HIP_TRY(hipMemcpyAsync(acc.data(), c->acc_tmp, B * 4, hipMemcpyDeviceToHost, c->st));
     HIP_TRY(hipMemcpyAsync(ta.data(), c->tafter_tmp, B * 4, hipMemcpyDeviceToHost, c->st));
