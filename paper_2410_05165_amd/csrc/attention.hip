@@ -221,7 +221,7 @@ template <int DH>
 __global__ void __launch_bounds__(256)
 attn_mfma_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ pk, const bf16_t* __restrict__ pv,
                  const bf16_t* __restrict__ tk, const bf16_t* __restrict__ tv, bf16_t* __restrict__ out, Rows rows,
-                 int H, int Pmax, float qscale) {
+                 int H, int Pmax, float qscale, int nusers, int nqblk) {
   constexpr int KT = 64;          // keys per tile
   constexpr int NKS = DH / 32;    // k-steps of S^T
   constexpr int NDB = DH / 16;    // 16-dim blocks of O^T
@@ -230,9 +230,16 @@ attn_mfma_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ pk, co
   __shared__ __align__(16) bf16_t Vt[DH * KT];
   __shared__ int kmax_s;
 
-  const int u = blockIdx.y, h = blockIdx.x;
+  // Workgroup L runs on XCD L % 8.  The Z query blocks of one (user, head) pair
+  // get consecutive indices on one XCD, so they run together and share the
+  // pair's prefix tiles in that XCD's L2; the pairs are dealt round-robin over
+  // the XCDs.
+  const int Lw = blockIdx.x, xcd = Lw & 7, qi8 = Lw >> 3, Z = nqblk;
+  const int pair = (qi8 / Z) * 8 + xcd, zb = qi8 % Z;
+  if (pair >= H * nusers) return;
+  const int u = pair / H, h = pair % H;
   const int ubeg = rows.user_off[u], uend = rows.user_off[u + 1];
-  const int r0 = ubeg + blockIdx.z * 64;
+  const int r0 = ubeg + zb * 64;
   if (r0 >= uend) return;
   const int nq = min(64, uend - r0);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -445,13 +452,14 @@ attn_mfma_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ pk, co
 template <int DH>
 static hipError_t launch_attn_mfma(const AttnCall& a, hipStream_t st) {
   const float qscale = 1.4426950408889634f / sqrtf((float)DH);
-  // query blocks vary slowest: workgroups are dealt to the XCDs round-robin by
-  // linear index, and the blocks past a user's rows exit at once, so the busy
-  // ones must form one contiguous run of linear indices to spread over all XCDs
-  dim3 grid(a.H, a.B, (a.Tq + 63) / 64);
-  hipLaunchKernelGGL(attn_mfma_kernel<DH>, grid, dim3(256), 0, st, (const bf16_t*)a.q, (const bf16_t*)a.pk,
-                     (const bf16_t*)a.pv, (const bf16_t*)a.tk, (const bf16_t*)a.tv, (bf16_t*)a.out, a.rows, a.H,
-                     a.Pmax, qscale);
+  // one-dimensional grid: ceil(pairs / 8) groups of 8 pairs x Z query blocks
+  const int Z = std::max(1, (a.Tq + 63) / 64);
+  const long pairs = (long)a.H * a.B;
+  const long nwg = (pairs + 7) / 8 * 8 * Z;
+  if (nwg > 0x7fffffffL) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(attn_mfma_kernel<DH>, dim3((unsigned)nwg), dim3(256), 0, st, (const bf16_t*)a.q,
+                     (const bf16_t*)a.pk, (const bf16_t*)a.pv, (const bf16_t*)a.tk, (const bf16_t*)a.tv,
+                     (bf16_t*)a.out, a.rows, a.H, a.Pmax, qscale, a.B, Z);
   return hipGetLastError();
 }
 
