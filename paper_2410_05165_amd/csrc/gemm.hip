@@ -4,9 +4,11 @@
 // BM x BN x 64 fetched by direct global->LDS DMA into two or three LDS stages
 // (XOR-swizzled 16-byte chunks), wave tile TM x TN blocks of 32x32, tile shape
 // chosen by the row count.  Epilogues are fused:
-//   QKV   rotary embedding on q and k (rotate-half pairs sit in registers of the
-//         same lane: partner block tn ^ (d_head/64)), rounding to bf16, q to its
-//         row buffer, k/v scattered into the prefix cache or the tree KV buffer;
+//   QKV   rotary embedding on q and k, rounding to bf16, q to its row buffer,
+//         k/v scattered into the prefix cache or the tree KV buffer.  The tile's
+//         weight rows are interleaved (qkv_logical) so that a column's
+//         rotate-half partner is lane ^ 16 of the same MFMA block, one
+//         v_permlane16_swap away whatever the tile width;
 //   GU    gate and up columns share a tile (first/second half of each wave's
 //         blocks), out = bf16(SiLU(gate) * up);
 //   RESID residual stream x += acc (fp32); with a partial buffer the k range
@@ -37,8 +39,9 @@ struct EpiArgs {
   bf16_t* q;         // [M, d]
   bf16_t* kdst;      // prefix cache or tree KV base of this layer
   bf16_t* vdst;
-  const float* cosT; // [max_pos, dh/2]
+  const float* cosT; // fp32 path: [max_pos, dh/2]
   const float* sinT;
+  const float* ropeT; // bf16 path: [max_pos][16][4] (cos, sin), rotary index 16*b + i at [pos][i][b]
   Rows rows;
   int kv_mode;       // 0 prefix cache [B][H][Pmax][dh], 1 tree [slot][d]
   int Pmax;
@@ -74,6 +77,17 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 // does that (r & 7 would put rows r and r + 8 on the same banks).
 __device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
 
+// Column order of the q/k/v product (bf16 path).  Within each head, the 32
+// columns of MFMA block b hold rotary indices 16b .. 16b+15 of the head's first
+// half in lanes 0..15 and the same indices of its second half in lanes 16..31,
+// so every column's rotate-half partner is lane ^ 16 of the same block.  Maps a
+// column's place pp within its head (as the tile holds it) to its column in
+// the head (d_head 64 or 128); a bijection on 0 .. d_head-1 that keeps runs of
+// 16 columns, and so 16-byte chunks of the bf16 output, contiguous.
+__device__ __forceinline__ int qkv_logical(int pp, int halfdh) {
+  return ((pp >> 5) << 4) + (pp & 15) + ((pp & 16) ? halfdh : 0);
+}
+
 // One k-tile (64 columns of A and W) into an LDS stage with direct global->LDS
 // DMA (global_load_lds_dwordx4): each wave instruction fills 1 KB = 8 rows of
 // 128 B; lane i lands at byte 16*i, i.e. row i/8, physical chunk i%8, and so
@@ -85,8 +99,7 @@ __device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
 // (activation and weight buffers are below 2^31 elements).
 template <int NA, int NB>
 __device__ __forceinline__ void load_stage(unsigned char* stage, int wave, const bf16_t* A, const int* a_off,
-                                           const bf16_t* B0, const bf16_t* B1, const int* b_off, const bool* b_hi,
-                                           int k0, int a_bytes) {
+                                           const bf16_t* const* Bp, const int* b_off, int k0, int a_bytes) {
 #pragma unroll
   for (int j = 0; j < NA; ++j)
     __builtin_amdgcn_global_load_lds((void*)(reinterpret_cast<const unsigned char*>(A) + (uint32_t)(a_off[j] + k0) * 2u),
@@ -94,7 +107,7 @@ __device__ __forceinline__ void load_stage(unsigned char* stage, int wave, const
 #pragma unroll
   for (int j = 0; j < NB; ++j)
     __builtin_amdgcn_global_load_lds(
-        (void*)(reinterpret_cast<const unsigned char*>(b_hi[j] ? B1 : B0) + (uint32_t)(b_off[j] + k0) * 2u),
+        (void*)(reinterpret_cast<const unsigned char*>(Bp[j]) + (uint32_t)(b_off[j] + k0) * 2u),
         (lds_void_t*)(stage + a_bytes + (wave * NB + j) * 1024), 16, 0, 0);
 }
 
@@ -186,7 +199,6 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
 
   // per-lane element offsets of the 16-byte chunks this lane fetches
   int a_off[NA], b_off[NB];
-  bool b_hi[NB];
 #pragma unroll
   for (int j = 0; j < NA; ++j) {
     int r = (wave * NA + j) * 8 + lrow;
@@ -194,30 +206,35 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
     gr = gr < M ? gr : M - 1;
     a_off[j] = gr * lda + kbase + ((lane & 7) ^ swz(r)) * 8;
   }
-  const bf16_t* B0;
-  const bf16_t* B1 = nullptr;
-  if (BMAP == BMAP_QKV) {
-    const int which = (tile_n * T::BN) / b.split;
-    B0 = which == 0 ? b.w0 : (which == 1 ? b.w1 : b.w2);
-  } else {
-    B0 = b.w0;
-    B1 = b.w1;
-  }
+  // Weight rows of the B tile.  DMA instruction j fills tile rows r0 .. r0+7
+  // (r0 = (wave*NB + j)*8), all from one weight matrix Bp[j], chosen from r0
+  // alone so that its base stays wave-uniform (d_model and d_ffn are multiples
+  // of 8, so no instruction straddles two matrices).
+  const bf16_t* Bp[NB];
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
-    const int r = (wave * NB + j) * 8 + lrow;
+    const int r0 = (wave * NB + j) * 8, r = r0 + lrow;
     int row;
-    b_hi[j] = false;
     if (BMAP == BMAP_GU) {
+      // gate rows in the first half of each wave's blocks, the matching up rows in the second
       constexpr int half = TN / 2;
       const int wn = r / (TN * 32), blk = (r / 32) % TN, cc = r % 32;
       row = tile_n * (T::BN / 2) + wn * (half * 32) + (blk % half) * 32 + cc;
       row = row < b.split ? row : b.split - 1;
-      b_hi[j] = blk >= half;
+      Bp[j] = (r0 / 32) % TN >= half ? b.w1 : b.w0;
+    } else if (BMAP == BMAP_QKV) {
+      // tile row = column of [q | k | v] (3 d_model), rows past it clamped to the last
+      int p = tile_n * T::BN + r;
+      p = p < N ? p : N - 1;
+      const int p0 = tile_n * T::BN + r0;
+      const int which = (p0 < N ? p0 : N - 1) / b.split;
+      const int hc = p - which * b.split, pp = hc & (e.dh - 1);
+      row = hc - pp + qkv_logical(pp, e.dh >> 1);
+      Bp[j] = which == 0 ? b.w0 : (which == 1 ? b.w1 : b.w2);
     } else {
       row = tile_n * T::BN + r;
       row = row < N ? row : N - 1;
-      if (BMAP == BMAP_QKV) row -= (tile_n * T::BN / b.split) * b.split;
+      Bp[j] = b.w0;
     }
     b_off[j] = row * K + kbase + ((lane & 7) ^ swz(r)) * 8;
   }
@@ -246,19 +263,19 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
   constexpr int WAITALL = (0x7 << 4) | (0xF << 8);  // vmcnt(0): every DMA of this wave landed
   if constexpr (NS == 2) {
     // nk is even (K % 128 == 0 is checked on the host): stages alternate st0, st1
-    load_stage<NA, NB>(st0, wave, A, a_off, B0, B1, b_off, b_hi, 0, T::A_BYTES);
+    load_stage<NA, NB>(st0, wave, A, a_off, Bp, b_off, 0, T::A_BYTES);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     // sched_barrier(0) after each DMA issue: left free, the scheduler sinks the
     // DMA below the stage's MFMAs, right before the wait that ends the stage,
     // and the load latency is exposed instead of hidden
     for (int kt = 0; kt < nk; kt += 2) {
-      load_stage<NA, NB>(st1, wave, A, a_off, B0, B1, b_off, b_hi, (kt + 1) * 64, T::A_BYTES);
+      load_stage<NA, NB>(st1, wave, A, a_off, Bp, b_off, (kt + 1) * 64, T::A_BYTES);
       __builtin_amdgcn_sched_barrier(0);
       mma_stage<WM, WN, TM, TN>(st0, wave_m, wave_n, fr, fc, acc, T::A_BYTES);
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
-      if (kt + 2 < nk) load_stage<NA, NB>(st0, wave, A, a_off, B0, B1, b_off, b_hi, (kt + 2) * 64, T::A_BYTES);
+      if (kt + 2 < nk) load_stage<NA, NB>(st0, wave, A, a_off, Bp, b_off, (kt + 2) * 64, T::A_BYTES);
       __builtin_amdgcn_sched_barrier(0);
       mma_stage<WM, WN, TM, TN>(st1, wave_m, wave_n, fr, fc, acc, T::A_BYTES);
       __builtin_amdgcn_s_waitcnt(0);
@@ -267,7 +284,7 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
   } else {
   static_for<NS - 1>([&](auto S) {
     constexpr int s_ = decltype(S)::value;
-    if (s_ < nk) load_stage<NA, NB>(stage(S), wave, A, a_off, B0, B1, b_off, b_hi, s_ * 64, T::A_BYTES);
+    if (s_ < nk) load_stage<NA, NB>(stage(S), wave, A, a_off, Bp, b_off, s_ * 64, T::A_BYTES);
   });
   // Stage 0 must have landed.  Leaving ALLOW loads in flight is only right when
   // the later stages' loads were issued behind it; otherwise wait for all.
@@ -280,7 +297,7 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
       const int kt = kt0 + s_;
       if (kt < nk) {
         if (kt + NS - 1 < nk)
-          load_stage<NA, NB>(stage(std::integral_constant<int, s_ + NS - 1>{}), wave, A, a_off, B0, B1, b_off, b_hi,
+          load_stage<NA, NB>(stage(std::integral_constant<int, s_ + NS - 1>{}), wave, A, a_off, Bp, b_off,
                              (kt + NS - 1) * 64, T::A_BYTES);
         __builtin_amdgcn_sched_barrier(0);
         mma_stage<WM, WN, TM, TN>(stage(S), wave_m, wave_n, fr, fc, acc, T::A_BYTES);
@@ -383,17 +400,26 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
           }
         });
       });
-    } else {  // EPI_QKV: rotary embedding on q and k; each wave's 128 columns lie in one of q, k, v
-      const int halfdh = e.dh >> 1;
-      const bool pair1 = halfdh == 32;       // partner block j^1 (d_head 64) or j^2 (d_head 128)
-      const bool rot = col0 / e.d < 2;
-      // column j*32+fr of the wave's head-aligned span has rotary index (j*32+fr) mod halfdh
-      const int ci0 = fr & (halfdh - 1), ci1 = (32 + fr) & (halfdh - 1);
+    } else {  // EPI_QKV: rotary embedding on q and k (column order of qkv_logical)
+      // per block (wave-uniform; d_model and d_head are multiples of 32): which of
+      // q, k, v it lies in, and b, its rotary indices being 16b + lane % 16
+      int bsel[TN];
+      bool rotj[TN];
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        int pc = col0 + j * 32;
+        pc = pc < N ? pc : N - 32;
+        const int wj = pc / e.d;
+        rotj[j] = wj < 2;
+        bsel[j] = ((pc - wj * e.d) & (e.dh - 1)) >> 5;
+      }
+      const bool lo = fr < 16;            // first half of the head: x1 cos - x2 sin, else x2 cos + x1 sin
+      const int i16 = fr & 15;
       static_for<TM>([&](auto I) {
         constexpr int i = decltype(I)::value;
-        // rows in groups of 4: positions, then the cos/sin of the group, all issued
-        // before any is used (one memory latency per group, not per row); v
-        // columns take cos 1, sin 0 without a branch
+        // rows in groups of 4: positions, then the (cos, sin) pairs of the group's
+        // rows and blocks, all issued before any is used; v columns take cos 1,
+        // sin 0 without a branch
         static_for<4>([&](auto Q) {
           constexpr int qg = decltype(Q)::value;
           int pos[4];
@@ -403,26 +429,30 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
             const int row = m0 + (wave_m < WMH ? 0 : HROWS) + hr;
             pos[r] = e.rows.pos[row < M ? row : M - 1];
           });
-          float c0[4], s0[4], c1[4], s1[4];
+          // (cos, sin) of each row and block: the block's rotary index picks the
+          // pair within the row's table entry by address, so no select on values
+          f32x2_t cs[4][TN];
           static_for<4>([&](auto R) {
             constexpr int r = decltype(R)::value;
-            const int base = rot ? pos[r] * halfdh : 0;
-            c0[r] = e.cosT[base + ci0]; s0[r] = e.sinT[base + ci0];
-            c1[r] = e.cosT[base + ci1]; s1[r] = e.sinT[base + ci1];
+            const float* t = e.ropeT + ((size_t)pos[r] * 16 + i16) * 8;
+#pragma unroll
+            for (int j = 0; j < TN; ++j) cs[r][j] = *reinterpret_cast<const f32x2_t*>(t + bsel[j] * 2);
           });
           static_for<4>([&](auto R) {
             constexpr int r = decltype(R)::value;
             constexpr int ra = qg * 4 + r;     // accumulator register of this row
             const int hr = hrow0 + i * 32 + qg * 8 + fc * 4 + r;
-            const float cc0 = rot ? c0[r] : 1.f, ss0 = rot ? s0[r] : 0.f;
-            const float cc1 = rot ? c1[r] : 1.f, ss1 = rot ? s1[r] : 0.f;
             static_for<TN>([&](auto J) {
               constexpr int j = decltype(J)::value;
-              constexpr bool odd = (j & 1) != 0;
               const float v = acc[i][j][ra];
-              const float pv = pair1 ? acc[i][j ^ 1][ra] : acc[i][j ^ 2][ra];
-              const float c = (pair1 || !odd) ? cc0 : cc1, sn = (pair1 || !odd) ? ss0 : ss1;
-              const bool lo = pair1 ? !odd : j < 2;   // first half of the head
+              // partner = lane ^ 16: v_permlane16_swap of two copies exchanges
+              // the odd 16-lane rows of the first with the even rows of the
+              // second, so the first holds the partner in lanes 16..31 and the
+              // second in lanes 0..15 (a VALU op, no LDS round trip)
+              const auto sw = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+              const float pv = __uint_as_float(lo ? sw[1] : sw[0]);
+              const float cb = cs[r][j][0], sb = cs[r][j][1];
+              const float c = rotj[j] ? cb : 1.f, sn = rotj[j] ? sb : 0.f;
               // explicit fma of a rounded product: the same arithmetic in every
               // tile shape (free contraction may differ between instantiations,
               // and rows must not depend on the shape their batch got)
@@ -445,9 +475,10 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
         const int fcol = tile_n * (T::BN / 2) + cc;
         if (fcol < b.split) *reinterpret_cast<u32x4_t*>(e.hout + (size_t)row * b.split + fcol) = v;
       } else {
-        const int col = tile_n * T::BN + cc;
+        const int col = tile_n * T::BN + cc;   // 8 columns of the tile's order, one run of qkv_logical
         if (col >= N) continue;
-        const int which = col / e.d, hc = col - which * e.d;
+        const int which = col / e.d, pc = col - which * e.d, pp = pc & (e.dh - 1);
+        const int hc = pc - pp + qkv_logical(pp, e.dh >> 1);
         if (which == 0) {
           *reinterpret_cast<u32x4_t*>(e.q + (size_t)row * e.d + hc) = v;
         } else {
@@ -572,7 +603,7 @@ static hipError_t launch_bf16(const GemmCall& g, hipStream_t st) {
   e.out = g.out; e.ldo = g.ldo; e.hout = (bf16_t*)g.hout;
   e.part = EPI == EPI_RESID ? g.part : nullptr;
   e.q = (bf16_t*)g.q; e.kdst = (bf16_t*)g.kdst; e.vdst = (bf16_t*)g.vdst;
-  e.cosT = g.cosT; e.sinT = g.sinT; e.rows = g.rows; e.kv_mode = g.kv_mode; e.Pmax = g.Pmax;
+  e.cosT = g.cosT; e.sinT = g.sinT; e.ropeT = g.ropeT; e.rows = g.rows; e.kv_mode = g.kv_mode; e.Pmax = g.Pmax;
   e.d = g.d; e.dh = g.dh; e.H = g.H;
   const int kparts = e.part ? 2 : 1;
   // each k-range is whole k-tiles of 64, an even number of them for two stages
@@ -597,8 +628,11 @@ static hipError_t launch_bf16(const GemmCall& g, hipStream_t st) {
 namespace {
 constexpr int kCUs = 256;
 struct Shape { int bm, bn, per_cu; float t0, t4k; };
-// q/k/v, gate/up: 256x256 (8 waves), 128x256 (8 waves), 64x256 (2 waves, two per CU)
-constexpr Shape kQkvShapes[] = {{256, 256, 1, 0.f, 120.f}, {128, 256, 1, 0.f, 70.f}, {64, 256, 2, 0.f, 72.f}};
+// q/k/v: 256x256 (8 waves), 128x256 (8 waves), 64x256 (2 waves, two per CU),
+// 256x192 (8 waves; 3 d_model is a multiple of 192, so no ragged column tile);
+// gate/up: the first three
+constexpr Shape kQkvShapes[] = {
+    {256, 256, 1, 0.f, 98.f}, {128, 256, 1, 0.f, 67.f}, {64, 256, 2, 0.f, 73.f}, {256, 192, 1, 0.f, 83.f}};
 constexpr Shape kGuShapes[] = {{256, 256, 1, 0.f, 102.f}, {128, 256, 1, 0.f, 63.f}, {64, 256, 2, 0.f, 66.f}};
 // o, down, output head: 256x256, 256x128 (8 waves), 128x128 (4 waves), 64x64 (2 waves)
 constexpr Shape kRowShapes[] = {
@@ -626,7 +660,8 @@ hipError_t gemm(const GemmCall& g, hipStream_t st) {
         switch (pick_shape(kQkvShapes, M, g.N, g.K)) {
           case 0: return launch_bf16<BMAP_QKV, EPI_QKV, kWideWM, 2, kWideTM, 4, 2>(g, st);
           case 1: return launch_bf16<BMAP_QKV, EPI_QKV, 4, 2, 1, 4, 2>(g, st);
-          default: return launch_bf16<BMAP_QKV, EPI_QKV, 1, 2, 2, 4, 2>(g, st);
+          case 2: return launch_bf16<BMAP_QKV, EPI_QKV, 1, 2, 2, 4, 2>(g, st);
+          default: return launch_bf16<BMAP_QKV, EPI_QKV, 4, 2, 2, 3, 2>(g, st);
         }
       case GEMM_GU:
         switch (pick_shape(kGuShapes, M, g.N, g.K)) {

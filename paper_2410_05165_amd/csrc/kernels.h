@@ -19,7 +19,8 @@ struct GemmCall {
   float* part;               // bf16 RESID: k split at K/2; the second half's product [Mmax, ldo] fp32 goes here
   void* hout;                // GU output [M, f]
   void* q; void* kdst; void* vdst;
-  const float* cosT; const float* sinT;
+  const float* cosT; const float* sinT;   // fp32 path: [max_pos, d_head/2] each
+  const float* ropeT;        // bf16 path: [max_pos][16][4] (cos, sin) of rotary index 16*b + i at [pos][i][b] (0 past d_head/2)
   Rows rows;
   int kv_mode, Pmax, d, dh, H;
   float* scratch;            // fp32 path: [Mmax, N] product

@@ -62,6 +62,7 @@ struct ModelRt {
   size_t pkv_layer_stride = 0;
   float* cosT = nullptr;
   float* sinT = nullptr;
+  float* ropeT = nullptr;
   float* lp = nullptr;           // [B*Tmax][nitem] log-probs by tree slot
   float* root = nullptr;         // [B][nitem] log-probs at the last prefix position
   int dh() const { return dims.d_model / dims.n_heads; }
@@ -304,6 +305,7 @@ void layout(atspeed_ctx& c, const atspeed_config& cfg, int trie_nodes, Arena& a)
     const int half = m.d_model / m.n_heads / 2;
     r.cosT = a.take<float>((size_t)c.max_pos * half);
     r.sinT = a.take<float>((size_t)c.max_pos * half);
+    r.ropeT = a.take<float>((size_t)c.max_pos * 16 * 4 * 2);
     r.lp = a.take<float>((size_t)B * Tm * c.nitem);
     r.root = a.take<float>((size_t)B * c.nitem);
   }
@@ -397,8 +399,20 @@ atspeed_status upload_rope(atspeed_ctx& c, ModelRt& r) {
       cs[(size_t)p * half + i] = (float)std::cos(ang);
       sn[(size_t)p * half + i] = (float)std::sin(ang);
     }
+  // the same values regrouped for the bf16 q/k/v epilogue: (cos, sin) of rotary
+  // index 16*b + i at [pos][i][b], so a lane's four blocks are two 16-byte loads
+  std::vector<float> rt((size_t)c.max_pos * 16 * 4 * 2, 0.f);
+  for (int p = 0; p < c.max_pos; ++p)
+    for (int i = 0; i < 16; ++i)
+      for (int b = 0; b < 4; ++b) {
+        const int ri = 16 * b + i;
+        if (ri >= half) continue;
+        rt[(((size_t)p * 16 + i) * 4 + b) * 2] = cs[(size_t)p * half + ri];
+        rt[(((size_t)p * 16 + i) * 4 + b) * 2 + 1] = sn[(size_t)p * half + ri];
+      }
   HIP_TRY(hipMemcpyAsync(r.cosT, cs.data(), cs.size() * 4, hipMemcpyHostToDevice, c.st));
   HIP_TRY(hipMemcpyAsync(r.sinT, sn.data(), sn.size() * 4, hipMemcpyHostToDevice, c.st));
+  HIP_TRY(hipMemcpyAsync(r.ropeT, rt.data(), rt.size() * 4, hipMemcpyHostToDevice, c.st));
   HIP_TRY(hipStreamSynchronize(c.st));
   return ATSPEED_OK;
 }
@@ -429,7 +443,7 @@ atspeed_status forward(atspeed_ctx& c, ModelRt& r, bool prefill, int Mmax, int T
     GemmCall g{};
     g.bf16 = c.bf16;
     g.Mmax = Mmax; g.Mdev = c.rows.M; g.scratch = c.scratch; g.rows = c.rows;
-    g.cosT = r.cosT; g.sinT = r.sinT; g.d = d; g.dh = dh; g.H = H; g.Pmax = c.cfg.max_prefix;
+    g.cosT = r.cosT; g.sinT = r.sinT; g.ropeT = r.ropeT; g.d = d; g.dh = dh; g.H = H; g.Pmax = c.cfg.max_prefix;
     // q, k, v (+ rotary), k/v to their cache
     g.kind = GEMM_QKV; g.A = c.xn; g.lda = d; g.N = 3 * d; g.K = d;
     g.w0 = w[1]; g.w1 = w[2]; g.w2 = w[3]; g.split = d; g.q = c.q;
