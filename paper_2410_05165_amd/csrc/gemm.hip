@@ -1,7 +1,7 @@
 // Dense projections of the decoder block: Y[M, N] = X[M, K] · W[N, K]^T.
 //
 // bf16 path: MFMA v_mfma_f32_32x32x16_bf16 (fp32 accumulate), block tile
-// BM x BN x 64 fetched by direct global->LDS DMA into two or three LDS stages
+// BM x BN x 64 fetched by direct global->LDS DMA into two LDS stages
 // (XOR-swizzled 16-byte chunks), wave tile TM x TN blocks of 32x32, tile shape
 // chosen by the row count.  Epilogues are fused:
 //   QKV   rotary embedding on q and k, rounding to bf16, q to its row buffer,
@@ -157,7 +157,7 @@ __device__ __forceinline__ void mma_stage(const unsigned char* stage, int wave_m
   });
 }
 
-template <int WM, int WN, int TM, int TN, int BMAP, int EPI, int NS>
+template <int WM, int WN, int TM, int TN, int BMAP, int EPI>
 __global__ void __launch_bounds__(64 * WM * WN)
 gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ Mdev, int Mt, int N, int K,
                  BArgs b, EpiArgs e) {
@@ -166,10 +166,8 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
   static_assert(NW == 2 || NW == 4 || NW == 8, "two, four or eight waves");
   constexpr int NA = T::BM / (8 * NW);   // wave instructions per stage for A (8 rows of 128 B each)
   constexpr int NB = T::BN / (8 * NW);
-  static_assert(NS == 2 || NS == 3, "two or three LDS stages");
   __shared__ __align__(1024) unsigned char st0[T::STAGE];
   __shared__ __align__(1024) unsigned char st1[T::STAGE];
-  __shared__ __align__(1024) unsigned char st2[NS == 3 ? T::STAGE : 16];
   const int M = *Mdev;
   // XCD-aware tile order: workgroup L is dispatched to XCD L % 8; XCD x owns the
   // contiguous range x*per .. x*per+per-1 of the tiles in N-major order, so the
@@ -189,11 +187,9 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
   const int tile_n = t / Mt, tile_m = t - tile_n * Mt;
   const int m0 = tile_m * T::BM;
   if (m0 >= M) return;
-  // two-stage pipelines keep the wave index in a scalar register (the DMA row
-  // bases and the gate/up weight choice derived from it are then wave-uniform);
-  // in the three-stage pipeline that made the compiler drain all loads once
-  // more per k-tile, so it keeps the vector form
-  const int tid = threadIdx.x, lane = tid & 63, wave = NS == 2 ? __builtin_amdgcn_readfirstlane(tid >> 6) : tid >> 6;
+  // wave index in a scalar register: the DMA row bases and the weight choice
+  // derived from it are then wave-uniform
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wave_m = wave / WN, wave_n = wave % WN;
   const int lrow = lane >> 3;
 
@@ -249,75 +245,30 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
 
   const int nk = K / kparts / T::BK;
   const int fr = lane & 31, fc = lane >> 5;
-  // NS-stage pipeline: stage s of round kt0 computes k-tile kt0+s while the
-  // DMA of k-tile kt0+s+NS-1 is in flight; each stage is its own LDS array and
-  // is chosen at compile time, so the compiler sees the DMA and the fragment
-  // reads of a step touch different objects and inserts no waits between them.
-  auto stage = [&](auto S) -> unsigned char* {
-    constexpr int s_ = decltype(S)::value % NS;
-    return s_ == 0 ? st0 : (s_ == 1 ? st1 : st2);
-  };
-  constexpr int NLOADS = NA + NB;                 // DMA instructions per stage per lane
-  constexpr int ALLOW = NLOADS * (NS - 2);        // loads that may stay in flight at a stage boundary
-  constexpr int WAITCNT = (ALLOW & 0xF) | (((ALLOW >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8);
-  constexpr int WAITALL = (0x7 << 4) | (0xF << 8);  // vmcnt(0): every DMA of this wave landed
-  if constexpr (NS == 2) {
-    // nk is even (K % 128 == 0 is checked on the host): stages alternate st0, st1
-    load_stage<NA, NB>(st0, wave, A, a_off, Bp, b_off, 0, T::A_BYTES);
+  // Two-stage pipeline: while the MFMAs consume one LDS stage, the DMA of the
+  // next k-tile fills the other.  Each stage is its own LDS array, named at
+  // compile time, so the compiler sees that a step's DMA and fragment reads
+  // touch different objects and inserts no waits between them.  (A third stage
+  // was slower on every shape measured: its partial waits cost more than the
+  // extra prefetch distance gained.)
+  // nk is even (each k-range is a multiple of 128, checked on the host)
+  load_stage<NA, NB>(st0, wave, A, a_off, Bp, b_off, 0, T::A_BYTES);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  // sched_barrier(0) after each DMA issue: left free, the scheduler sinks the
+  // DMA below the stage's MFMAs, right before the wait that ends the stage,
+  // and the load latency is exposed instead of hidden
+  for (int kt = 0; kt < nk; kt += 2) {
+    load_stage<NA, NB>(st1, wave, A, a_off, Bp, b_off, (kt + 1) * 64, T::A_BYTES);
+    __builtin_amdgcn_sched_barrier(0);
+    mma_stage<WM, WN, TM, TN>(st0, wave_m, wave_n, fr, fc, acc, T::A_BYTES);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    // sched_barrier(0) after each DMA issue: left free, the scheduler sinks the
-    // DMA below the stage's MFMAs, right before the wait that ends the stage,
-    // and the load latency is exposed instead of hidden
-    for (int kt = 0; kt < nk; kt += 2) {
-      load_stage<NA, NB>(st1, wave, A, a_off, Bp, b_off, (kt + 1) * 64, T::A_BYTES);
-      __builtin_amdgcn_sched_barrier(0);
-      mma_stage<WM, WN, TM, TN>(st0, wave_m, wave_n, fr, fc, acc, T::A_BYTES);
-      __builtin_amdgcn_s_waitcnt(0);
-      __syncthreads();
-      if (kt + 2 < nk) load_stage<NA, NB>(st0, wave, A, a_off, Bp, b_off, (kt + 2) * 64, T::A_BYTES);
-      __builtin_amdgcn_sched_barrier(0);
-      mma_stage<WM, WN, TM, TN>(st1, wave_m, wave_n, fr, fc, acc, T::A_BYTES);
-      __builtin_amdgcn_s_waitcnt(0);
-      __syncthreads();
-    }
-  } else {
-  static_for<NS - 1>([&](auto S) {
-    constexpr int s_ = decltype(S)::value;
-    if (s_ < nk) load_stage<NA, NB>(stage(S), wave, A, a_off, Bp, b_off, s_ * 64, T::A_BYTES);
-  });
-  // Stage 0 must have landed.  Leaving ALLOW loads in flight is only right when
-  // the later stages' loads were issued behind it; otherwise wait for all.
-  if (NS - 2 < nk) __builtin_amdgcn_s_waitcnt(WAITCNT);
-  else __builtin_amdgcn_s_waitcnt(WAITALL);
-  __syncthreads();
-  for (int kt0 = 0; kt0 < nk; kt0 += NS) {
-    static_for<NS>([&](auto S) {
-      constexpr int s_ = decltype(S)::value;
-      const int kt = kt0 + s_;
-      if (kt < nk) {
-        if (kt + NS - 1 < nk)
-          load_stage<NA, NB>(stage(std::integral_constant<int, s_ + NS - 1>{}), wave, A, a_off, Bp, b_off,
-                             (kt + NS - 1) * 64, T::A_BYTES);
-        __builtin_amdgcn_sched_barrier(0);
-        mma_stage<WM, WN, TM, TN>(stage(S), wave_m, wave_n, fr, fc, acc, T::A_BYTES);
-        // Own DMA of the next stage landed (only the newest stage may still be in
-        // flight); the fragment reads of this stage were consumed by the MFMAs.
-        // A bare barrier then orders both for every wave (a fenced __syncthreads
-        // would drain the newest stage's DMA too).  The barrier intrinsic does
-        // not order memory for the compiler, so empty asm with a memory clobber
-        // on both sides keeps the next stage's fragment reads and DMA below it.
-        // Near the end of k no newer stage was issued: then the next stage's DMA
-        // is the newest in flight and must be waited for in full.
-        asm volatile("" ::: "memory");
-        if (kt + NS - 1 < nk) __builtin_amdgcn_s_waitcnt(WAITCNT);
-        else __builtin_amdgcn_s_waitcnt(WAITALL);
-        __builtin_amdgcn_s_barrier();
-        asm volatile("" ::: "memory");
-      }
-    });
-  }
-  __syncthreads();
+    if (kt + 2 < nk) load_stage<NA, NB>(st0, wave, A, a_off, Bp, b_off, (kt + 2) * 64, T::A_BYTES);
+    __builtin_amdgcn_sched_barrier(0);
+    mma_stage<WM, WN, TM, TN>(st1, wave_m, wave_n, fr, fc, acc, T::A_BYTES);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
   }
 
   // ---- epilogue.  acc[i][j][r] is row (r/4)*8 + (lane/32)*4 + r%4, column lane%32 of block (i, j).
@@ -584,18 +535,10 @@ __global__ void epi_f32_kernel(const float* __restrict__ C, const int* __restric
 }
 
 // ------------------------------------------------------------------ launchers
-// Large batches: 256x256 tiles of 8 waves (64x128 each, two waves per SIMD, so
-// one wave's LDS and barrier waits hide behind the other's MFMAs) for the wide
-// projections (q/k/v, gate/up), 256x128 tiles of 8 waves (64x64) with three LDS
-// stages for the d_model-wide ones (o, down) and the output head.
-constexpr int kWideWM = 4, kWideTM = 2;
-#ifndef NARROW_WM
-#define NARROW_WM 4
-#define NARROW_WN 2
-#define NARROW_TM 2
-#define NARROW_TN 2
-#endif
-template <int BMAP, int EPI, int WMW, int WNW, int TMW, int TNW, int NS>
+// Launch of one instantiation over the tiles of a call.  The widest tiles,
+// 256x256 of 8 waves (64x128 each, two waves per SIMD), let one wave's LDS and
+// barrier waits hide behind the other's MFMAs.
+template <int BMAP, int EPI, int WMW, int WNW, int TMW, int TNW>
 static hipError_t launch_bf16(const GemmCall& g, hipStream_t st) {
   using T = Tile<WMW, WNW, TMW, TNW>;
   BArgs b{(const bf16_t*)g.w0, (const bf16_t*)g.w1, (const bf16_t*)g.w2, g.split};
@@ -606,12 +549,12 @@ static hipError_t launch_bf16(const GemmCall& g, hipStream_t st) {
   e.cosT = g.cosT; e.sinT = g.sinT; e.ropeT = g.ropeT; e.rows = g.rows; e.kv_mode = g.kv_mode; e.Pmax = g.Pmax;
   e.d = g.d; e.dh = g.dh; e.H = g.H;
   const int kparts = e.part ? 2 : 1;
-  // each k-range is whole k-tiles of 64, an even number of them for two stages
-  if (g.K % (kparts * 64 * (NS == 2 ? 2 : 1)) != 0) return hipErrorInvalidValue;
+  // each k-range is an even number of k-tiles of 64 (two stages)
+  if (g.K % (kparts * 128) != 0) return hipErrorInvalidValue;
   const int Mt = (g.Mmax + T::BM - 1) / T::BM, Nt = (g.N + T::BN - 1) / T::BN;
   const int per = (kparts * Mt * Nt + 7) / 8;
   dim3 grid(8 * per);
-  auto kern = gemm_bf16_kernel<WMW, WNW, TMW, TNW, BMAP, EPI, NS>;
+  auto kern = gemm_bf16_kernel<WMW, WNW, TMW, TNW, BMAP, EPI>;
   hipLaunchKernelGGL(kern, grid, dim3(T::NT), 0, st, (const bf16_t*)g.A, g.lda, g.Mdev, Mt, g.N, g.K, b, e);
   return hipGetLastError();
 }
@@ -619,10 +562,13 @@ static hipError_t launch_bf16(const GemmCall& g, hipStream_t st) {
 // Tile shape by row count.  A shape's cost is modelled as the number of rounds
 // of its tiles over the CUs (256 x the workgroups of that shape one CU holds)
 // times the time of one round, t0 + t4k x (k per workgroup) / 4096, fitted to
-// measurements on MI355X at the 7B projections for 320 to 2,236 rows: few rows
+// measurements on MI355X at the 7B projections for 320 to 4,096 rows: few rows
 // leave a 256-row tile mostly empty and give too few tiles to fill the CUs,
 // many rows favour the large tiles' higher MFMA rate, and in between the
-// better shape is the one whose last round is fuller.  The shape does not
+// better shape is the one whose last round is fuller.  A last round with a
+// fraction φ of its slots used costs (partial + (1 - partial) φ) of a round:
+// its tiles share the CUs and memory with fewer others (the row shapes were
+// fitted with partial 0.5, q/k/v and gate/up with 1).  The shape does not
 // change any element's k-order, so results do not depend on it.  g.Mmax is
 // the row count of the call when the caller knows it, else an upper bound.
 namespace {
@@ -634,18 +580,21 @@ struct Shape { int bm, bn, per_cu; float t0, t4k; };
 constexpr Shape kQkvShapes[] = {
     {256, 256, 1, 0.f, 98.f}, {128, 256, 1, 0.f, 67.f}, {64, 256, 2, 0.f, 73.f}, {256, 192, 1, 0.f, 83.f}};
 constexpr Shape kGuShapes[] = {{256, 256, 1, 0.f, 102.f}, {128, 256, 1, 0.f, 63.f}, {64, 256, 2, 0.f, 66.f}};
-// o, down, output head: 256x256, 256x128 (8 waves), 128x128 (4 waves), 64x64 (2 waves)
+// o, down, output head: 256x256, 256x128 (8 waves), 128x128 (4 waves, two per
+// CU), 64x64 (2 waves, four per CU)
 constexpr Shape kRowShapes[] = {
-    {256, 256, 1, 19.8f, 98.4f}, {256, 128, 1, 10.6f, 62.8f}, {128, 128, 1, 5.3f, 41.7f}, {64, 64, 1, 2.f, 14.f}};
+    {256, 256, 1, 18.9f, 97.5f}, {256, 128, 1, 10.5f, 55.5f}, {128, 128, 2, 9.6f, 59.f}, {64, 64, 4, 2.f, 41.7f}};
 
 template <int NSH>
-int pick_shape(const Shape (&sh)[NSH], int M, int N, int K, int kparts = 1) {
+int pick_shape(const Shape (&sh)[NSH], int M, int N, int K, int kparts, float partial) {
   int best = 0;
   float best_cost = 0.f;
   for (int i = 0; i < NSH; ++i) {
     const long tiles = kparts * (long)((M + sh[i].bm - 1) / sh[i].bm) * ((N + sh[i].bn - 1) / sh[i].bn);
     const long slots = (long)kCUs * sh[i].per_cu;
-    const float cost = (float)((tiles + slots - 1) / slots) * (sh[i].t0 + sh[i].t4k * (float)K / kparts / 4096.f);
+    const long full = tiles / slots, rest = tiles - full * slots;
+    const float rounds = (float)full + (rest ? partial + (1.f - partial) * (float)rest / (float)slots : 0.f);
+    const float cost = rounds * (sh[i].t0 + sh[i].t4k * (float)K / kparts / 4096.f);
     if (i == 0 || cost < best_cost) { best = i; best_cost = cost; }
   }
   return best;
@@ -657,31 +606,31 @@ hipError_t gemm(const GemmCall& g, hipStream_t st) {
     const int M = g.Mmax > 0 ? g.Mmax : 1;
     switch (g.kind) {
       case GEMM_QKV:
-        switch (pick_shape(kQkvShapes, M, g.N, g.K)) {
-          case 0: return launch_bf16<BMAP_QKV, EPI_QKV, kWideWM, 2, kWideTM, 4, 2>(g, st);
-          case 1: return launch_bf16<BMAP_QKV, EPI_QKV, 4, 2, 1, 4, 2>(g, st);
-          case 2: return launch_bf16<BMAP_QKV, EPI_QKV, 1, 2, 2, 4, 2>(g, st);
-          default: return launch_bf16<BMAP_QKV, EPI_QKV, 4, 2, 2, 3, 2>(g, st);
+        switch (pick_shape(kQkvShapes, M, g.N, g.K, 1, 1.f)) {
+          case 0: return launch_bf16<BMAP_QKV, EPI_QKV, 4, 2, 2, 4>(g, st);
+          case 1: return launch_bf16<BMAP_QKV, EPI_QKV, 4, 2, 1, 4>(g, st);
+          case 2: return launch_bf16<BMAP_QKV, EPI_QKV, 1, 2, 2, 4>(g, st);
+          default: return launch_bf16<BMAP_QKV, EPI_QKV, 4, 2, 2, 3>(g, st);
         }
       case GEMM_GU:
-        switch (pick_shape(kGuShapes, M, g.N, g.K)) {
-          case 0: return launch_bf16<BMAP_GU, EPI_GU, kWideWM, 2, kWideTM, 4, 2>(g, st);
-          case 1: return launch_bf16<BMAP_GU, EPI_GU, 4, 2, 1, 4, 2>(g, st);
-          default: return launch_bf16<BMAP_GU, EPI_GU, 1, 2, 2, 4, 2>(g, st);
+        switch (pick_shape(kGuShapes, M, g.N, g.K, 1, 1.f)) {
+          case 0: return launch_bf16<BMAP_GU, EPI_GU, 4, 2, 2, 4>(g, st);
+          case 1: return launch_bf16<BMAP_GU, EPI_GU, 4, 2, 1, 4>(g, st);
+          default: return launch_bf16<BMAP_GU, EPI_GU, 1, 2, 2, 4>(g, st);
         }
       case GEMM_RESID:
-        switch (pick_shape(kRowShapes, M, g.N, g.K, g.part ? 2 : 1)) {
-          case 0: return launch_bf16<BMAP_PLAIN, EPI_RESID, kWideWM, 2, kWideTM, 4, 2>(g, st);
-          case 1: return launch_bf16<BMAP_PLAIN, EPI_RESID, NARROW_WM, NARROW_WN, NARROW_TM, NARROW_TN, 3>(g, st);
-          case 2: return launch_bf16<BMAP_PLAIN, EPI_RESID, 2, 2, 2, 2, 3>(g, st);
-          default: return launch_bf16<BMAP_PLAIN, EPI_RESID, 1, 2, 2, 1, 3>(g, st);
+        switch (pick_shape(kRowShapes, M, g.N, g.K, g.part ? 2 : 1, 0.5f)) {
+          case 0: return launch_bf16<BMAP_PLAIN, EPI_RESID, 4, 2, 2, 4>(g, st);
+          case 1: return launch_bf16<BMAP_PLAIN, EPI_RESID, 4, 2, 2, 2>(g, st);
+          case 2: return launch_bf16<BMAP_PLAIN, EPI_RESID, 2, 2, 2, 2>(g, st);
+          default: return launch_bf16<BMAP_PLAIN, EPI_RESID, 1, 2, 2, 1>(g, st);
         }
       default:
-        switch (pick_shape(kRowShapes, M, g.N, g.K)) {
-          case 0: return launch_bf16<BMAP_PLAIN, EPI_STORE, kWideWM, 2, kWideTM, 4, 2>(g, st);
-          case 1: return launch_bf16<BMAP_PLAIN, EPI_STORE, NARROW_WM, NARROW_WN, NARROW_TM, NARROW_TN, 3>(g, st);
-          case 2: return launch_bf16<BMAP_PLAIN, EPI_STORE, 2, 2, 2, 2, 3>(g, st);
-          default: return launch_bf16<BMAP_PLAIN, EPI_STORE, 1, 2, 2, 1, 3>(g, st);
+        switch (pick_shape(kRowShapes, M, g.N, g.K, 1, 0.5f)) {
+          case 0: return launch_bf16<BMAP_PLAIN, EPI_STORE, 4, 2, 2, 4>(g, st);
+          case 1: return launch_bf16<BMAP_PLAIN, EPI_STORE, 4, 2, 2, 2>(g, st);
+          case 2: return launch_bf16<BMAP_PLAIN, EPI_STORE, 2, 2, 2, 2>(g, st);
+          default: return launch_bf16<BMAP_PLAIN, EPI_STORE, 1, 2, 2, 1>(g, st);
         }
     }
   }

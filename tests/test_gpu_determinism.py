@@ -1,13 +1,12 @@
 """Bitwise reproducibility of the forward, and losslessness across batch sizes,
 after another context has used the GPU.
 
-Regression test for a race in the three-stage GEMM pipeline: near the end of k
-the wait before the last stage let that stage's own DMA stay in flight, so the
-last k-tile could be read before it landed.  It showed with small row counts
-(short stages) after other work had run, as different results from run to run;
-here the fp32 `tiny` context runs first, then the bf16 `small` target-only beam
-search runs twice (with and without the logits dump) and must equal itself and
-the speculative decode bitwise.
+A GEMM pipeline whose waits let a k-tile be read before its DMA landed shows up
+here as results that differ from run to run, most readily with small row
+counts (short stages) after other work has run (a three-stage variant of the
+pipeline once had exactly that race).  The fp32 `tiny` context runs first, then
+the bf16 `small` target-only beam search runs twice (with and without the
+logits dump) and must equal itself and the speculative decode bitwise.
 """
 import numpy as np
 import pytest
