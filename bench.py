@@ -32,17 +32,26 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA, published figure
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E, published figure
 
 
+def gemm_code_sha(path=None):
+    """sha256 of the GEMM source with comments and whitespace removed: the
+    counter record stays valid across comment-only edits, not across code ones."""
+    import hashlib
+    import re
+    path = path or os.path.join(ROOT, "paper_2410_05165_amd", "csrc", "gemm.hip")
+    text = open(path, encoding="utf-8").read()
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return hashlib.sha256("".join(text.split()).encode()).hexdigest()
+
+
 def gemm_traffic(kernel_key):
     """HBM bytes per launch of a kernel from the committed rocprofv3 counter record,
-    or None if the kernel source changed since the counters were taken."""
-    import hashlib
+    or None if the kernel code changed since the counters were taken."""
     path = os.path.join(ROOT, "profiles", "traffic_b7.json")
-    src = os.path.join(ROOT, "paper_2410_05165_amd", "csrc", "gemm.hip")
     try:
         rec = json.load(open(path))
-        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
         ent = rec["kernels"][kernel_key]
-        return ent["bytes_per_launch"] if rec["gemm_src_sha256"] == sha else None
+        return ent["bytes_per_launch"] if rec["gemm_code_sha256"] == gemm_code_sha() else None
     except (OSError, KeyError, ValueError):
         return None
 

@@ -249,8 +249,9 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
   // next k-tile fills the other.  Each stage is its own LDS array, named at
   // compile time, so the compiler sees that a step's DMA and fragment reads
   // touch different objects and inserts no waits between them.  (A third stage
-  // was slower on every shape measured: its partial waits cost more than the
-  // extra prefetch distance gained.)
+  // was slower on every shape measured: the compiler tracks only a few
+  // in-flight LDS-DMA stores, so with two stages in flight it drained them all
+  // once per round.)
   // nk is even (each k-range is a multiple of 128, checked on the host)
   load_stage<NA, NB>(st0, wave, A, a_off, Bp, b_off, 0, T::A_BYTES);
   __builtin_amdgcn_s_waitcnt(0);
