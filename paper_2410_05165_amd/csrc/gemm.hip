@@ -170,8 +170,12 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
   __shared__ __align__(1024) unsigned char st1[T::STAGE];
   const int M = *Mdev;
   // XCD-aware tile order: workgroup L is dispatched to XCD L % 8; XCD x owns the
-  // contiguous range x*per .. x*per+per-1 of the tiles in N-major order, so the
-  // M-tiles that share a weight tile run together on one XCD and share its L2.
+  // contiguous range x*per .. x*per+per-1 of the tiles.  Tiles are numbered in
+  // groups of GM M-tiles, N-major inside a group, so the workgroups that run at
+  // once on an XCD cover a few M-tiles times a few N-tiles and share both their
+  // activation and their weight slices in its L2 (numbering all M-tiles first
+  // would give each of them its own activation slice once M exceeds GM tiles:
+  // at 38,400 rows that fetched 28 GB per gate/up launch).
   // A RESID call with e.part splits k in two halves at K/2 for every row count
   // (so a row's arithmetic never depends on the batch): workgroups of the
   // first half add their product into the residual, those of the second store
@@ -184,7 +188,10 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
   if (tk >= ntiles) return;
   const int ks = tk / tiles1, t = tk - ks * tiles1;
   const int kbase = ks * (K / kparts);
-  const int tile_n = t / Mt, tile_m = t - tile_n * Mt;
+  constexpr int GM = 8;
+  const int grp = t / (GM * Nt), gm0 = grp * GM, gsz = Mt - gm0 < GM ? Mt - gm0 : GM;
+  const int tr = t - grp * GM * Nt;
+  const int tile_n = tr / gsz, tile_m = gm0 + tr - tile_n * gsz;
   const int m0 = tile_m * T::BM;
   if (m0 >= M) return;
   // wave index in a scalar register: the DMA row bases and the weight choice
