@@ -174,8 +174,11 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
   // groups of GM M-tiles, N-major inside a group, so the workgroups that run at
   // once on an XCD cover a few M-tiles times a few N-tiles and share both their
   // activation and their weight slices in its L2 (numbering all M-tiles first
-  // would give each of them its own activation slice once M exceeds GM tiles:
-  // at 38,400 rows that fetched 28 GB per gate/up launch).
+  // gives each running workgroup its own activation slice once M is large: at
+  // 38,400 rows that fetched 28 GB per gate/up launch).  GM = 4 measured best
+  // over 1,920-38,400 rows: with many rows the activations, not the weights,
+  // fall out of the Infinity Cache, so an activation slice should serve more
+  // N-tiles than a weight slice serves M-tiles.
   // A RESID call with e.part splits k in two halves at K/2 for every row count
   // (so a row's arithmetic never depends on the batch): workgroups of the
   // first half add their product into the residual, those of the second store
@@ -188,7 +191,7 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
   if (tk >= ntiles) return;
   const int ks = tk / tiles1, t = tk - ks * tiles1;
   const int kbase = ks * (K / kparts);
-  constexpr int GM = 8;
+  constexpr int GM = 4;
   const int grp = t / (GM * Nt), gm0 = grp * GM, gsz = Mt - gm0 < GM ? Mt - gm0 : GM;
   const int tr = t - grp * GM * Nt;
   const int tile_n = tr / gsz, tile_m = gm0 + tr - tile_n * gsz;
