@@ -178,7 +178,10 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
   // 38,400 rows that fetched 28 GB per gate/up launch).  GM = 4 measured best
   // over 1,920-38,400 rows: with many rows the activations, not the weights,
   // fall out of the Infinity Cache, so an activation slice should serve more
-  // N-tiles than a weight slice serves M-tiles.
+  // N-tiles than a weight slice serves M-tiles.  The last group takes the
+  // remainder (GM to 2 GM - 1 M-tiles): a group of one or two M-tiles would
+  // spread over all N-tiles and make its XCDs stream the whole weight matrix
+  // for a few rows (with five 64-row tiles that cost the 320-row step 4%).
   // A RESID call with e.part splits k in two halves at K/2 for every row count
   // (so a row's arithmetic never depends on the batch): workgroups of the
   // first half add their product into the residual, those of the second store
@@ -192,8 +195,10 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
   const int ks = tk / tiles1, t = tk - ks * tiles1;
   const int kbase = ks * (K / kparts);
   constexpr int GM = 4;
-  const int grp = t / (GM * Nt), gm0 = grp * GM, gsz = Mt - gm0 < GM ? Mt - gm0 : GM;
-  const int tr = t - grp * GM * Nt;
+  const int ngrp = Mt / GM > 0 ? Mt / GM : 1;                 // the last group takes the remainder
+  const int g0 = t / (GM * Nt), grp = g0 < ngrp - 1 ? g0 : ngrp - 1;
+  const int gm0 = grp * GM, gsz = grp == ngrp - 1 ? Mt - gm0 : GM;
+  const int tr = t - gm0 * Nt;
   const int tile_n = tr / gsz, tile_m = gm0 + tr - tile_n * gsz;
   const int m0 = tile_m * T::BM;
   if (m0 >= M) return;
