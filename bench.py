@@ -349,6 +349,26 @@ def bench_decode(args, w, eng, pre, dev):
     eng.atspeed_set_timing(False)
     value = B * args.steps / elapsed
     log(f"decode {1e3 * elapsed / args.steps:.1f} ms -> {value:.0f} lists/s; last decode steps {st.n_steps}")
+    # Roofline of the dominant kernel at one fixed shape: the t = 0 verify step
+    # (the context's own sampled draft), gate/up launches bracketed by events.
+    gu_ms, gu_n, rows = 0.0, 0, 0
+    for _ in range(max(3, args.steps)):
+        eng.atspeed_prefill(prefix)
+        eng.atspeed_draft()
+        tn, _, _, td, _ = eng.tree_tensors(B)
+        nn, dd = tn.cpu().numpy(), td.cpu().numpy()
+        rows = int(sum(int((dd[u, :nn[u]] < L).sum()) for u in range(B)))   # forwarded: depth < L
+        eng.atspeed_set_timing(["gu"])
+        eng.atspeed_verify()
+        g = eng.atspeed_get_timing()["gu"]
+        eng.atspeed_set_timing(False)
+        gu_ms += g[0]
+        gu_n += g[1]
+    m = w.target
+    gu_flops = 2.0 * rows * m.d_model * 2 * m.d_ffn
+    gu_avg = gu_ms / gu_n
+    gu_tflops = gu_flops / (gu_avg * 1e-3) / 1e12
+    log(f"t=0 verify: {rows} rows, gate/up {1e3 * gu_avg:.1f} us per launch, {gu_tflops:.0f} TFLOP/s")
     out = {"metric": "top-K lists/sec/GPU (relaxed sampling verification, whole decode)", "value": round(value, 2),
            "unit": "lists/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
            "ms_per_step": round(1e3 * elapsed / args.steps, 3), "higher_is_better": True, "scaling": "weak",
@@ -356,6 +376,11 @@ def bench_decode(args, w, eng, pre, dev):
            "config": {"workload": f"{w.name}: whole decode with {w.mode}, B={B}, P={w.prefix_len}, K={K}, N={w.N}, "
                                   f"gamma={w.gamma}, tau={w.temperature}", "global_batch": B, "seq_len": w.prefix_len,
                       "parallelism": "none (1 GPU)"},
+           "roofline": dict(bound="mfma", kernel=f"gemm_bf16 gate/up at the t=0 verify step ({rows} rows)",
+                            achieved=round(gu_tflops, 2), peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
+                            frac=round(gu_tflops / PEAK_BF16_TFLOPS, 4), traffic=None,
+                            per_launch_flops=gu_flops, avg_launch_ms=round(gu_avg, 4), launches_timed=int(gu_n)),
+           "cpu_baseline": None,
            "kernels": {k: dict(ms_per_step=v[0] / steps_kt, launches_per_step=v[1] / steps_kt)
                        for k, v in kt.items() if v[1]},
            "accepted_levels_last_decode": acc[:st.n_steps].tolist()}
