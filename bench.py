@@ -44,9 +44,12 @@ def gemm_code_sha(path=None):
     return hashlib.sha256("".join(text.split()).encode()).hexdigest()
 
 
-def gemm_traffic(kernel_key):
-    """HBM bytes per launch of a kernel from the committed rocprofv3 counter record,
-    or None if the kernel code changed since the counters were taken."""
+def gemm_traffic(kernel_key, workload):
+    """HBM bytes per launch of a kernel from the committed rocprofv3 counter record
+    (taken on the b7 verify step), or None for another workload or if the kernel
+    code changed since the counters were taken."""
+    if workload != "b7":
+        return None
     path = os.path.join(ROOT, "profiles", "traffic_b7.json")
     try:
         rec = json.load(open(path))
@@ -540,7 +543,7 @@ def main():
     gu_tflops = flops["gu"] / (gu_avg * 1e-3) / 1e12
     roofline = dict(bound="mfma", kernel="gemm_bf16 gate/up (SiLU*up epilogue)",
                     achieved=round(gu_tflops, 2), peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
-                    frac=round(gu_tflops / PEAK_BF16_TFLOPS, 4), traffic=gemm_traffic("gate/up GEMM"),
+                    frac=round(gu_tflops / PEAK_BF16_TFLOPS, 4), traffic=gemm_traffic("gate/up GEMM", w.name),
                     per_launch_flops=flops["gu"], avg_launch_ms=round(gu_avg, 4),
                     launches_timed=int(kt_gu[1]))
 

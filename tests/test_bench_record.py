@@ -37,3 +37,11 @@ def test_code_edits_change_the_hash(tmp_path):
 
 def test_library_source_hashes():
     assert len(bench.gemm_code_sha()) == 64
+
+
+def test_traffic_record_is_for_the_b7_step_only():
+    # the committed counters were taken on the 1,920-row b7 verify step; other
+    # workloads (stress, small) get no traffic figure from them
+    assert bench.gemm_traffic("gate/up GEMM", "stress") is None
+    assert bench.gemm_traffic("gate/up GEMM", "small") is None
+    assert bench.gemm_traffic("no such kernel", "b7") is None
