@@ -82,16 +82,30 @@ __device__ inline int select_smallest(const unsigned long long* keys, int n, int
       if ((k & mk) == pf) atomicAdd(&sh.hist[(k >> shift) & 255], 1);
     }
     __syncthreads();
-    if (tid == 0) {
-      int below = 0, b = 0;
-      for (; b < 256; ++b) {
-        if (below + sh.hist[b] >= sh.need) break;
-        below += sh.hist[b];
+    if (tid < 64) {
+      // wave 0 finds the bucket b where the running count first reaches need:
+      // a prefix sum over 4 buckets per lane, then the one lane holding the
+      // crossing (below b < need <= below b + hist[b]) records it
+      const int h[4] = {sh.hist[4 * tid], sh.hist[4 * tid + 1], sh.hist[4 * tid + 2], sh.hist[4 * tid + 3]};
+      const int s4 = h[0] + h[1] + h[2] + h[3];
+      int incl = s4;
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(incl, o, 64);
+        if (tid >= o) incl += y;
       }
-      sh.need -= below;
-      sh.prefix |= (unsigned long long)b << shift;
-      sh.mask |= 0xFFull << shift;
-      if (sh.hist[b] == sh.need) sh.done = 1;
+      const int need = sh.need;
+      int below = incl - s4, b = -1, bbelow = 0, hb = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (b < 0 && below < need && below + h[q] >= need) { b = 4 * tid + q; bbelow = below; hb = h[q]; }
+        below += h[q];
+      }
+      if (b >= 0) {
+        sh.need = need - bbelow;
+        sh.prefix |= (unsigned long long)b << shift;
+        sh.mask |= 0xFFull << shift;
+        if (hb == need - bbelow) sh.done = 1;
+      }
     }
     __syncthreads();
   }
