@@ -150,11 +150,19 @@ __global__ void plan_tree_rows_kernel(TreeDev tr, const int* lo, const int* hi, 
     if (maxrows) *maxrows = mx;
   }
   __syncthreads();
-  for (int u = 0; u < B; ++u) {
-    const int a = lo[u], cnt = off[u + 1] - off[u];
+  // every row in parallel: its user is the last u with off[u] <= r (users
+  // without rows share their offset with the next one and are never picked)
+  const int total = off[B];
+  for (int r = threadIdx.x; r < total; r += blockDim.x) {
+    int ul = 0, uh = B - 1;
+    while (ul < uh) {
+      const int mid = (ul + uh + 1) >> 1;
+      if (off[mid] <= r) ul = mid; else uh = mid - 1;
+    }
+    const int u = ul;
     const size_t tb = (size_t)u * tr.max_nodes;
-    for (int i = threadIdx.x; i < cnt; i += blockDim.x) {
-      const int s = a + i, r = off[u] + i;
+    {
+      const int s = lo[u] + (r - off[u]);
       const int dep = tr.depth[tb + s];
       rows.user[r] = u;
       rows.token[r] = tr.token[tb + s];
@@ -339,6 +347,9 @@ verify_strict_kernel(StateDev s, TreeDev tr, TrieDev trie, const float* lpt, con
   __shared__ const float* plp[kMaxPar];
   __shared__ unsigned long long sel[2 * kMaxSel];
   __shared__ int ok_s, stop_s, npar_s;
+  constexpr int kTreeLds = 1024;     // nodes whose (depth, path) are staged in LDS
+  __shared__ uint32_t tpath_s[kTreeLds];
+  __shared__ int depth_s[kTreeLds];
   const int u = blockIdx.x, tid = threadIdx.x;
   const int t = s.t[u];
   const int K = s.K;
@@ -357,11 +368,16 @@ verify_strict_kernel(StateDev s, TreeDev tr, TrieDev trie, const float* lpt, con
       pslot[i] = sl; plp[i] = lpt + (tb + sl) * nitem;
     }
   }
+  // the drafted nodes, read once: each selected path is looked up among them
+  // at every level (from global memory that lookup was a chain of dependent loads)
+  const int ntree = tr.n_nodes[u];
+  const bool staged = ntree <= kTreeLds;
+  if (staged)
+    for (int i = tid; i < ntree; i += blockDim.x) { tpath_s[i] = tr.tpath[tb + i]; depth_s[i] = tr.depth[tb + i]; }
   if (tid == 0) stop_s = 0;
   __syncthreads();
   unsigned long long* keys = keys_all + (size_t)u * max_cand;
   int accepted = 0, t_after = t;
-  const int ntree = tr.n_nodes[u];
   for (int j = 1; j <= J + 1; ++j) {
     const int lvl0 = t + j - 1;        // 0-based level of the codes chosen now
     if (lvl0 >= L) break;
@@ -382,8 +398,11 @@ verify_strict_kernel(StateDev s, TreeDev tr, TrieDev trie, const float* lpt, con
       for (int q = 0; q < npar; ++q) if (ppath[q] == ppre) { pi = q; break; }
       mytrie = trie_child(trie, ptrie[pi], code);
       if (!bonus) {
-        for (int i = 0; i < ntree; ++i)
-          if (tr.depth[tb + i] == lvl0 + 1 && tr.tpath[tb + i] == mypath) { myslot = i; break; }
+        for (int i = 0; i < ntree; ++i) {
+          const int di = staged ? depth_s[i] : tr.depth[tb + i];
+          const uint32_t pi = staged ? tpath_s[i] : tr.tpath[tb + i];
+          if (di == lvl0 + 1 && pi == mypath) { myslot = i; break; }
+        }
         if (myslot < 0) atomicAnd(&ok_s, 0);
       }
     }
