@@ -592,10 +592,12 @@ constexpr int kCUs = 256;
 struct Shape { int bm, bn, per_cu; float t0, t4k; };
 // q/k/v: 256x256 (8 waves), 128x256 (8 waves), 64x256 (2 waves, two per CU),
 // 256x192 (8 waves; 3 d_model is a multiple of 192, so no ragged column tile);
-// gate/up: the first three
+// (fitted warm); gate/up: the first three, fitted with the weights arriving cold
+// from HBM as they do in a forward (picks the fastest measured shape at every
+// one of 13 row counts from 320 to 4,096)
 constexpr Shape kQkvShapes[] = {
     {256, 256, 1, 0.f, 98.f}, {128, 256, 1, 0.f, 67.f}, {64, 256, 2, 0.f, 73.f}, {256, 192, 1, 0.f, 83.f}};
-constexpr Shape kGuShapes[] = {{256, 256, 1, 0.f, 102.f}, {128, 256, 1, 0.f, 63.f}, {64, 256, 2, 0.f, 66.f}};
+constexpr Shape kGuShapes[] = {{256, 256, 1, 0.f, 104.f}, {128, 256, 1, 0.f, 70.f}, {64, 256, 2, 0.f, 78.f}};
 // o, down, output head: 256x256, 256x128 (8 waves), 128x128 (4 waves, two per
 // CU), 64x64 (2 waves, four per CU)
 constexpr Shape kRowShapes[] = {
