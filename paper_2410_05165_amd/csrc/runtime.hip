@@ -647,7 +647,14 @@ atspeed_status atspeed_draft(atspeed_ctx* c) {
   HIP_TRY(hipMemsetAsync(c->lo, 0, sizeof(int) * B, c->st));
   launch_plan_tree(c->tree, c->lo, c->state.npath, B, c->P, c->rows, nullptr, c->st);
   HIP_TRY(hipGetLastError());
-  ST_TRY(forward(*c, c->dft, false, B * c->Tmax, c->Tmax, nullptr));
+  // Row bounds of the draft forwards (the row counts themselves stay on the
+  // device): the Y_t paths are prefixes of at most K beams at depths 1..t < L,
+  // and a drafted level holds at most N nodes per user (the strict and the
+  // paper's relaxed draft keep at most N; the exact relaxed draft keeps the
+  // distinct winners of K draws, and N >= K).  The bounds size the launches and
+  // choose the GEMM tiles, so they are kept tight.
+  const int path_rows = std::max(1, cf.K * (L - 1)), level_rows = std::max(1, cf.N);
+  ST_TRY(forward(*c, c->dft, false, B * path_rows, path_rows, nullptr));
   launch_draft_beam_scores(c->state, c->tree, c->dft.lp, c->dft.root, c->nitem, cf.codebook, L, B, c->st);
   HIP_TRY(hipGetLastError());
   for (int j = 1; j <= std::min(cf.gamma, L); ++j) {
@@ -661,7 +668,7 @@ atspeed_status atspeed_draft(atspeed_ctx* c) {
     if (j < std::min(cf.gamma, L)) {  // log-probs of the new level feed the next one
       launch_plan_tree(c->tree, c->lvl_lo, c->lvl_hi, B, c->P, c->rows, nullptr, c->st);
       HIP_TRY(hipGetLastError());
-      ST_TRY(forward(*c, c->dft, false, B * c->Tmax, c->Tmax, nullptr));
+      ST_TRY(forward(*c, c->dft, false, B * level_rows, level_rows, nullptr));
     }
   }
   c->drafted = true;
