@@ -450,11 +450,12 @@ def main():
             tt.append(time.perf_counter() - a)
         r = dict(lists_per_s=B / float(np.median(tt)), ms_per_decode=1e3 * float(np.median(tt)),
                  steps=int(st.n_steps), ms_prefill=st.ms_prefill, ms_draft=st.ms_draft, ms_verify=st.ms_verify,
-                 lists_per_s_decode_only=B / ((st.ms_draft + st.ms_verify) / 1e3), profile=label)
+                 lists_per_s_decode_only=B / ((st.ms_draft + st.ms_verify) / 1e3),
+                 target_tree_rows=int(st.rows_target), profile=label)
         log(f"e2e decode ({label}): {r['ms_per_decode']:.1f} ms ({r['lists_per_s']:.0f} lists/s), steps {st.n_steps}")
         return r, (items.cpu().numpy(), scores.cpu().numpy(), n.cpu().numpy())
 
-    e2e = e2e_l1 = None
+    e2e = e2e_l1 = e2e_reuse = e2e_l1_reuse = None
     if not args.no_e2e:
         e2e, out0 = e2e_natural(eng, "natural")
         # the level-1 start: level 1 from the prefill, speculation from t = 1
@@ -463,6 +464,18 @@ def main():
         eng1.close()
         for x, y in zip(out0, out1):
             assert (x == y).all(), "level-1 start changed the lists"
+        # tree-KV reuse across the verify steps, from t = 0 and from level 1
+        for start in (0, 1):
+            eng2 = Engine(w, tw, dw, cat, mode=mode, seed=key[0] | (key[1] << 32), sd_start_level=start,
+                          reuse_tree_kv=1)
+            r2, out2 = e2e_natural(eng2, "natural, tree-KV reuse" + (", level-1 start" if start else ""))
+            eng2.close()
+            for x, y in zip(out0, out2):
+                assert (x == y).all(), "tree-KV reuse changed the lists"
+            if start:
+                e2e_l1_reuse = r2
+            else:
+                e2e_reuse = r2
 
     # ---- replay-all-accept tree from the GPU's own target beam search
     levels = gpu_target_beam_search(eng, w, prefix, upload_tree)
@@ -580,6 +593,8 @@ def main():
         "e2e_decode": e2e,
         "e2e_decode_level1_start": e2e_l1,
         "e2e_decode_paper_as": e2e_as,
+        "e2e_decode_reuse": e2e_reuse,
+        "e2e_decode_level1_start_reuse": e2e_l1_reuse,
         "decode_bound": probe,
     }
     print(json.dumps(out), flush=True)

@@ -83,6 +83,17 @@ typedef struct {
                            root log-probs (a verify with no drafted levels, no forward)
                            and speculates from t = 1, so no drafted level 1 is wasted.
                            The lists are the same either way.                       */
+  int32_t reuse_tree_kv; /* atspeed_decode_topk: 1 keeps the target's per-layer K/V and
+                           log-probs of every forwarded tree node until the next
+                           verify of the same call, which takes the nodes it shares
+                           with the previous tree (same depth and path: the Y_t
+                           paths and accepted levels) from there and forwards only
+                           the others.  A node's K/V depends only on the prefix and
+                           its path, so the lists are the same either way.  Costs
+                           2 x target n_layers x max_batch x (K*(L-1) + gamma*N) x
+                           d_model K/V elements (plus two log-prob buffers) of
+                           workspace instead of one layer's.  atspeed_verify
+                           itself always forwards the whole tree.  0: off.      */
   void* stream;         /* hipStream_t                                              */
 } atspeed_config;
 
@@ -128,6 +139,7 @@ typedef struct {
   int32_t* accepted;   /* [L, max_batch]: accepted levels per step, -1 once done */
   int32_t* t_after;    /* [L, max_batch]: item level reached after each step     */
   double ms_prefill, ms_draft, ms_verify;  /* stream time per stage (HIP events) */
+  int64_t rows_target; /* target tree rows forwarded over all verify steps       */
 } atspeed_stats;
 
 /* Kernel classes timed by atspeed_get_timing. */

@@ -35,7 +35,8 @@ class Config(C.Structure):
     _fields_ = [("target", Dims), ("draft", Dims), ("L", C.c_int32), ("codebook", C.c_int32),
                 ("K", C.c_int32), ("N", C.c_int32), ("gamma", C.c_int32), ("max_batch", C.c_int32),
                 ("max_prefix", C.c_int32), ("mode", C.c_int32), ("temperature", C.c_float),
-                ("seed", C.c_uint64), ("dtype", C.c_int32), ("sd_start_level", C.c_int32), ("stream", C.c_void_p)]
+                ("seed", C.c_uint64), ("dtype", C.c_int32), ("sd_start_level", C.c_int32),
+                ("reuse_tree_kv", C.c_int32), ("stream", C.c_void_p)]
 
 
 class Weights(C.Structure):
@@ -54,7 +55,8 @@ class Tree(C.Structure):
 
 class Stats(C.Structure):
     _fields_ = [("n_steps", C.c_int32), ("accepted", C.POINTER(C.c_int32)), ("t_after", C.POINTER(C.c_int32)),
-                ("ms_prefill", C.c_double), ("ms_draft", C.c_double), ("ms_verify", C.c_double)]
+                ("ms_prefill", C.c_double), ("ms_draft", C.c_double), ("ms_verify", C.c_double),
+                ("rows_target", C.c_int64)]
 
 
 class KernelTimes(C.Structure):
@@ -115,7 +117,8 @@ class Engine:
 
     def __init__(self, w, target_w: Dict[str, np.ndarray], draft_w: Optional[Dict[str, np.ndarray]],
                  catalog: np.ndarray, max_batch: Optional[int] = None, max_prefix: Optional[int] = None,
-                 device: str = "cuda:0", mode: int = STRICT, stream=None, seed: int = 0, sd_start_level: int = 0):
+                 device: str = "cuda:0", mode: int = STRICT, stream=None, seed: int = 0, sd_start_level: int = 0,
+                 reuse_tree_kv: int = 0):
         import torch
         self.torch = torch
         self.lib = load_library()
@@ -135,6 +138,7 @@ class Engine:
         cfg.mode, cfg.temperature, cfg.seed = mode, w.temperature, seed
         cfg.dtype = BF16 if self.bf16 else FP32
         cfg.sd_start_level = sd_start_level
+        cfg.reuse_tree_kv = reuse_tree_kv
         cfg.stream = self.stream.cuda_stream
         self.cfg = cfg
         self._keep = []

@@ -59,6 +59,7 @@ struct ModelRt {
   void* tk = nullptr;            // tree KV [tree_layers][B*Tmax][d]
   void* tv = nullptr;
   size_t tkv_layer_stride = 0;   // elements between layers (0: one shared buffer)
+  int kv_layer0 = 0;             // first tree-KV layer of the current buffer set (tree-KV reuse)
   size_t pkv_layer_stride = 0;
   float* cosT = nullptr;
   float* sinT = nullptr;
@@ -120,6 +121,21 @@ struct atspeed_ctx {
   int B = 0, P = 0;
   bool prefilled = false;
   bool drafted = false;
+  // tree-KV reuse (cfg.reuse_tree_kv): the target's per-layer tree K/V and its
+  // log-probs by slot live in two buffer sets that alternate between verifies;
+  // a verify of the decode loop takes the nodes the previous one already
+  // forwarded from the other set instead of forwarding them again
+  bool reuse = false;
+  int kv_cur = 0;               // set holding the last verify's K/V and log-probs
+  bool carry_ok = false;        // the last verify was the decode loop's own, since the prefill
+  float* lp_set[2] = {nullptr, nullptr};
+  uint32_t* prev_tpath = nullptr;  // [B*Tmax] path keys of the last verify's tree
+  int* prev_depth = nullptr;       // [B*Tmax]
+  int* prev_n = nullptr;           // [B] its forwarded (or carried) nodes: slots [0, prev_n)
+  int* src = nullptr;              // [B*Tmax] previous slot of each node or -1
+  int* fidx = nullptr;             // [B*Tmax] per user, the nodes still to forward
+  int* fcnt = nullptr;             // [B]
+  int64_t rows_fwd = 0;            // target tree rows forwarded (decode statistics)
   // timing instrumentation
   uint32_t timing_mask = 0;   // kernel classes whose launches are bracketed by events
   std::vector<hipEvent_t> ev_pool;
@@ -203,6 +219,7 @@ atspeed_status check_config(const atspeed_config* cfg) {
   if (c.N < c.K || c.N > kMaxSel) return fail(ATSPEED_E_INVALID, "N must be K..128");
   if (c.gamma < 1) return fail(ATSPEED_E_INVALID, "gamma must be >= 1");
   if (c.sd_start_level != 0 && c.sd_start_level != 1) return fail(ATSPEED_E_INVALID, "sd_start_level must be 0 or 1");
+  if (c.reuse_tree_kv != 0 && c.reuse_tree_kv != 1) return fail(ATSPEED_E_INVALID, "reuse_tree_kv must be 0 or 1");
   if (c.max_batch < 1 || c.max_batch > 1024) return fail(ATSPEED_E_INVALID, "max_batch must be 1..1024");
   if (c.max_prefix < 1) return fail(ATSPEED_E_INVALID, "max_prefix must be >= 1");
   if (c.dtype != ATSPEED_FP32 && c.dtype != ATSPEED_BF16) return fail(ATSPEED_E_INVALID, "dtype");
@@ -298,8 +315,11 @@ void layout(atspeed_ctx& c, const atspeed_config& cfg, int trie_nodes, Arena& a)
     r.pkv_layer_stride = (size_t)B * P * m.d_model;
     r.pk = a.take<char>(pkv * es);
     r.pv = a.take<char>(pkv * es);
-    const int tl = w == 0 ? 1 : m.n_layers;
-    r.tkv_layer_stride = w == 0 ? 0 : (size_t)B * Tm * m.d_model;
+    // the target's tree K/V is dead once a layer's attention has run, so one
+    // buffer serves every layer -- unless it is kept for the next verify
+    const bool keep = w == 0 && cfg.reuse_tree_kv;
+    const int tl = w == 0 ? (keep ? 2 * m.n_layers : 1) : m.n_layers;
+    r.tkv_layer_stride = w == 0 && !keep ? 0 : (size_t)B * Tm * m.d_model;
     r.tk = a.take<char>((size_t)tl * B * Tm * m.d_model * es);
     r.tv = a.take<char>((size_t)tl * B * Tm * m.d_model * es);
     const int half = m.d_model / m.n_heads / 2;
@@ -308,6 +328,17 @@ void layout(atspeed_ctx& c, const atspeed_config& cfg, int trie_nodes, Arena& a)
     r.ropeT = a.take<float>((size_t)c.max_pos * 16 * 4 * 2);
     r.lp = a.take<float>((size_t)B * Tm * c.nitem);
     r.root = a.take<float>((size_t)B * c.nitem);
+    if (keep) {
+      c.reuse = true;
+      c.lp_set[0] = r.lp;
+      c.lp_set[1] = a.take<float>((size_t)B * Tm * c.nitem);
+      c.prev_tpath = a.take<uint32_t>((size_t)B * Tm);
+      c.prev_depth = a.take<int>((size_t)B * Tm);
+      c.prev_n = a.take<int>(B);
+      c.src = a.take<int>((size_t)B * Tm);
+      c.fidx = a.take<int>((size_t)B * Tm);
+      c.fcnt = a.take<int>(B);
+    }
   }
   const size_t M = c.Mmax;
   c.x = a.take<float>(M * dmax);
@@ -449,8 +480,8 @@ atspeed_status forward(atspeed_ctx& c, ModelRt& r, bool prefill, int Mmax, int T
     g.w0 = w[1]; g.w1 = w[2]; g.w2 = w[3]; g.split = d; g.q = c.q;
     char* pk = (char*)r.pk + (size_t)l * r.pkv_layer_stride * es;
     char* pv = (char*)r.pv + (size_t)l * r.pkv_layer_stride * es;
-    char* tk = (char*)r.tk + (size_t)l * r.tkv_layer_stride * es;
-    char* tv = (char*)r.tv + (size_t)l * r.tkv_layer_stride * es;
+    char* tk = (char*)r.tk + (size_t)(r.kv_layer0 + l) * r.tkv_layer_stride * es;
+    char* tv = (char*)r.tv + (size_t)(r.kv_layer0 + l) * r.tkv_layer_stride * es;
     g.kv_mode = prefill ? 0 : 1;
     g.kdst = prefill ? (void*)pk : (void*)tk;
     g.vdst = prefill ? (void*)pv : (void*)tv;
@@ -507,13 +538,25 @@ atspeed_status read_err(atspeed_ctx& c, int* out) {
 // Tree of the context or the caller: the same layout, the caller's arrays.
 TreeDev tree_view(atspeed_ctx& c) { return c.tree; }
 
-atspeed_status tree_forward(atspeed_ctx& c, float* dbg_logits) {
+// carry: the decode loop's own verify, which may take the nodes the previous
+// verify of the loop forwarded (with tree-KV reuse configured).
+atspeed_status tree_forward(atspeed_ctx& c, float* dbg_logits, bool carry = false) {
   HIP_TRY(hipMemsetAsync(c.err, 0, sizeof(int), c.st));
   HIP_TRY(hipMemsetAsync(c.lo, 0, sizeof(int) * c.B, c.st));
   MARK(ATSPEED_K_SELECT);
   launch_tree_index(c.tree, c.trie, c.state, c.B, c.cfg.target.item_base, c.cfg.codebook, c.cfg.L, c.err, c.st);
   HIP_TRY(hipGetLastError());
-  launch_plan_tree(c.tree, c.lo, c.state.nfwd, c.B, c.P, c.rows, c.plan_max, c.st);
+  const bool use_prev = c.reuse && carry && c.carry_ok;
+  const int nset = c.kv_cur ^ 1;   // this verify's buffer set
+  if (c.reuse) {
+    c.carry_ok = false;            // until this verify has completed
+    launch_carry_match(c.tree, c.state, c.prev_tpath, c.prev_depth, use_prev ? c.prev_n : nullptr, c.src, c.fidx,
+                       c.fcnt, c.B, c.st);
+    HIP_TRY(hipGetLastError());
+    launch_plan_tree(c.tree, c.lo, c.fcnt, c.B, c.P, c.rows, c.plan_max, c.st, c.fidx);
+  } else {
+    launch_plan_tree(c.tree, c.lo, c.state.nfwd, c.B, c.P, c.rows, c.plan_max, c.st);
+  }
   HIP_TRY(hipGetLastError());
   // One read-back per forward: the validity word, the row count and the largest
   // per-user row count, so a malformed tree never reaches the forward and every
@@ -524,7 +567,32 @@ atspeed_status tree_forward(atspeed_ctx& c, float* dbg_logits) {
   HIP_TRY(hipMemcpyAsync(&info[2], c.plan_max, sizeof(int), hipMemcpyDeviceToHost, c.st));
   HIP_TRY(hipStreamSynchronize(c.st));
   if (info[0]) return fail(ATSPEED_E_INVALID, "malformed tree (code " + std::to_string(info[0]) + ")");
+  if (c.reuse) {
+    ModelRt& r = c.tgt;
+    const int nl = r.dims.n_layers;
+    const size_t es = esize(c), layer_bytes = r.tkv_layer_stride * es;
+    r.kv_layer0 = nset * nl;
+    r.lp = c.lp_set[nset];
+    if (use_prev) {
+      launch_carry_copy(c.src, c.state.nfwd, c.B, c.Tmax, nl, layer_bytes, r.dims.d_model * (int)es,
+                        (char*)r.tk + (size_t)c.kv_cur * nl * layer_bytes,
+                        (char*)r.tv + (size_t)c.kv_cur * nl * layer_bytes, (char*)r.tk + (size_t)nset * nl * layer_bytes,
+                        (char*)r.tv + (size_t)nset * nl * layer_bytes, c.lp_set[c.kv_cur], c.lp_set[nset], c.nitem,
+                        c.st);
+      HIP_TRY(hipGetLastError());
+    }
+  }
   if (info[1] > 0) ST_TRY(forward(c, c.tgt, false, info[1], info[2], dbg_logits));
+  c.rows_fwd += info[1];
+  if (c.reuse) {
+    // this tree's forwarded and carried nodes are slots [0, nfwd) of the new set
+    const size_t n = (size_t)c.B * c.Tmax;
+    HIP_TRY(hipMemcpyAsync(c.prev_tpath, c.tree.tpath, n * 4, hipMemcpyDeviceToDevice, c.st));
+    HIP_TRY(hipMemcpyAsync(c.prev_depth, c.tree.depth, n * 4, hipMemcpyDeviceToDevice, c.st));
+    HIP_TRY(hipMemcpyAsync(c.prev_n, c.state.nfwd, (size_t)c.B * 4, hipMemcpyDeviceToDevice, c.st));
+    c.kv_cur = nset;
+    c.carry_ok = carry;
+  }
   return ATSPEED_OK;
 }
 
@@ -632,6 +700,7 @@ atspeed_status atspeed_prefill(atspeed_ctx* c, int32_t B, int32_t P, const int32
   HIP_TRY(hipStreamSynchronize(c->st));  // host vectors above go out of scope
   c->prefilled = true;
   c->drafted = false;
+  c->carry_ok = false;
   return ATSPEED_OK;
 }
 
@@ -712,13 +781,17 @@ static atspeed_status accept_on(atspeed_ctx* c, const float* lpt, const float* r
   return ATSPEED_OK;
 }
 
-atspeed_status atspeed_verify(atspeed_ctx* c, int32_t* accepted, int32_t* t_after, float* logits) {
+static atspeed_status verify_step(atspeed_ctx* c, int32_t* accepted, int32_t* t_after, float* logits, bool carry) {
   if (!c) return fail(ATSPEED_E_INVALID, "ctx is null");
   if (!c->prefilled) return fail(ATSPEED_E_STATE, "verify before prefill");
-  ST_TRY(tree_forward(*c, logits));
+  ST_TRY(tree_forward(*c, logits, carry));
   ST_TRY(accept_on(c, c->tgt.lp, c->tgt.root, accepted, t_after));
   c->drafted = false;
   return ATSPEED_OK;
+}
+
+atspeed_status atspeed_verify(atspeed_ctx* c, int32_t* accepted, int32_t* t_after, float* logits) {
+  return verify_step(c, accepted, t_after, logits, false);
 }
 
 atspeed_status atspeed_accept(atspeed_ctx* c, const float* logits, const float* root_logits, int32_t* accepted,
@@ -799,6 +872,7 @@ atspeed_status atspeed_decode_topk(atspeed_ctx* c, int32_t B, int32_t P, const i
     HIP_TRY(hipEventCreate(&ev[0]));
     HIP_TRY(hipEventCreate(&ev[1]));
     stats->n_steps = 0;
+    stats->rows_target = 0;
     stats->ms_prefill = stats->ms_draft = stats->ms_verify = 0;
     HIP_TRY(hipEventRecord(ev[0], c->st));
   }
@@ -814,6 +888,7 @@ atspeed_status atspeed_decode_topk(atspeed_ctx* c, int32_t B, int32_t P, const i
   };
   ST_TRY(atspeed_prefill(c, B, P, prefix, nullptr));
   ST_TRY(lap(timing ? &stats->ms_prefill : nullptr));
+  c->rows_fwd = 0;
   const int L = c->cfg.L;
   std::vector<int> acc(B), ta(B);
   for (int step = 0; step < L; ++step) {
@@ -825,7 +900,7 @@ atspeed_status atspeed_decode_topk(atspeed_ctx* c, int32_t B, int32_t P, const i
       ST_TRY(atspeed_draft(c));
       ST_TRY(lap(timing ? &stats->ms_draft : nullptr));
     }
-    ST_TRY(atspeed_verify(c, c->acc_tmp, c->tafter_tmp, nullptr));
+    ST_TRY(verify_step(c, c->acc_tmp, c->tafter_tmp, nullptr, true));
     HIP_TRY(hipMemcpyAsync(acc.data(), c->acc_tmp, B * 4, hipMemcpyDeviceToHost, c->st));
     HIP_TRY(hipMemcpyAsync(ta.data(), c->tafter_tmp, B * 4, hipMemcpyDeviceToHost, c->st));
     HIP_TRY(hipStreamSynchronize(c->st));
@@ -834,6 +909,7 @@ atspeed_status atspeed_decode_topk(atspeed_ctx* c, int32_t B, int32_t P, const i
       if (stats->accepted) std::copy(acc.begin(), acc.end(), stats->accepted + (size_t)step * c->cfg.max_batch);
       if (stats->t_after) std::copy(ta.begin(), ta.end(), stats->t_after + (size_t)step * c->cfg.max_batch);
       stats->n_steps = step + 1;
+      stats->rows_target = c->rows_fwd;
     }
     if (std::all_of(ta.begin(), ta.end(), [&](int v) { return v >= L; })) break;
   }

@@ -76,9 +76,20 @@ void launch_tree_from_beams(const StateDev& s, const TreeDev& tr, const TrieDev&
 void launch_tree_index(const TreeDev& tr, const TrieDev& trie, const StateDev& s, int B, int item_base, int codebook,
                        int L, int* err, hipStream_t st);
 // Row plan of one forward: nodes with slot in [lo[u], hi[u]) of every user, users
-// in order; writes rows.M and (if maxrows) the largest per-user row count.
+// in order (with idx: entries [lo[u], hi[u]) of the user's node list idx[u*max_nodes..]);
+// writes rows.M and (if maxrows) the largest per-user row count.
 void launch_plan_tree(const TreeDev& tr, const int* lo, const int* hi, int B, int P, const Rows& rows, int* maxrows,
-                      hipStream_t st);
+                      hipStream_t st, const int* idx = nullptr);
+// Tree-KV reuse across the verifies of one decode: matches the nodes to forward
+// (s.nfwd) against the previous tree's forwarded nodes by (depth, path key),
+// writing src (previous slot or -1), the list idx of nodes still to forward and
+// its length cnt (prev_n null: nothing matches); then copies the matched nodes'
+// per-layer K/V rows and log-prob rows between the two buffer sets.
+void launch_carry_match(const TreeDev& tr, const StateDev& s, const uint32_t* prev_tpath, const int* prev_depth,
+                        const int* prev_n, int* src, int* idx, int* cnt, int B, hipStream_t st);
+void launch_carry_copy(const int* src, const int* nfwd, int B, int Tm, int n_layers, size_t layer_bytes,
+                       int row_bytes, const void* k_old, const void* v_old, void* k_new, void* v_new,
+                       const float* lp_old, float* lp_new, int nitem, hipStream_t st);
 // Prefill rows sharing the first S positions: the longest prefix all users have
 // in common is computed on the device (launch_common_prefix); user 0 forwards all
 // P positions, the others P - S, and their first S K/V rows are user 0's

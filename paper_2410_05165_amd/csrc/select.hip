@@ -131,9 +131,10 @@ __global__ void find_beam_slots_kernel(TreeDev tr, StateDev s, int L, int* err) 
   }
 }
 
-// Rows of one forward: nodes with slot in [lo[u], hi[u]) of every user, users in order.
-__global__ void plan_tree_rows_kernel(TreeDev tr, const int* lo, const int* hi, int B, int P, Rows rows,
-                                      int* maxrows) {
+// Rows of one forward: nodes with slot in [lo[u], hi[u]) of every user, users in
+// order; with idx, entries [lo[u], hi[u]) of the user's node list idx instead.
+__global__ void plan_tree_rows_kernel(TreeDev tr, const int* lo, const int* hi, const int* idx, int B, int P,
+                                      Rows rows, int* maxrows) {
   __shared__ int off[1025];
   if (threadIdx.x == 0) {
     int acc = 0, mx = 0;
@@ -162,7 +163,8 @@ __global__ void plan_tree_rows_kernel(TreeDev tr, const int* lo, const int* hi, 
     const int u = ul;
     const size_t tb = (size_t)u * tr.max_nodes;
     {
-      const int s = lo[u] + (r - off[u]);
+      const int e = lo[u] + (r - off[u]);
+      const int s = idx ? idx[tb + e] : e;
       const int dep = tr.depth[tb + s];
       rows.user[r] = u;
       rows.token[r] = tr.token[tb + s];
@@ -178,6 +180,72 @@ __global__ void plan_tree_rows_kernel(TreeDev tr, const int* lo, const int* hi, 
       rows.nanc[r] = dep;
     }
   }
+}
+
+// Tree nodes whose target K/V the previous verify of the same decode already
+// holds.  A node's K/V and log-probs depend only on the prefix and the node's
+// path (its position is P + depth - 1), so a node of this tree with the same
+// (depth, path) as a node forwarded (or carried) by the previous verify takes
+// that node's values instead of a forward.  For every node i < nfwd[u]:
+// src[i] = its slot in the previous tree or -1; idx lists, in order, the nodes
+// with src -1 (the rows to forward) and cnt[u] counts them.  np_prev null: no
+// previous tree, everything is forwarded.
+__global__ void __launch_bounds__(256) carry_match_kernel(TreeDev tr, StateDev s, const uint32_t* prev_tpath,
+                                                          const int* prev_depth, const int* prev_n, int* src,
+                                                          int* idx, int* cnt) {
+  const int u = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const size_t tb = (size_t)u * tr.max_nodes;
+  const int n = s.nfwd[u];
+  const int np = prev_n ? prev_n[u] : 0;
+  __shared__ int wsum[4];
+  int base = 0;
+  for (int c0 = 0; c0 < n; c0 += 256) {   // uniform trip count over the block
+    const int i = c0 + tid;
+    int j = -1;
+    if (i < n) {
+      const int dep = tr.depth[tb + i];
+      const uint32_t key = tr.tpath[tb + i];
+      for (int q = 0; q < np; ++q)
+        if (prev_depth[tb + q] == dep && prev_tpath[tb + q] == key) { j = q; break; }
+      src[tb + i] = j;
+    }
+    // order-preserving compaction of the nodes to forward
+    const bool fwd = i < n && j < 0;
+    const unsigned long long m = __ballot(fwd);
+    const int rank = __popcll(m & ((1ull << lane) - 1ull));
+    if (lane == 0) wsum[wave] = __popcll(m);
+    __syncthreads();
+    int before = base;
+    for (int w = 0; w < wave; ++w) before += wsum[w];
+    if (fwd) idx[tb + before + rank] = i;
+    base += wsum[0] + wsum[1] + wsum[2] + wsum[3];
+    __syncthreads();
+  }
+  if (tid == 0) cnt[u] = base;
+}
+
+// Copies the carried nodes' K/V rows (every layer) and log-prob rows from the
+// previous verify's buffers into this verify's, at the nodes' new slots.  One
+// block per slot; the two buffer sets are disjoint.
+__global__ void __launch_bounds__(256) carry_copy_kernel(const int* src, const int* nfwd, int Tm, int n_layers,
+                                                         size_t layer_bytes, int row_bytes, const char* k_old,
+                                                         const char* v_old, char* k_new, char* v_new,
+                                                         const float* lp_old, float* lp_new, int nitem) {
+  const int node = blockIdx.x, u = node / Tm, i = node - u * Tm;
+  if (i >= nfwd[u]) return;
+  const int j = src[node];
+  if (j < 0) return;
+  const size_t from = (size_t)u * Tm + j;
+  const int nv = row_bytes / 16;
+  for (int l = 0; l < n_layers; ++l) {
+    const size_t o_new = l * layer_bytes + (size_t)node * row_bytes, o_old = l * layer_bytes + from * row_bytes;
+    for (int e = threadIdx.x; e < nv; e += blockDim.x) {
+      reinterpret_cast<uint4*>(k_new + o_new)[e] = reinterpret_cast<const uint4*>(k_old + o_old)[e];
+      reinterpret_cast<uint4*>(v_new + o_new)[e] = reinterpret_cast<const uint4*>(v_old + o_old)[e];
+    }
+  }
+  for (int e = threadIdx.x; e < nitem; e += blockDim.x)
+    lp_new[(size_t)node * nitem + e] = lp_old[from * nitem + e];
 }
 
 // Length of the prefix every user shares with user 0 (tokens equal at every
@@ -444,8 +512,20 @@ void launch_tree_index(const TreeDev& tr, const TrieDev& trie, const StateDev& s
   hipLaunchKernelGGL(find_beam_slots_kernel, dim3(B), dim3(64), 0, st, tr, s, L, err);
 }
 void launch_plan_tree(const TreeDev& tr, const int* lo, const int* hi, int B, int P, const Rows& rows, int* maxrows,
-                      hipStream_t st) {
-  hipLaunchKernelGGL(plan_tree_rows_kernel, dim3(1), dim3(1024), 0, st, tr, lo, hi, B, P, rows, maxrows);
+                      hipStream_t st, const int* idx) {
+  hipLaunchKernelGGL(plan_tree_rows_kernel, dim3(1), dim3(1024), 0, st, tr, lo, hi, idx, B, P, rows, maxrows);
+}
+void launch_carry_match(const TreeDev& tr, const StateDev& s, const uint32_t* prev_tpath, const int* prev_depth,
+                        const int* prev_n, int* src, int* idx, int* cnt, int B, hipStream_t st) {
+  hipLaunchKernelGGL(carry_match_kernel, dim3(B), dim3(256), 0, st, tr, s, prev_tpath, prev_depth, prev_n, src, idx,
+                     cnt);
+}
+void launch_carry_copy(const int* src, const int* nfwd, int B, int Tm, int n_layers, size_t layer_bytes,
+                       int row_bytes, const void* k_old, const void* v_old, void* k_new, void* v_new,
+                       const float* lp_old, float* lp_new, int nitem, hipStream_t st) {
+  hipLaunchKernelGGL(carry_copy_kernel, dim3(B * Tm), dim3(256), 0, st, src, nfwd, Tm, n_layers, layer_bytes,
+                     row_bytes, (const char*)k_old, (const char*)v_old, (char*)k_new, (char*)v_new, lp_old, lp_new,
+                     nitem);
 }
 void launch_common_prefix(const int* prefix, int B, int P, int* out, hipStream_t st) {
   hipLaunchKernelGGL(common_prefix_kernel, dim3(1), dim3(1024), 0, st, prefix, B, P, out);

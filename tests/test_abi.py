@@ -51,7 +51,7 @@ def test_workspace_bytes_and_argument_errors():
     assert lib.atspeed_workspace_bytes(C.byref(_cfg(binding)), C.byref(cat), C.byref(n)) == 0
     assert n.value > 0
     bad = [dict(K=0), dict(N=5), dict(L=5), dict(codebook=300), dict(gamma=0), dict(max_batch=0),
-           dict(mode=7), dict(dtype=3), dict(sd_start_level=2)]
+           dict(mode=7), dict(dtype=3), dict(sd_start_level=2), dict(reuse_tree_kv=2)]
     for kw in bad:
         st = lib.atspeed_workspace_bytes(C.byref(_cfg(binding, **kw)), C.byref(cat), C.byref(n))
         assert st == 1, (kw, st)
@@ -94,3 +94,20 @@ def test_create_rejects_bad_workspace_before_any_launch():
                               C.byref(ctx)) == 3  # too small
     assert lib.atspeed_prefill(None, 1, 1, None, None) == 1
     assert lib.atspeed_verify(None, None, None, None) == 1
+
+
+def test_tree_kv_reuse_workspace():
+    """reuse_tree_kv keeps two sets of the target's per-layer tree K/V and tree
+    log-probs instead of one layer's K/V: the workspace grows by the K/V of
+    2 * n_layers - 1 layers, one more log-prob buffer, and six small index
+    arrays (four slot-sized, two user-sized), up to alignment padding."""
+    binding, lib = _lib()
+    codes, cat = _catalog(binding)
+    n0, n1 = C.c_size_t(0), C.c_size_t(0)
+    assert lib.atspeed_workspace_bytes(C.byref(_cfg(binding)), C.byref(cat), C.byref(n0)) == 0
+    assert lib.atspeed_workspace_bytes(C.byref(_cfg(binding, reuse_tree_kv=1)), C.byref(cat), C.byref(n1)) == 0
+    B, Tm, d, nl, es, nitem = 1, 10 * 3 + 4 * 10, 128, 2, 4, 4 * 256
+    kv = 2 * (2 * nl - 1) * B * Tm * d * es
+    extra = kv + B * Tm * nitem * 4 + 4 * B * Tm * 4 + 2 * B * 4
+    pad = 64 * 256   # each buffer starts on a 256-byte boundary
+    assert extra - pad <= n1.value - n0.value <= extra + pad, (n1.value - n0.value, extra)
