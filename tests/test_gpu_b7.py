@@ -49,7 +49,7 @@ def b7():
     print("[b7] generating weights", flush=True)
     tw, dw = make_weights(w, "target"), make_weights(w, "draft")
     eng = Engine(w, tw, dw, cat)
-    yield dict(w=w, cat=cat, pre=pre, tw=tw, eng=eng)
+    yield dict(w=w, cat=cat, pre=pre, tw=tw, dw=dw, eng=eng)
     eng.close()
 
 
@@ -118,3 +118,35 @@ def test_b7_logits_and_selection(b7):
         np.testing.assert_allclose(sc[v, :nb[v]], [s for _, s in res.beams], rtol=0, atol=1e-4)
     print(f"[b7] selection/acceptance equal to Algorithm 1 for {w.batch - ties} of {w.batch} users "
           f"({ties} decided inside the 1e-3 tie zone)")
+
+
+def test_b7_tree_kv_reuse_keeps_the_lists(b7):
+    """At the full shape, the decode with tree-KV reuse (nodes recurring from the
+    previous verify take its K/V and log-probs instead of a forward) returns the
+    lists, scores and counts of the decode that forwards every node, bitwise,
+    and forwards fewer target tree rows."""
+    import ctypes as C
+    from paper_2410_05165_amd.binding import Engine, Stats
+    w = b7["w"]
+    dev = torch.device("cuda:0")
+    prefix = torch.from_numpy(b7["pre"]).to(dev)
+    eng_r = Engine(w, b7["tw"], b7["dw"], b7["cat"], reuse_tree_kv=1)
+    try:
+        outs, rows = [], []
+        for eng in (b7["eng"], eng_r):
+            items = torch.zeros((w.batch, w.K, w.L), dtype=torch.int32, device=dev)
+            scores = torch.zeros((w.batch, w.K), dtype=torch.float32, device=dev)
+            n = torch.zeros(w.batch, dtype=torch.int32, device=dev)
+            acc = np.full((w.L, w.batch), -9, np.int32)
+            st = Stats()
+            st.accepted = acc.ctypes.data_as(C.POINTER(C.c_int32))
+            eng.atspeed_decode_topk(prefix, items, scores, n, st)
+            torch.cuda.synchronize()
+            outs.append((items.cpu().numpy(), scores.cpu().numpy(), n.cpu().numpy(), acc[:st.n_steps].copy()))
+            rows.append(int(st.rows_target))
+        print(f"[b7 reuse] target tree rows {rows[0]} -> {rows[1]}", flush=True)
+        for x, y in zip(*outs):
+            np.testing.assert_array_equal(x, y)
+        assert 0 < rows[1] < rows[0]
+    finally:
+        eng_r.close()
