@@ -38,12 +38,13 @@ def _decode(eng, w, prefix):
     items = torch.zeros((w.batch, w.K, w.L), dtype=torch.int32, device=DEV)
     scores = torch.zeros((w.batch, w.K), dtype=torch.float32, device=DEV)
     n = torch.zeros(w.batch, dtype=torch.int32, device=DEV)
-    acc = np.full((w.L, w.batch), -9, np.int32)
+    # the library writes step s's row at s * max_batch: size the array by the context
+    acc = np.full((w.L, eng.cfg.max_batch), -9, np.int32)
     st = Stats()
     st.accepted = acc.ctypes.data_as(C.POINTER(C.c_int32))
     eng.atspeed_decode_topk(prefix, items, scores, n, st)
     torch.cuda.synchronize()
-    return (items.cpu().numpy(), scores.cpu().numpy(), n.cpu().numpy(), acc[:st.n_steps].copy()), st
+    return (items.cpu().numpy(), scores.cpu().numpy(), n.cpu().numpy(), acc[:st.n_steps, :w.batch].copy()), st
 
 
 @pytest.mark.parametrize("name,mode,start", [
@@ -102,3 +103,26 @@ def test_public_verify_forwards_whole_tree_with_reuse_configured():
     for a, b in zip(outs[0], outs[1]):
         for x, y in zip(a, b):
             np.testing.assert_array_equal(np.asarray(x), np.asarray(y))
+
+
+def test_reuse_with_fewer_users_than_max_batch():
+    """A context sized for 16 users decodes 5, then all 16, then 3: each call's
+    lists equal those of a context without reuse (the carried slots are indexed
+    by the call's own users; every prefill drops what an earlier call left)."""
+    from paper_2410_05165_amd.binding import Engine
+    w, cat, pre, tw, dw = _case("small")
+    eng0 = Engine(w, tw, dw, cat, reuse_tree_kv=0)
+    eng1 = Engine(w, tw, dw, cat, reuse_tree_kv=1)
+    try:
+        for b in (5, 16, 3):
+            wb = w.with_(batch=b)
+            prefix = torch.from_numpy(np.ascontiguousarray(pre[:b])).to(DEV)
+            print(f"[small, {b} of {w.batch} users] decode without and with reuse", flush=True)
+            ref, st0 = _decode(eng0, wb, prefix)
+            got, st1 = _decode(eng1, wb, prefix)
+            for x, y in zip(got, ref):
+                np.testing.assert_array_equal(x, y)
+            assert 0 < st1.rows_target <= st0.rows_target
+    finally:
+        eng1.close()
+        eng0.close()
