@@ -47,8 +47,11 @@ Parity: RELAXED_EXACT is pinned by chi-square tests of its per-slot output
 against pi_p, of its acceptance frequency against 1 - TVD (Eq. 6) and of its
 level acceptance against (1 - TVD)^K (tests/test_oracle_relaxed.py).
 RELAXED_PAPER is only approximately pi_p by construction (its accepted draws
-follow min(p, q)): parity unpinned beyond the identical-draft case (q = p
-accepts every level) and GPU-vs-oracle agreement on the same streams.
+follow min(p, q)); its parts are pinned where they reduce to a known law: with
+N = K = 1 it is Leviathan et al.'s speculative sampling, whose output follows
+pi_p exactly; with q = p every draft passes and the kept K are a uniform subset
+of the N drafts; q = p accepts every level.  The composite law with 0 < passes
+< K stays parity unpinned beyond GPU-vs-oracle agreement on the same streams.
 """
 from __future__ import annotations
 

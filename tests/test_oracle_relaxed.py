@@ -116,3 +116,56 @@ def test_paper_mode_outputs_valid_distinct_beams():
         assert len(paths) == len(set(paths)) <= 2
         assert all(trie.is_prefix(p) for p in paths)
         assert res.t_after == len(paths[0]) and 0 <= res.accepted <= res.t_after
+
+
+def test_paper_mode_with_one_draft_is_speculative_sampling():
+    """RELAXED_PAPER with N = K = 1 and one drafted level is the speculative
+    sampling of Leviathan et al.: one draft from pi_q, kept with probability
+    min(1, pi_p / pi_q), else one draw from norm(max(0, pi_p - pi_q)).  Its output
+    then follows pi_p exactly (their Theorem), and not pi_q.  A flipped
+    acceptance ratio, a residual of pi_q - pi_p or a draft from pi_p each break
+    one of the two chi-square checks."""
+    trie = Trie(np.array([[a, b] for a in range(CB) for b in range(CB)]))
+    lp, lq = _tables(1)
+    paths, logp, _ = level_dist([((), 0.0)], lp, trie, CB, 1.0)
+    _, logq, _ = level_dist([((), 0.0)], lq, trie, CB, 1.0)
+    p, q = np.exp(logp), np.exp(logq)
+    runs = 6000
+    counts = np.zeros(len(paths))
+    for r in range(runs):
+        rs = Streams((r, 4242), 0)
+        D = draft_paper(lq, trie, [()], [0.0], 1, 1, CB, 1.0, rs, 0)
+        res = verify_paper(lp, lq, trie, [((), 0.0)], [0.0], D, 1, L, CB, 1.0, rs, 0)
+        lvl1 = res.levels[0]
+        assert len(lvl1) == 1
+        counts[paths.index(lvl1[0][0])] += 1
+    chi2_p = float(((counts - runs * p) ** 2 / (runs * p)).sum())
+    chi2_q = float(((counts - runs * q) ** 2 / (runs * q)).sum())
+    # chi-square with 3 dof, alpha = 1e-3: 16.27
+    assert chi2_p < 16.27, (counts / runs, p)
+    assert chi2_q > 16.27, (counts / runs, q)
+
+
+def test_paper_mode_keeps_a_uniform_subset_when_k_pass():
+    """With q = p every one of the N distinct drafts passes (pi_p / pi_q = 1), so
+    the reading of Alg. 2 keeps K of them uniformly at random: over the C(N, K)
+    subsets of draft positions the counts are uniform (keeping the first K
+    drawn, or the K best-scored, fails)."""
+    trie = Trie(np.array([[a, b] for a in range(CB) for b in range(CB)]))
+    lp, _ = _tables(5)
+    N, K, runs = 3, 2, 3000
+    counts = {}
+    for r in range(runs):
+        rs = Streams((r, 99), 0)
+        D = draft_paper(lp, trie, [()], [0.0], 1, N, CB, 1.0, rs, 0)
+        res = verify_paper(lp, lp, trie, [((), 0.0)], [0.0], D, K, L, CB, 1.0, rs, 0)
+        assert res.accepted == 1
+        drafted = [p for p, _ in D[0]]
+        kept = frozenset(drafted.index(p) for p, _ in res.levels[0])
+        assert len(kept) == K
+        counts[kept] = counts.get(kept, 0) + 1
+    assert len(counts) == math.comb(N, K)
+    exp = runs / math.comb(N, K)
+    chi2 = sum((c - exp) ** 2 / exp for c in counts.values())
+    # chi-square with 2 dof, alpha = 1e-3: 13.82
+    assert chi2 < 13.82, counts
