@@ -28,8 +28,12 @@ minus the (n+1)-th) so that a GPU result can be compared outside ties.
 Parity: beam search pinned by brute-force enumeration of the catalog and a
 hand-worked table example; the speculative loop pinned by the losslessness
 invariant (equal to target beam search for any draft) and by the all-accept
-special cases (tests/test_oracle_search.py).  Accepted lengths themselves have
-no definition other than the algorithm: parity unpinned beyond those cases.
+special cases (tests/test_oracle_search.py).  Accepted lengths and the level
+reached are pinned against their definition through the enumeration-pinned
+beam search: level t+i is accepted while the target's own TopK at that level
+lies inside drafted level i, then one target level follows (up to L); checked
+under natural drafts and under drafts that drop one target path at a chosen
+level, the item-completing level included.
 """
 from __future__ import annotations
 
@@ -179,7 +183,8 @@ def sd_decode_strict(lp: Scorer, lq: Scorer, trie, K: int, N: int, gamma: int, L
     """Speculative decoding with strict verification until the items are complete.
 
     ``drafter(Y_paths, J)`` may replace the draft beam search (it must return J
-    levels of paths, each level's parents in the previous level).
+    levels of (path, draft score) beams, each level's parents in the previous
+    level).
     """
     t = 0
     Y: List[Beam] = [((), 0.0)]

@@ -170,3 +170,63 @@ def test_top_margin_and_ties():
     sel, m = top(c, 2)
     assert [p for p, _ in sel] == [(0,), (1,)] and abs(m - 0.4) < 1e-15
     assert top(c, 3)[1] == float("inf")
+
+
+def _accepted_by_definition(want, t, levels, L):
+    """Algorithm 1's accepted length from its definition: level t+i is accepted
+    while the target's TopK at that level (its own beam search, pinned above by
+    enumeration) lies inside drafted level i; then one target level follows."""
+    a = 0
+    for i, lvl in enumerate(levels, start=1):
+        if {p for p, _ in want[t + i - 1]} <= set(lvl):
+            a = i
+        else:
+            break
+    return a, min(L, t + a + 1)
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_accepted_lengths_match_the_subset_definition(seed):
+    K, L = 3, 4
+    w = _wl(seed=seed, K=K, N=6)
+    cat, pre, tgt, lp, lq = _setup(w, user=seed % 2)
+    tr = Trie(cat)
+    want = beam_search(lp, tr, K, L, w.codebook)
+    rng = np.random.default_rng(seed)
+    breaks = []
+
+    def make_drafter(last):
+        return lambda Y, J: drafter(Y, J, last)
+
+    def drafter(Y, J, last):
+        # the target's own levels padded with other children, one target path
+        # dropped at a random level (J + 1: none dropped) or at the last one
+        # (at t = 0 with gamma = L that is the item-completing level L)
+        t = len(Y[0])
+        brk = J if last else int(rng.integers(1, J + 2))
+        breaks.append((t, brk))
+        out, prev = [], list(Y)
+        for i in range(1, J + 1):
+            lvl = [p for p, _ in want[t + i - 1] if p[:-1] in prev]
+            dropped = set()
+            if i == brk:
+                dropped = {lvl[-1]}
+                lvl = lvl[:-1]
+            extra = [p + (c,) for p in prev for c in tr.children(p)
+                     if p + (c,) not in lvl and p + (c,) not in dropped]
+            lvl = lvl + extra[:max(0, w.N - len(lvl))]
+            out.append([(p, 0.0) for p in lvl])
+            prev = lvl
+        return out
+
+    for dr in (None, make_drafter(False), make_drafter(True)):
+        breaks.clear()
+        got, steps = sd_decode_strict(lp, lq, tr, K, w.N, L, L, w.codebook, drafter=dr)
+        assert [p for p, _ in got] == [p for p, _ in want[-1]]
+        for n, st in enumerate(steps):
+            levels = [[p for p, _ in lvl] for lvl in st.drafted]
+            a, t_after = _accepted_by_definition(want, st.t, levels, L)
+            assert (st.result.accepted, st.result.t_after) == (a, t_after), (dr, st.t, a, t_after)
+            if dr is not None:
+                t, brk = breaks[n]
+                assert a == min(brk - 1, len(levels))
