@@ -228,6 +228,8 @@ def decode_replay_as(eng, w, prefix, levels, kids, reps, seed=1):
     decode(True)                                # the library accepts exactly the forced levels
     final = eng.atspeed_get_state(B)
     assert (final[2] == levels[-1][2]).all(), "replayed decode differs from target beam search"
+    for _ in range(2):                          # with the checked decode: 3 warm-ups
+        decode(False)
     torch.cuda.synchronize()
     tt_ = []
     for _ in range(reps):
@@ -439,9 +441,10 @@ def main():
         scores = torch.zeros((B, K), dtype=torch.float32, device=dev)
         n = torch.zeros(B, dtype=torch.int32, device=dev)
         st = Stats()
-        engine.atspeed_decode_topk(prefix, items, scores, n, None)
+        for _ in range(3):                      # warm-up decodes
+            engine.atspeed_decode_topk(prefix, items, scores, n, None)
         torch.cuda.synchronize()
-        reps, tt = 3, []
+        reps, tt = 20, []                       # median of 20 timed decodes
         for _ in range(reps):
             torch.cuda.synchronize()
             a = time.perf_counter()
@@ -481,7 +484,7 @@ def main():
     levels = gpu_target_beam_search(eng, w, prefix, upload_tree)
     e2e_as = None
     if not args.no_e2e:
-        e2e_as = decode_replay_as(eng, w, prefix, levels, kids, reps=3)
+        e2e_as = decode_replay_as(eng, w, prefix, levels, kids, reps=20)
         log(f"e2e decode, replay-paper-AS: {e2e_as['ms_per_decode']:.1f} ms ({e2e_as['lists_per_s']:.0f} lists/s), "
             f"{e2e_as['steps']} steps, accepted levels per step {e2e_as['accepted_mean']:.2f} "
             f"(first step {e2e_as['accepted_first_step_mean']:.2f})")
