@@ -230,11 +230,13 @@ ATSPEED_API atspeed_status atspeed_accept(atspeed_ctx* ctx, const float* logits_
 /* Whole decode: prefill, then draft/verify steps until every user holds L-token
  * items (Algorithm 1 / 2 repeated; the schedule options sd_start_level and
  * reuse_tree_kv of the config change the work, not the lists).  items_dev
- * [B, K, L] int32 codes (best first), scores_dev [B, K] fp32 cumulative target
- * log-probs, n_items_dev [B] number of valid lists (< K only when the catalog
- * has fewer candidates).  stats_host (nullable): steps, per-step accepted levels
- * and levels reached, stage times and target tree rows forwarded.  Synchronises
- * once per step. */
+ * [B, K, L] int32 codes (strict: best first; relaxed modes: in code order),
+ * scores_dev [B, K] fp32 cumulative target
+ * log-probs, n_items_dev [B] number of valid lists (< K when the catalog has
+ * fewer candidates, or in the relaxed modes when a rejected level's residual
+ * distribution max(0, p - q) has fewer candidates than the draws it owes).
+ * stats_host (nullable): steps, per-step accepted levels and levels reached,
+ * stage times and target tree rows forwarded.  Synchronises once per step. */
 ATSPEED_API atspeed_status atspeed_decode_topk(atspeed_ctx* ctx, int32_t B, int32_t P, const int32_t* prefix_dev,
                                    int32_t* items_dev, float* scores_dev, int32_t* n_items_dev,
                                    atspeed_stats* stats_host);
