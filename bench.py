@@ -320,7 +320,7 @@ def decode_bound_probe(eng, w, prefix, levels, steps):
                 what="target-only beam step at t=1: target weights + prefix KV read once per step")
 
 
-def bench_decode(args, w, eng, pre, dev):
+def bench_decode(args, w, eng, pre, dev, make_engine=None):
     """Relaxed workloads: a step is one whole decode (prefill, sampled drafting and
     relaxed verification until every user holds L-token items); the replay-tree
     step of the strict workload does not apply (relaxed verification consumes
@@ -354,6 +354,27 @@ def bench_decode(args, w, eng, pre, dev):
     eng.atspeed_set_timing(False)
     value = B * args.steps / elapsed
     log(f"decode {1e3 * elapsed / args.steps:.1f} ms -> {value:.0f} lists/s; last decode steps {st.n_steps}")
+    # the same decode with tree-KV reuse across its verify steps (same lists)
+    reuse = None
+    if make_engine is not None:
+        out0 = (items.cpu().numpy(), scores.cpu().numpy(), n.cpu().numpy())
+        eng_r = make_engine(reuse_tree_kv=1)
+        st_r = Stats()
+        for _ in range(args.warmup):
+            eng_r.atspeed_decode_topk(prefix, items, scores, n, None)
+        torch.cuda.synchronize()
+        a = time.perf_counter()
+        for _ in range(args.steps):
+            eng_r.atspeed_decode_topk(prefix, items, scores, n, st_r)
+        torch.cuda.synchronize()
+        el_r = time.perf_counter() - a
+        eng_r.close()
+        for x, y in zip(out0, (items.cpu().numpy(), scores.cpu().numpy(), n.cpu().numpy())):
+            assert (x == y).all(), "tree-KV reuse changed the relaxed lists"
+        reuse = dict(ms_per_decode=1e3 * el_r / args.steps, lists_per_s=B * args.steps / el_r,
+                     target_tree_rows=int(st_r.rows_target), target_tree_rows_without_reuse=int(st.rows_target))
+        log(f"decode with tree-KV reuse {reuse['ms_per_decode']:.1f} ms, target rows "
+            f"{st.rows_target} -> {st_r.rows_target}")
     # Roofline of the dominant kernel at one fixed shape: the t = 0 verify step
     # (the context's own sampled draft), gate/up launches bracketed by events.
     gu_ms, gu_n, rows = 0.0, 0, 0
@@ -388,7 +409,8 @@ def bench_decode(args, w, eng, pre, dev):
            "cpu_baseline": None,
            "kernels": {k: dict(ms_per_step=v[0] / steps_kt, launches_per_step=v[1] / steps_kt)
                        for k, v in kt.items() if v[1]},
-           "accepted_levels_last_decode": acc[:st.n_steps].tolist()}
+           "accepted_levels_last_decode": acc[:st.n_steps].tolist(),
+           "decode_reuse": reuse}
     print(json.dumps(out), flush=True)
     eng.close()
 
@@ -430,7 +452,9 @@ def main():
     eng = Engine(w, tw, dw, cat, mode=mode, seed=key[0] | (key[1] << 32))
     log(f"engine ready, workspace {eng.ws.numel() / 2**30:.2f} GiB ({time.time() - t0:.1f}s)")
     if relaxed:
-        return bench_decode(args, w, eng, pre, dev)
+        return bench_decode(args, w, eng, pre, dev,
+                            make_engine=lambda **kw: Engine(w, tw, dw, cat, mode=mode, seed=key[0] | (key[1] << 32),
+                                                            **kw))
     kids = catalog_children(cat)
     prefix = torch.from_numpy(pre).to(dev)
     B, K, L = w.batch, w.K, w.L
