@@ -27,8 +27,13 @@ bf16 (ties to even); everything else, including the residual stream, softmax
 and logits, is fp64.  The fp32 workload rounds nothing.
 
 Parity: pinned by the tests in tests/test_oracle_model.py (closed forms for
-zero-weight and zero-query cases, rotary embedding as complex rotation,
-causality and prefix-cache invariants, hand-computed SwiGLU value).
+zero-weight and zero-query cases, a two-token attention case whose weights
+(1/4, 3/4) follow from the 1/sqrt(d_head) scale, through the plain forward and
+the prefix-cache branch, rotary embedding as complex rotation, causality and
+prefix-cache invariants, hand-computed SwiGLU value).  ``item_log_softmax`` is
+pinned in tests/test_oracle_search.py: it sums to one over every item column,
+and a hand-worked two-level search (tests/golden/normaliser_example.json) gives
+other beams or scores under a per-level normaliser or none.
 """
 from __future__ import annotations
 

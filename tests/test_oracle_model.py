@@ -99,6 +99,43 @@ def test_swiglu_hand_value():
     assert abs(0.5 * 3 * 2 / (1 + math.exp(-2)) - 2.642391233933647) < 1e-12
 
 
+def _one_head_d2(a, b):
+    # d = 2, one head (d_head 2), FFN off, W_q = a I, W_k = b I, W_v = W_o = I,
+    # identity item head; token 0 embeds to sqrt(2) e1, token 1 to sqrt(2) e2.
+    dims = ModelDims(1, 2, 1, 1, 2, 0)
+    W = {"tok_emb": np.array([[math.sqrt(2.0), 0.0], [0.0, math.sqrt(2.0)]], np.float64),
+         "l0.wq": (a * np.eye(2)).astype(np.float64), "l0.wk": (b * np.eye(2)).astype(np.float64),
+         "l0.wv": np.eye(2, dtype=np.float32), "l0.wo": np.eye(2, dtype=np.float32),
+         "l0.w_gate": np.zeros((1, 2), np.float32), "l0.w_up": np.zeros((1, 2), np.float32),
+         "l0.w_down": np.zeros((2, 1), np.float32),
+         "l0.attn_norm": np.ones(2, np.float32), "l0.ffn_norm": np.ones(2, np.float32),
+         "final_norm": np.ones(2, np.float32), "lm_head_item": np.eye(2, dtype=np.float32)}
+    return Decoder(dims, W, "fp32")
+
+
+def test_attention_scale_closed_form():
+    # Sequence (token 0 at position 0, token 1 at position 1).  After the norm the
+    # inputs are h0 = sqrt(2) r e1 and h1 = sqrt(2) r e2 with r = 1/sqrt(1 + eps).
+    # With d_head = 2 the rotary angle of pair 0 at position p is p radians, so
+    # q1 = a sqrt(2) r (-sin 1, cos 1), k0 = b sqrt(2) r e1, k1 = b sqrt(2) r (-sin 1, cos 1):
+    #   q1.k0 = -2 a b r^2 sin 1,   q1.k1 = 2 a b r^2.
+    # Scaled by 1/sqrt(d_head) = 1/sqrt(2), the score gap s11 - s10 is
+    # sqrt(2) a b r^2 (1 + sin 1); a b is chosen to make it ln 3, so token 1's
+    # attention weights are (1/4, 3/4).  Its output is x1 + h0/4 + 3 h1/4 =
+    # sqrt(2) (r/4, 1 + 3r/4), and the identity head reads the ratio r / (4 + 3r).
+    r = 1.0 / math.sqrt(1.0 + RMS_EPS)
+    ab = math.log(3.0) / (math.sqrt(2.0) * r * r * (1.0 + math.sin(1.0)))
+    dec = _one_head_d2(1.5, ab / 1.5)
+    want = r / (4.0 + 3.0 * r)
+    logits, _ = dec.forward(np.array([[0, 1]]), np.arange(2))
+    assert abs(logits[0, 1, 0] / logits[0, 1, 1] - want) < 1e-12
+    # the same value through the prefix-cache branch (prefix = token 0, path = token 1)
+    got = dec.path_logits(dec.prefill(np.array([0])), [(1,)])[0]
+    assert abs(got[0] / got[1] - want) < 1e-12
+    # token 0 sees only itself: its output stays on e1
+    assert abs(logits[0, 0, 1]) < 1e-15 and logits[0, 0, 0] > 0
+
+
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
 def test_causality_and_prefix_cache(dtype):
     w = _tiny_workload(dtype=dtype)

@@ -1,6 +1,7 @@
 """Pins for the oracle's beam search and strict speculative decoding (CPU)."""
 import itertools
 import json
+import math
 import os
 
 import numpy as np
@@ -68,6 +69,45 @@ def test_beam_search_hand_example():
     # beam search is not exhaustive: the exact best pair was pruned at level 1 for K=2
     full = beam_search(table_scorer(table), tr, 100, g["L"], cb)[-1]
     assert [list(p) for p, _ in full[:2]] == g["exhaustive_top2"]
+
+
+class _TableLogits:
+    """Stand-in decoder: raw item logits per path, read back through model_scorer."""
+
+    def __init__(self, masses, item_base, codebook):
+        self.rows = {k: np.log(np.asarray(v, dtype=np.float64)) for k, v in masses.items()}
+        self.base, self.cb = item_base, codebook
+
+    def path_logits(self, cache, toks):
+        keys = [",".join(str(t - self.base - self.cb * l) for l, t in enumerate(tk)) for tk in toks]
+        return np.stack([self.rows[k] for k in keys])
+
+
+def test_item_log_softmax_is_normalised_over_all_item_columns():
+    rng = np.random.default_rng(11)
+    z = rng.standard_normal((5, 1024)) * np.array([[1.0], [10.0], [100.0], [0.01], [300.0]])
+    lp = item_log_softmax(z)
+    np.testing.assert_allclose(np.exp(lp).sum(axis=-1), 1.0, rtol=0, atol=1e-12)
+    # a log-softmax is a shift of the logits by one constant per row
+    d = z - lp
+    np.testing.assert_allclose(d, np.broadcast_to(d[:, :1], d.shape), rtol=0, atol=1e-9)
+
+
+def test_normaliser_hand_example():
+    # Beams and scores of the hand-worked example in tests/golden/normaliser_example.json,
+    # scored through model_scorer exactly as the oracle's searches score a model.
+    with open(os.path.join(GOLDEN, "normaliser_example.json")) as f:
+        g = json.load(f)
+    cb, L = g["codebook"], g["L"]
+    tr = Trie(np.array(g["catalog"]))
+    for base in (0, 5):
+        lp = model_scorer(_TableLogits(g["masses"], base, cb), None, base, cb)
+        for kname, want in g["expected"].items():
+            K = int(kname.split("=")[1])
+            final = beam_search(lp, tr, K, L, cb)[-1]
+            assert [list(p) for p, _ in final] == want["beams"]
+            np.testing.assert_allclose([s for _, s in final], [math.log(a / b) for a, b in want["prob"]],
+                                       rtol=0, atol=1e-12)
 
 
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
