@@ -82,7 +82,9 @@ typedef struct {
                            Algorithm 1 does; 1 first takes level 1 from the prefill's
                            root log-probs (a verify with no drafted levels, no forward)
                            and speculates from t = 1, so no drafted level 1 is wasted.
-                           The lists are the same either way.                       */
+                           The lists are the same either way.  Strict mode only:
+                           with a relaxed mode, 1 makes create (and
+                           workspace_bytes) return ATSPEED_E_INVALID.             */
   int32_t reuse_tree_kv; /* atspeed_decode_topk: 1 keeps the target's per-layer K/V and
                            log-probs of every forwarded tree node until the next
                            verify of the same call, which takes the nodes it shares
@@ -240,6 +242,18 @@ ATSPEED_API atspeed_status atspeed_accept(atspeed_ctx* ctx, const float* logits_
 ATSPEED_API atspeed_status atspeed_decode_topk(atspeed_ctx* ctx, int32_t B, int32_t P, const int32_t* prefix_dev,
                                    int32_t* items_dev, float* scores_dev, int32_t* n_items_dev,
                                    atspeed_stats* stats_host);
+
+/* Log-probabilities a verify step consumes (parity and inspection access).
+ * model 0: the target's log p(. | x, path) of every node the last verify (or
+ * tree_logits) forwarded; model 1: the draft's log q(. | x, path) of every node
+ * the last draft forwarded (the Y_t paths and the drafted levels below the
+ * deepest); both normalised over the L*codebook item-token columns (Sec. 3.1,
+ * constrained generation; p_j and q_j of Algorithms 1 and 2).  lp_dev
+ * [B, max_nodes, L*codebook] fp32 by tree slot (rows of nodes that were not
+ * forwarded are undefined), root_dev [B, L*codebook] fp32 at the last prefix
+ * position; both device, caller-owned, B = the prefilled batch.  Synchronises
+ * the stream.  ATSPEED_E_STATE before prefill, or model 1 without a draft. */
+ATSPEED_API atspeed_status atspeed_logprobs(atspeed_ctx* ctx, int32_t model, float* lp_dev, float* root_dev);
 
 /* State access (host arrays; synchronise the stream).  t [B]; nbeams [B];
  * paths [B, K, L] codes (entries past depth t undefined); scores [B, K] fp32. */

@@ -36,6 +36,13 @@ In both modes the level that completes the item is final whatever the test
 says; when every drafted level is accepted and the item is incomplete, the next
 level is drawn from pi_p (EXACT: K i.i.d. slots; PAPER: Gumbel-top-K).
 
+Logging (paper reading): every acceptance test is recorded with its margin
+|log u - (log pi_p - log pi_q)|, its Philox counter and both values, and every
+Gumbel-top-k draw (drafting, the uniform K-subset, the residual redraw, the
+target's bonus level) with its k + 1 best keyed candidates and their counters,
+so that a GPU result that differs can be checked against the oracle with one
+near-tie decision taken the other way.
+
 Randomness: every uniform comes from Philox4x32-10 (oracle.philox) at counter
 (user, step, level * 2^16 + draw, cand * 4 + tag), tag 0 draft, 1 accept,
 2 subset, 3 target draw / residual; cand = (rank of the parent among the
@@ -112,10 +119,26 @@ def gumbel_argmax(paths, logw, noise) -> Path:
     return best
 
 
-def gumbel_topk(paths, logw, noise, k) -> List[Path]:
-    keyed = [(lw + noise(p), p) for p, lw in zip(paths, logw) if lw != -math.inf]
-    keyed.sort(key=lambda x: (-x[0], x[1]))
-    return [p for _, p in keyed[:k]]
+def gumbel_keys(paths, logw, rs: "Streams", ctr) -> list:
+    """Every candidate of positive weight as (log-weight + Gumbel, path, counter,
+    Gumbel), best first (ties -> smaller path); ``ctr(path)`` is the Philox
+    counter (step, level, draw, cand, tag) of its Gumbel noise.  The first k
+    paths are the Gumbel-top-k draw without replacement."""
+    out = []
+    for p, lw in zip(paths, logw):
+        if lw == -math.inf:
+            continue
+        c = ctr(p)
+        g = rs.g(*c)
+        out.append((lw + g, p, c, g))
+    out.sort(key=lambda x: (-x[0], x[1]))
+    return out
+
+
+def _log_topk(log, kind, lvl, k, keyed):
+    # the draw's decisions: the k best and the first one left out
+    if log is not None:
+        log.append((kind, lvl, k, keyed[:k + 1]))
 
 
 # ---------------------------------------------------------------- drafting
@@ -139,7 +162,7 @@ def draft_exact(lq: Scorer, trie, Y: Sequence[Path], Yq: Sequence[float], J: int
 
 
 def draft_paper(lq: Scorer, trie, Y: Sequence[Path], Yq: Sequence[float], J: int, N: int, codebook: int,
-                tau: float, rs: Streams, step: int) -> List[List[Beam]]:
+                tau: float, rs: Streams, step: int, log: Optional[list] = None) -> List[List[Beam]]:
     """J levels of N distinct draws (Gumbel-top-N) from pi_q; beams carry draft scores, in draw order."""
     t = len(Y[0]) if Y else 0
     parents: List[Beam] = list(zip(Y, Yq))
@@ -148,7 +171,9 @@ def draft_paper(lq: Scorer, trie, Y: Sequence[Path], Yq: Sequence[float], J: int
         lvl = t + j
         paths, logq, sq = level_dist(parents, lq, trie, codebook, tau)
         ci = cand_index([p for p, _ in parents], codebook)
-        pick = gumbel_topk(paths, logq, lambda c: rs.g(step, lvl, 0, ci[c[:-1]] + c[-1], TAG_DRAFT), N)
+        keyed = gumbel_keys(paths, logq, rs, lambda c: (step, lvl, 0, ci[c[:-1]] + c[-1], TAG_DRAFT))
+        _log_topk(log, "draft", lvl, N, keyed)
+        pick = [p for _, p, _, _ in keyed[:N]]
         lvl_beams = [(p, sq[p]) for p in pick]
         out.append(lvl_beams)
         parents = lvl_beams
@@ -233,21 +258,27 @@ def verify_paper(lp: Scorer, lq: Scorer, trie, Y: Sequence[Beam], Yq: Sequence[f
         acc = []
         for i, (y, _) in enumerate(drafted[j - 1]):
             a = ip.get(y, -math.inf) - iq[y]
-            lu = math.log(rs.u(step, lvl, i, 0, TAG_ACCEPT))
+            ctr = (step, lvl, i, 0, TAG_ACCEPT)
+            lu = math.log(rs.u(*ctr))
             if log is not None:
-                log.append(("accept", lvl, i, abs(lu - a) if a > -math.inf else math.inf))
+                log.append(("accept", lvl, i, abs(lu - a) if a > -math.inf else math.inf, ctr, a, lu))
             if lu <= a:
                 acc.append((i, y))
         if len(acc) >= K:
-            keep = sorted(acc, key=lambda iy: (-rs.g(step, lvl, iy[0], 0, TAG_SUBSET), iy[1]))[:K]
-            Tj = [(p, sp[p]) for p in sorted(y for _, y in keep)]
+            # K of the accepted, uniformly: Gumbel-top-K over equal weights
+            draw_of = {y: i for i, y in acc}
+            keyed = gumbel_keys([y for _, y in acc], [0.0] * len(acc), rs,
+                                lambda y: (step, lvl, draw_of[y], 0, TAG_SUBSET))
+            _log_topk(log, "subset", lvl, K, keyed)
+            Tj = [(p, sp[p]) for p in sorted(y for _, y, _, _ in keyed[:K])]
             ok = True
         else:
             ci = cand_index([p for p, _ in T], codebook)
             zero = {y for _, y in acc}
             res = _residual(paths, logp, lambda c: iq.get(c, -math.inf), zero)
-            extra = gumbel_topk(paths, res, lambda c: rs.g(step, lvl, 0, ci[c[:-1]] + c[-1], TAG_TARGET),
-                                K - len(acc))
+            keyed = gumbel_keys(paths, res, rs, lambda c: (step, lvl, 0, ci[c[:-1]] + c[-1], TAG_TARGET))
+            _log_topk(log, "residual", lvl, K - len(acc), keyed)
+            extra = [p for _, p, _, _ in keyed[:K - len(acc)]]
             Tj = [(p, sp[p]) for p in sorted(zero | set(extra))]
             ok = False
         levels.append(Tj)
@@ -260,8 +291,9 @@ def verify_paper(lp: Scorer, lq: Scorer, trie, Y: Sequence[Beam], Yq: Sequence[f
     lvl = t + J + 1
     paths, logp, sp = level_dist(T, lp, trie, codebook, tau)
     ci = cand_index([p for p, _ in T], codebook)
-    pick = gumbel_topk(paths, logp, lambda c: rs.g(step, lvl, 0, ci[c[:-1]] + c[-1], TAG_TARGET), K)
-    Tn = [(p, sp[p]) for p in sorted(pick)]
+    keyed = gumbel_keys(paths, logp, rs, lambda c: (step, lvl, 0, ci[c[:-1]] + c[-1], TAG_TARGET))
+    _log_topk(log, "target_draw", lvl, K, keyed)
+    Tn = [(p, sp[p]) for p in sorted(p for _, p, _, _ in keyed[:K])]
     levels.append(Tn)
     return VerifyResult(J, lvl, Tn, levels)
 

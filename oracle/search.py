@@ -23,7 +23,8 @@ Definitions followed:
   vocabulary; trie-invalid codes are dropped without renormalising.
 
 Scores are fp64.  Every top-n decision records its margin (the n-th score
-minus the (n+1)-th) so that a GPU result can be compared outside ties.
+minus the (n+1)-th) and the two sequences it separates, so that a GPU result
+can be compared outside ties.
 
 Parity: beam search pinned by brute-force enumeration of the catalog and a
 hand-worked table example; the speculative loop pinned by the losslessness
@@ -82,6 +83,7 @@ class Decision:
     kind: str      # "target_topk", "draft_topn"
     level: int     # item level (1-based depth of the selected sequences)
     margin: float  # n-th minus (n+1)-th score; inf if no (n+1)-th candidate
+    pair: Optional[Tuple[Path, Path]] = None   # (n-th selected, (n+1)-th) sequences
 
 
 def extend(beams: Sequence[Beam], lp: Scorer, trie, codebook: int) -> List[Beam]:
@@ -95,11 +97,19 @@ def extend(beams: Sequence[Beam], lp: Scorer, trie, codebook: int) -> List[Beam]
     return out
 
 
+def top_boundary(cands: List[Beam], n: int) -> Tuple[List[Beam], float, Optional[Tuple[Path, Path]]]:
+    """The n best by score (ties: lexicographically smaller path first), the
+    margin and the pair of sequences the margin separates."""
+    srt = sorted(cands, key=lambda b: (-b[1], b[0]))
+    if len(srt) > n:
+        return srt[:n], srt[n - 1][1] - srt[n][1], (srt[n - 1][0], srt[n][0])
+    return srt[:n], float("inf"), None
+
+
 def top(cands: List[Beam], n: int) -> Tuple[List[Beam], float]:
     """The n best by score (ties: lexicographically smaller path first) and the margin."""
-    srt = sorted(cands, key=lambda b: (-b[1], b[0]))
-    margin = (srt[n - 1][1] - srt[n][1]) if len(srt) > n else float("inf")
-    return srt[:n], margin
+    sel, margin, _ = top_boundary(cands, n)
+    return sel, margin
 
 
 def beam_search(lp: Scorer, trie, K: int, L: int, codebook: int,
@@ -108,9 +118,9 @@ def beam_search(lp: Scorer, trie, K: int, L: int, codebook: int,
     beams: List[Beam] = [((), 0.0)]
     levels = []
     for lvl in range(1, L + 1):
-        beams, m = top(extend(beams, lp, trie, codebook), K)
+        beams, m, pr = top_boundary(extend(beams, lp, trie, codebook), K)
         if log is not None:
-            log.append(Decision("target_topk", lvl, m))
+            log.append(Decision("target_topk", lvl, m, pr))
         levels.append(beams)
     return levels
 
@@ -128,9 +138,9 @@ def draft_levels(lq: Scorer, trie, Y: Sequence[Path], J: int, N: int, codebook: 
     out = []
     for j in range(1, J + 1):
         cands = extend(cur, lq, trie, codebook)
-        cur, m = top(cands, N)
+        cur, m, pr = top_boundary(cands, N)
         if log is not None:
-            log.append(Decision("draft_topn", t + j, m))
+            log.append(Decision("draft_topn", t + j, m, pr))
         out.append(cur)
     return out
 
@@ -151,9 +161,9 @@ def verify_strict(lp: Scorer, trie, Y: Sequence[Beam], drafted: Sequence[Sequenc
     T: List[Beam] = list(Y)
     levels = []
     for j in range(1, J + 1):
-        Tj, m = top(extend(T, lp, trie, codebook), K)
+        Tj, m, pr = top_boundary(extend(T, lp, trie, codebook), K)
         if log is not None:
-            log.append(Decision("target_topk", t + j, m))
+            log.append(Decision("target_topk", t + j, m, pr))
         levels.append(Tj)
         ok = {p for p, _ in Tj} <= set(drafted[j - 1])
         if t + j == L:
@@ -162,9 +172,9 @@ def verify_strict(lp: Scorer, trie, Y: Sequence[Beam], drafted: Sequence[Sequenc
             return VerifyResult(j - 1, t + j, Tj, levels)
         T = Tj
     # every drafted level accepted and the item is not complete: one target level more
-    Tn, m = top(extend(T, lp, trie, codebook), K)
+    Tn, m, pr = top_boundary(extend(T, lp, trie, codebook), K)
     if log is not None:
-        log.append(Decision("target_topk", t + J + 1, m))
+        log.append(Decision("target_topk", t + J + 1, m, pr))
     levels.append(Tn)
     return VerifyResult(J, t + J + 1, Tn, levels)
 

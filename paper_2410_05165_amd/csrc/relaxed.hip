@@ -398,7 +398,11 @@ verify_relaxed_kernel(StateDev s, TreeDev tr, TrieDev trie, const float* lpt, co
           sh.count = npos;
         }
         __syncthreads();
-        const int extra = select_smallest(keys, n, min(K - m, sh.count), sel, sh);
+        // every wave takes the count into a register before select_smallest's
+        // thread 0 reuses sh.count as its output counter
+        const int npos = sh.count;
+        __syncthreads();
+        const int extra = select_smallest(keys, n, min(K - m, npos), sel, sh);
         for (int i = tid; i < extra; i += blockDim.x) fin[m + i] = (uint32_t)sel[i];
         mo = m + extra;
       }

@@ -226,6 +226,8 @@ atspeed_status check_config(const atspeed_config* cfg) {
   if (c.mode != ATSPEED_STRICT && c.mode != ATSPEED_RELAXED_EXACT && c.mode != ATSPEED_RELAXED_PAPER)
     return fail(ATSPEED_E_INVALID, "mode must be strict, relaxed-exact or relaxed-paper");
   if (c.mode != ATSPEED_STRICT && !(c.temperature > 0.f)) return fail(ATSPEED_E_INVALID, "temperature must be > 0");
+  if (c.mode != ATSPEED_STRICT && c.sd_start_level != 0)
+    return fail(ATSPEED_E_INVALID, "sd_start_level 1 is defined for strict verification only");
   ST_TRY(check_dims(c.target, c, "target"));
   if (c.draft.n_layers > 0) {
     ST_TRY(check_dims(c.draft, c, "draft"));
@@ -808,6 +810,19 @@ atspeed_status atspeed_accept(atspeed_ctx* c, const float* logits, const float* 
   HIP_TRY(log_softmax_rows(logits, c->Mall, c->B * c->Tmax, c->nitem, nullptr, c->tgt.lp, nullptr, c->st));
   HIP_TRY(log_softmax_rows(root_logits, c->Mb, c->B, c->nitem, nullptr, c->tgt.root, nullptr, c->st));
   ST_TRY(accept_on(c, c->tgt.lp, c->tgt.root, accepted, t_after));
+  HIP_TRY(hipStreamSynchronize(c->st));
+  return ATSPEED_OK;
+}
+
+atspeed_status atspeed_logprobs(atspeed_ctx* c, int32_t model, float* lp, float* root) {
+  if (!c || !lp || !root) return fail(ATSPEED_E_INVALID, "null argument");
+  if (model != 0 && model != 1) return fail(ATSPEED_E_INVALID, "model must be 0 (target) or 1 (draft)");
+  if (!c->prefilled) return fail(ATSPEED_E_STATE, "logprobs before prefill");
+  const ModelRt& m = model == 0 ? c->tgt : c->dft;
+  if (!m.present) return fail(ATSPEED_E_STATE, "context has no draft model");
+  const size_t row = (size_t)c->nitem * sizeof(float);
+  HIP_TRY(hipMemcpyAsync(lp, m.lp, (size_t)c->B * c->Tmax * row, hipMemcpyDeviceToDevice, c->st));
+  HIP_TRY(hipMemcpyAsync(root, m.root, (size_t)c->B * row, hipMemcpyDeviceToDevice, c->st));
   HIP_TRY(hipStreamSynchronize(c->st));
   return ATSPEED_OK;
 }

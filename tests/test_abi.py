@@ -51,7 +51,8 @@ def test_workspace_bytes_and_argument_errors():
     assert lib.atspeed_workspace_bytes(C.byref(_cfg(binding)), C.byref(cat), C.byref(n)) == 0
     assert n.value > 0
     bad = [dict(K=0), dict(N=5), dict(L=5), dict(codebook=300), dict(gamma=0), dict(max_batch=0),
-           dict(mode=7), dict(dtype=3), dict(sd_start_level=2), dict(reuse_tree_kv=2)]
+           dict(mode=7), dict(dtype=3), dict(sd_start_level=2), dict(reuse_tree_kv=2),
+           dict(mode=1, sd_start_level=1), dict(mode=2, sd_start_level=1)]
     for kw in bad:
         st = lib.atspeed_workspace_bytes(C.byref(_cfg(binding, **kw)), C.byref(cat), C.byref(n))
         assert st == 1, (kw, st)

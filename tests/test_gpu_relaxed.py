@@ -27,10 +27,18 @@ def _key_seed(w):
     return [int(k[0]), int(k[1])], int(k[0]) | (int(k[1]) << 32)
 
 
+# (K, N, temperature): the tiny workload's own, and the widest selection (128)
+# at a temperature where a rejected level owes more residual draws than one
+# wave holds (the oracle redraws 50 and 77 of 128 in the paper reading)
+WIDTHS = {"k10": (10, 10, 1.0), "k128": (128, 128, 0.2)}
+
+
+@pytest.mark.parametrize("width", list(WIDTHS))
 @pytest.mark.parametrize("mode", list(MODES))
-def test_tiny_relaxed_steps_match_oracle(mode):
+def test_tiny_relaxed_steps_match_oracle(mode, width):
     from paper_2410_05165_amd.binding import Engine
-    e = env("tiny")
+    K, N, tau = WIDTHS[width]
+    e = env("tiny", K=K, N=N, temperature=tau)
     w = e["w"]
     key, seed = _key_seed(w)
     eng = Engine(w, e["tw"], e["dw"], e["cat"], mode=MODES[mode], seed=seed)
@@ -50,7 +58,7 @@ def test_tiny_relaxed_steps_match_oracle(mode):
         t, nb, paths, sc = eng.atspeed_get_state(1)
         got = [tuple(int(c) for c in paths[0, k, :t[0]]) for k in range(nb[0])]
         want = [p for p, _ in res.beams]
-        print(f"[{mode}] step {i}: t {t0}->{t[0]} accepted {int(acc[0])} (oracle {res.t_after}, {res.accepted}), "
+        print(f"[{mode} {width}] step {i}: t {t0}->{t[0]} accepted {int(acc[0])} (oracle {res.t_after}, {res.accepted}), "
               f"{len(got)} beams")
         assert int(ta[0]) == res.t_after and int(acc[0]) == res.accepted
         assert got == want

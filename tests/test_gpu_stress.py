@@ -10,7 +10,8 @@ holds at any size:
 * batch invariance: the first 4 users decoded as a batch of 4 get bitwise the
   lists they got in the batch of 128;
 * selection and acceptance on the GPU's t = 0 logits equal the oracle's
-  Algorithm 1 for sampled users (up to ties inside SEL_TIE).
+  Algorithm 1 for sampled users (a difference only where one near-tie
+  decision, margin below 1e-3, taken the other way gives the GPU's result).
 The model path at this width is checked against the oracle by the 7B test, and
 1,024-token prefixes by the 'longctx' variant.
 """
@@ -21,7 +22,7 @@ pytestmark = pytest.mark.gpu
 
 torch = pytest.importorskip("torch")
 
-from _gpu_common import SEL_TIE, logit_table, upload_tree  # noqa: E402
+from _gpu_common import flipped_scorer, logit_table, strict_tie, upload_tree  # noqa: E402
 from synth import get_workload, make_catalog, make_prefixes, make_weights  # noqa: E402
 from oracle.search import verify_strict  # noqa: E402
 from oracle.trie import Trie  # noqa: E402
@@ -124,8 +125,13 @@ def test_stress_selection_matches_algorithm_1(stress):
         res = verify_strict(lp, trie, [((), 0.0)], D, w.K, w.L, w.codebook, log)
         got = [tuple(int(c) for c in sp[u, k, :t[u]]) for k in range(nb[u])]
         print(f"[stress] user {u}: accepted {acc[u]} (oracle {res.accepted}), t -> {ta[u]}")
-        if got != [p for p, _ in res.beams] or acc[u] != res.accepted or ta[u] != res.t_after:
-            assert min(d.margin for d in log) < SEL_TIE
+
+        def same(r):
+            return [p for p, _ in r.beams] == got and r.accepted == acc[u] and r.t_after == ta[u]
+        if not same(res):
+            d = strict_tie(log, lambda d: verify_strict(flipped_scorer(lp, d, w.codebook), trie, [((), 0.0)], D,
+                                                        w.K, w.L, w.codebook), same)
+            assert d is not None, (u, got, [p for p, _ in res.beams])
             ties += 1
             continue
         np.testing.assert_allclose(ssc[u, :nb[u]], [s for _, s in res.beams], rtol=0, atol=1e-4)
