@@ -179,8 +179,12 @@ ATSPEED_API atspeed_status atspeed_create(const atspeed_config* cfg, const atspe
 ATSPEED_API void atspeed_destroy(atspeed_ctx* ctx);
 ATSPEED_API const char* atspeed_last_error(void);
 
-/* Prefill: one causal forward of the target (and draft) over B prefixes of P
- * tokens each (prefix_dev [B, P] int32, device), filling the prefix KV caches and
+/* Prefill of the users' histories x (task formulation, Sec. 2): the prefilling
+ * stage that the appendix case study separates from decoding (its time is the
+ * same with and without speculative decoding), which every verify's tree
+ * attention then reads (Sec. 3.3).  One causal forward of the target (and draft)
+ * over B prefixes of P tokens each (prefix_dev [B, P] int32, device), filling the
+ * prefix KV caches and
  * the root log-probs (logits at the last prefix position).  Positions that all
  * users share with user 0 (a common prompt; found on the device, one read-back)
  * are forwarded once and their K/V copied to the other users: the results are
