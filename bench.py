@@ -1,19 +1,21 @@
 #!/usr/bin/env python3
-"""Throughput of the AtSpeed verify step on one MI355X.
+"""Throughput of the AtSpeed top-K decode on one MI355X.
 
 Workload (default): the LLaMA-7B-shaped target (32 layers, d 4096, 32 heads,
 FFN 11008, vocabulary 33,024 with 1,024 item tokens), 4-layer draft, 100,000
 random 4-token items, 32 users with 144-token prefixes, K = 10, N = 20,
 gamma = 4, strict verification; random-init bf16 weights N(0, 0.02).
 
-A step is one ``atspeed_verify`` over the batch: tree planning, one target
-forward over the t = 0 tree (drafted depths 1..3 forwarded, 60 nodes per user),
-item log-softmax, cumulative log-probs, trie-constrained TopK and strict
-acceptance.  The tree is the replay-all-accept tree (every drafted level holds
-the target's TopK, padded to N with other valid extensions), so each step
-completes the top-K lists of all users: value = users x steps / time.  Random
-weights make natural acceptance ~0, so the end-to-end decode (prefill + draft +
-verify until complete, natural acceptance) is reported beside it.
+A step is one ``atspeed_decode_topk`` over the batch: prefill of target and
+draft, then speculative steps (device drafting, one target forward over the
+tree, item log-softmax, cumulative log-probs, trie-constrained TopK, strict
+acceptance) until every user's top-K list is complete, with the library's own
+drafts (natural acceptance; random weights accept about nothing).  value =
+users x steps / time.  Beside it: the same decode with the level-1 start and
+tree-KV reuse, under the replay-paper-AS and replay-all-accept profiles, the
+t = 0 verify step alone, the decode-bound probe and the relaxed (config-4)
+decode; the roofline kernel is the target's gate/up GEMM over the timed
+decodes.
 
 Prints ONE JSON line.  Progress goes to stderr.
 """
@@ -259,11 +261,13 @@ def gpu_target_beam_search(eng, w, prefix, upload_tree):
     return levels
 
 
-def cpu_baseline(w, tw, pre, cat, tree_paths):
-    """The oracle's verify step for one user of the same workload (fp64, per-path forwards)."""
-    import numpy as np
+def cpu_baseline(w, tw, dw, pre, cat, gpu_items):
+    """The oracle's whole decode of user 0 under the natural profile (fp64): the
+    target's and the draft's prefill, then speculative steps -- draft beam search
+    (Eq. 1), per-path target forwards of the levels Algorithm 1 examines,
+    strict verification -- until the top-K list is complete."""
     from oracle.model import Decoder
-    from oracle.search import model_scorer, verify_strict
+    from oracle.search import model_scorer, sd_decode_strict
     from oracle.trie import Trie
     try:
         from threadpoolctl import threadpool_info
@@ -271,21 +275,21 @@ def cpu_baseline(w, tw, pre, cat, tree_paths):
     except Exception:
         threads = os.cpu_count() or 1
     trie = Trie(cat)
-    dec = Decoder(w.target, tw, w.dtype, cache_f64=False)
-    log("cpu baseline: oracle prefill of user 0 (untimed set-up)")
-    cache = dec.prefill(pre[0])
-    lp = model_scorer(dec, cache, w.target.item_base, w.codebook)
-    D = [[p for p in tree_paths if len(p) == d] for d in range(1, w.L + 1)]
-    fwd = [p for lvl in D[:-1] for p in lvl]
-    log("cpu baseline: oracle verify of user 0 (timed)")
+    tgt = Decoder(w.target, tw, w.dtype, cache_f64=False)
+    dft = Decoder(w.draft, dw, w.dtype)
+    log("cpu baseline: oracle decode of user 0 (timed: prefill of both models + speculative steps)")
     t0 = time.perf_counter()
-    lp(fwd)                        # logits of every forwarded tree node (one causal forward per path)
-    res = verify_strict(lp, trie, [((), 0.0)], D, w.K, w.L, w.codebook)
+    lp = model_scorer(tgt, tgt.prefill(pre[0]), w.target.item_base, w.codebook)
+    lq = model_scorer(dft, dft.prefill(pre[0]), w.draft.item_base, w.codebook)
+    final, steps = sd_decode_strict(lp, lq, trie, w.K, w.N, w.gamma, w.L, w.codebook)
     dt = time.perf_counter() - t0
+    got = [tuple(int(c) for c in row) for row in gpu_items]
+    same = sum(1 for p, _ in final if p in set(got))
     return dict(value=1.0 / dt, unit="lists/s", cores=int(threads), kind="oracle",
-                sample=f"verify step of 1 of {w.batch} users (t=0 replay tree, {len(fwd)} forwarded nodes: "
-                       f"per-path fp64 forwards of all of them + Algorithm 1), {dt:.1f} s; "
-                       f"accepted={res.accepted}, host cpus={os.cpu_count()}"), res
+                sample=f"whole decode of user 0 of {w.batch} (natural drafts: fp64 prefill of target and draft, "
+                       f"{len(steps)} speculative steps of draft beam search + per-path target forwards + "
+                       f"Algorithm 1), {dt:.1f} s; its top-{w.K} list shares {same} of {w.K} items with the GPU's "
+                       f"(bf16 vs fp64 logits); host cpus={os.cpu_count()}")
 
 
 def decode_bound_probe(eng, w, prefix, levels, steps):
@@ -320,99 +324,78 @@ def decode_bound_probe(eng, w, prefix, levels, steps):
                 what="target-only beam step at t=1: target weights + prefix KV read once per step")
 
 
-def bench_decode(args, w, eng, pre, dev, make_engine=None):
-    """Relaxed workloads: a step is one whole decode (prefill, sampled drafting and
-    relaxed verification until every user holds L-token items); the replay-tree
-    step of the strict workload does not apply (relaxed verification consumes
-    the context's own sampled draft)."""
+def timed_decodes(eng, w, prefix, steps, warmup, roofline=True):
+    """``warmup`` untimed decodes, then exactly ``steps`` timed ones (host clock,
+    bracketed by device synchronisation).  With ``roofline`` the target's gate/up
+    GEMM launches inside the timed region are bracketed by HIP events on the
+    library's stream, with their algorithmic flops (2 x rows x 2f x d per launch)."""
+    import ctypes as C
     import numpy as np
     import torch
     from paper_2410_05165_amd.binding import Stats
     B, K, L = w.batch, w.K, w.L
-    prefix = torch.from_numpy(pre).to(dev)
-    items = torch.zeros((B, K, L), dtype=torch.int32, device=dev)
-    scores = torch.zeros((B, K), dtype=torch.float32, device=dev)
-    n = torch.zeros(B, dtype=torch.int32, device=dev)
-    for _ in range(args.warmup):
+    items = torch.zeros((B, K, L), dtype=torch.int32, device=prefix.device)
+    scores = torch.zeros((B, K), dtype=torch.float32, device=prefix.device)
+    n = torch.zeros(B, dtype=torch.int32, device=prefix.device)
+    for _ in range(warmup):
         eng.atspeed_decode_topk(prefix, items, scores, n, None)
     torch.cuda.synchronize()
-    acc = np.zeros((L, B), np.int32)
+    acc = np.zeros((L, eng.cfg.max_batch), np.int32)
     st = Stats()
-    import ctypes as C
     st.accepted = acc.ctypes.data_as(C.POINTER(C.c_int32))
-    a = time.perf_counter()
-    for _ in range(args.steps):
-        eng.atspeed_decode_topk(prefix, items, scores, n, st)
+    if roofline:
+        eng.atspeed_set_timing(["gu"], target_only=True)
+    per = []
     torch.cuda.synchronize()
-    elapsed = time.perf_counter() - a
-    # breakdown by kernel class: a separate pass with every launch bracketed
-    steps_kt = max(1, args.steps // 2)
-    eng.atspeed_set_timing(True)
-    for _ in range(steps_kt):
-        eng.atspeed_decode_topk(prefix, items, scores, n, None)
-    kt = eng.atspeed_get_timing()
-    eng.atspeed_set_timing(False)
-    value = B * args.steps / elapsed
-    log(f"decode {1e3 * elapsed / args.steps:.1f} ms -> {value:.0f} lists/s; last decode steps {st.n_steps}")
-    # the same decode with tree-KV reuse across its verify steps (same lists)
-    reuse = None
-    if make_engine is not None:
-        out0 = (items.cpu().numpy(), scores.cpu().numpy(), n.cpu().numpy())
-        eng_r = make_engine(reuse_tree_kv=1)
-        st_r = Stats()
-        for _ in range(args.warmup):
-            eng_r.atspeed_decode_topk(prefix, items, scores, n, None)
-        torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
         a = time.perf_counter()
-        for _ in range(args.steps):
-            eng_r.atspeed_decode_topk(prefix, items, scores, n, st_r)
-        torch.cuda.synchronize()
-        el_r = time.perf_counter() - a
-        eng_r.close()
-        for x, y in zip(out0, (items.cpu().numpy(), scores.cpu().numpy(), n.cpu().numpy())):
-            assert (x == y).all(), "tree-KV reuse changed the relaxed lists"
-        reuse = dict(ms_per_decode=1e3 * el_r / args.steps, lists_per_s=B * args.steps / el_r,
-                     target_tree_rows=int(st_r.rows_target), target_tree_rows_without_reuse=int(st.rows_target))
-        log(f"decode with tree-KV reuse {reuse['ms_per_decode']:.1f} ms, target rows "
-            f"{st.rows_target} -> {st_r.rows_target}")
-    # Roofline of the dominant kernel at one fixed shape: the t = 0 verify step
-    # (the context's own sampled draft), gate/up launches bracketed by events.
-    gu_ms, gu_n, rows = 0.0, 0, 0
-    for _ in range(max(3, args.steps)):
-        eng.atspeed_prefill(prefix)
-        eng.atspeed_draft()
-        tn, _, _, td, _ = eng.tree_tensors(B)
-        nn, dd = tn.cpu().numpy(), td.cpu().numpy()
-        rows = int(sum(int((dd[u, :nn[u]] < L).sum()) for u in range(B)))   # forwarded: depth < L
-        eng.atspeed_set_timing(["gu"])
-        eng.atspeed_verify()
-        g = eng.atspeed_get_timing()["gu"]
+        eng.atspeed_decode_topk(prefix, items, scores, n, st)    # returns after its final synchronisation
+        per.append(time.perf_counter() - a)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    gu = None
+    if roofline:
+        ms, nl, gf = eng.atspeed_get_timing()["gu"]
         eng.atspeed_set_timing(False)
-        gu_ms += g[0]
-        gu_n += g[1]
-    m = w.target
-    gu_flops = 2.0 * rows * m.d_model * 2 * m.d_ffn
-    gu_avg = gu_ms / gu_n
-    gu_tflops = gu_flops / (gu_avg * 1e-3) / 1e12
-    log(f"t=0 verify: {rows} rows, gate/up {1e3 * gu_avg:.1f} us per launch, {gu_tflops:.0f} TFLOP/s")
-    out = {"metric": "top-K lists/sec/GPU (relaxed sampling verification, whole decode)", "value": round(value, 2),
-           "unit": "lists/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-           "ms_per_step": round(1e3 * elapsed / args.steps, 3), "higher_is_better": True, "scaling": "weak",
-           "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-           "config": {"workload": f"{w.name}: whole decode with {w.mode}, B={B}, P={w.prefix_len}, K={K}, N={w.N}, "
-                                  f"gamma={w.gamma}, tau={w.temperature}", "global_batch": B, "seq_len": w.prefix_len,
-                      "parallelism": "none (1 GPU)"},
-           "roofline": dict(bound="mfma", kernel=f"gemm_bf16 gate/up at the t=0 verify step ({rows} rows)",
-                            achieved=round(gu_tflops, 2), peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
-                            frac=round(gu_tflops / PEAK_BF16_TFLOPS, 4), traffic=None,
-                            per_launch_flops=gu_flops, avg_launch_ms=round(gu_avg, 4), launches_timed=int(gu_n)),
-           "cpu_baseline": None,
-           "kernels": {k: dict(ms_per_step=v[0] / steps_kt, launches_per_step=v[1] / steps_kt)
-                       for k, v in kt.items() if v[1]},
-           "accepted_levels_last_decode": acc[:st.n_steps].tolist(),
-           "decode_reuse": reuse}
-    print(json.dumps(out), flush=True)
-    eng.close()
+        gu = dict(ms=ms, launches=int(nl), gflop=gf)
+    out = (items.cpu().numpy(), scores.cpu().numpy(), n.cpu().numpy())
+    r = dict(lists_per_s=B * steps / elapsed, ms_per_decode=1e3 * elapsed / steps,
+             ms_per_decode_median=1e3 * float(np.median(per)), steps=int(st.n_steps),
+             ms_prefill=round(st.ms_prefill, 3), ms_draft=round(st.ms_draft, 3), ms_verify=round(st.ms_verify, 3),
+             lists_per_s_decode_only=B / ((st.ms_draft + st.ms_verify) / 1e3),
+             target_tree_rows=int(st.rows_target), accepted_levels=acc[:st.n_steps, :B].tolist())
+    return r, out, gu, elapsed
+
+
+def relaxed_line(w, tw, dw, cat, pre, dev, steps, warmup):
+    """Config-4 style decode: relaxed sampling verification (paper reading of
+    Algorithm 2) at the workload's K, N and temperature, with and without tree-KV
+    reuse (same lists)."""
+    import numpy as np
+    import torch
+    from paper_2410_05165_amd.binding import Engine
+    key = [int(x) for x in __import__("synth").philox_key(w)]
+    prefix = torch.from_numpy(pre).to(dev)
+    res = {}
+    outs = []
+    for reuse in (0, 1):
+        eng = Engine(w, tw, dw, cat, mode={"relaxed_exact": 1, "relaxed_paper": 2}[w.mode],
+                     seed=key[0] | (key[1] << 32), reuse_tree_kv=reuse)
+        r, out, gu, _ = timed_decodes(eng, w, prefix, steps, warmup, roofline=not reuse)
+        eng.close()
+        outs.append(out)
+        if gu:
+            r["gate_up_tflops"] = round(gu["gflop"] / gu["ms"], 1)
+        r["lists_mean"] = float(out[2].mean())
+        res["reuse" if reuse else "plain"] = r
+        log(f"relaxed decode ({w.name}, reuse {reuse}): {r['ms_per_decode']:.1f} ms "
+            f"({r['lists_per_s']:.0f} user lists/s), {r['steps']} steps, mean lists per user {r['lists_mean']:.1f}")
+    for x, y in zip(*outs):
+        assert (x == y).all(), "tree-KV reuse changed the relaxed lists"
+    res["workload"] = (f"{w.name}: whole decode with {w.mode} at tau={w.temperature}, B={w.batch}, "
+                       f"P={w.prefix_len}, K={w.K}, N={w.N}, gamma={w.gamma}")
+    return res
 
 
 def main():
@@ -422,8 +405,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="b7")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-e2e", action="store_true")
-    ap.add_argument("--no-probe", action="store_true", help="skip the decode-bound probe (profiling runs)")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="only the headline decode (profiling runs): no other profiles, verify step, probe or relaxed line")
+    ap.add_argument("--only", default="",
+                    help="comma list of extra sections to run: schedule,paper_as,all_accept,verify,probe,relaxed")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one plain device copy of this size (HBM counter calibration)")
     args = ap.parse_args()
@@ -435,8 +420,13 @@ def main():
     import numpy as np
     import torch
     from synth import get_workload, make_catalog, make_prefixes, make_weights
-    from paper_2410_05165_amd.binding import Engine, Stats
+    from paper_2410_05165_amd.binding import Engine
 
+    sections = {"schedule", "paper_as", "all_accept", "verify", "probe", "relaxed"}
+    if args.no_extras:
+        sections = set()
+    elif args.only:
+        sections = set(args.only.split(","))
     w = get_workload(args.workload)
     dev = torch.device("cuda:0")
     t0 = time.time()
@@ -446,152 +436,157 @@ def main():
     tw = make_weights(w, "target")
     log(f"target weights {sum(a.nbytes for a in tw.values()) / 2**30:.1f} GiB ({time.time() - t0:.1f}s)")
     dw = make_weights(w, "draft")
-    relaxed = w.mode != "strict"
     mode = {"strict": 0, "relaxed_exact": 1, "relaxed_paper": 2}[w.mode]
     key = [int(x) for x in __import__("synth").philox_key(w)]
-    eng = Engine(w, tw, dw, cat, mode=mode, seed=key[0] | (key[1] << 32))
+    seed = key[0] | (key[1] << 32)
+    eng = Engine(w, tw, dw, cat, mode=mode, seed=seed)
     log(f"engine ready, workspace {eng.ws.numel() / 2**30:.2f} GiB ({time.time() - t0:.1f}s)")
-    if relaxed:
-        return bench_decode(args, w, eng, pre, dev,
-                            make_engine=lambda **kw: Engine(w, tw, dw, cat, mode=mode, seed=key[0] | (key[1] << 32),
-                                                            **kw))
-    kids = catalog_children(cat)
     prefix = torch.from_numpy(pre).to(dev)
     B, K, L = w.batch, w.K, w.L
+    m = w.target
 
-    # ---- end-to-end decode (natural acceptance)
-    def e2e_natural(engine, label):
-        items = torch.zeros((B, K, L), dtype=torch.int32, device=dev)
-        scores = torch.zeros((B, K), dtype=torch.float32, device=dev)
-        n = torch.zeros(B, dtype=torch.int32, device=dev)
-        st = Stats()
-        for _ in range(3):                      # warm-up decodes
-            engine.atspeed_decode_topk(prefix, items, scores, n, None)
-        torch.cuda.synchronize()
-        reps, tt = 20, []                       # median of 20 timed decodes
-        for _ in range(reps):
-            torch.cuda.synchronize()
-            a = time.perf_counter()
-            engine.atspeed_decode_topk(prefix, items, scores, n, st)
-            torch.cuda.synchronize()
-            tt.append(time.perf_counter() - a)
-        r = dict(lists_per_s=B / float(np.median(tt)), ms_per_decode=1e3 * float(np.median(tt)),
-                 steps=int(st.n_steps), ms_prefill=st.ms_prefill, ms_draft=st.ms_draft, ms_verify=st.ms_verify,
-                 lists_per_s_decode_only=B / ((st.ms_draft + st.ms_verify) / 1e3),
-                 target_tree_rows=int(st.rows_target), profile=label)
-        log(f"e2e decode ({label}): {r['ms_per_decode']:.1f} ms ({r['lists_per_s']:.0f} lists/s), steps {st.n_steps}")
-        return r, (items.cpu().numpy(), scores.cpu().numpy(), n.cpu().numpy())
-
-    e2e = e2e_l1 = e2e_reuse = e2e_l1_reuse = None
-    if not args.no_e2e:
-        e2e, out0 = e2e_natural(eng, "natural")
-        # the level-1 start: level 1 from the prefill, speculation from t = 1
-        eng1 = Engine(w, tw, dw, cat, mode=mode, seed=key[0] | (key[1] << 32), sd_start_level=1)
-        e2e_l1, out1 = e2e_natural(eng1, "natural, level-1 start")
-        eng1.close()
-        for x, y in zip(out0, out1):
-            assert (x == y).all(), "level-1 start changed the lists"
-        # tree-KV reuse across the verify steps, from t = 0 and from level 1
-        for start in (0, 1):
-            eng2 = Engine(w, tw, dw, cat, mode=mode, seed=key[0] | (key[1] << 32), sd_start_level=start,
-                          reuse_tree_kv=1)
-            r2, out2 = e2e_natural(eng2, "natural, tree-KV reuse" + (", level-1 start" if start else ""))
-            eng2.close()
-            for x, y in zip(out0, out2):
-                assert (x == y).all(), "tree-KV reuse changed the lists"
-            if start:
-                e2e_l1_reuse = r2
-            else:
-                e2e_reuse = r2
-
-    # ---- replay-all-accept tree from the GPU's own target beam search
-    levels = gpu_target_beam_search(eng, w, prefix, upload_tree)
-    e2e_as = None
-    if not args.no_e2e:
-        e2e_as = decode_replay_as(eng, w, prefix, levels, kids, reps=20)
-        log(f"e2e decode, replay-paper-AS: {e2e_as['ms_per_decode']:.1f} ms ({e2e_as['lists_per_s']:.0f} lists/s), "
-            f"{e2e_as['steps']} steps, accepted levels per step {e2e_as['accepted_mean']:.2f} "
-            f"(first step {e2e_as['accepted_first_step_mean']:.2f})")
-    trees = replay_all_accept_tree(eng, kids, w, levels)
-    final = levels[-1]
-    eng.atspeed_prefill(prefix)
-    upload_tree(eng, trees, B)
-    n_fwd = sum(sum(1 for p in t if len(p) < L) for t in trees)
-    root_state = (np.zeros(B, np.int32), np.ones(B, np.int32), np.zeros((B, K, L), np.int32),
-                  np.zeros((B, K), np.float32))
-    acc = torch.zeros(B, dtype=torch.int32, device=dev)
-    tafter = torch.zeros(B, dtype=torch.int32, device=dev)
-
-    def step():
-        eng.atspeed_set_state(*root_state)
-        eng.atspeed_verify(acc, tafter)
-
-    step()
-    t_, nb_, paths_, sc_ = eng.atspeed_get_state(B)
-    assert (acc.cpu().numpy() == L).all() and (t_ == L).all(), "replay tree is not all-accept"
-    assert (paths_ == final[2]).all() and (sc_ == final[3]).all(), "verify differs from target beam search"
-    log(f"replay tree: {n_fwd} forwarded nodes ({n_fwd // B}/user), all levels accepted")
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    # Timed region: HIP events bracket only the gate/up launches (the roofline
-    # kernel), since every event adds stream time.
-    eng.atspeed_set_timing(["gu"])
-    torch.cuda.synchronize()
-    a = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - a
-    kt_gu = eng.atspeed_get_timing()["gu"]
-    eng.atspeed_set_timing(False)
-    ms_step = 1e3 * elapsed / args.steps
-    value = B * args.steps / elapsed
-    log(f"verify step {ms_step:.2f} ms -> {value:.0f} lists/s")
-    # Breakdown by kernel class: a separate pass with every launch bracketed.
-    steps_kt = max(3, args.steps // 2)
-    eng.atspeed_set_timing(True)
-    for _ in range(steps_kt):
-        step()
-    kt = eng.atspeed_get_timing()
-    eng.atspeed_set_timing(False)
-
-    # ---- roofline of the dominant kernel (gate/up GEMM) and of the other classes
-    M, d, f, H = n_fwd, w.target.d_model, w.target.d_ffn, w.target.n_heads
-    P, nl = w.prefix_len, w.target.n_layers
-    flops = {"qkv": 2 * M * d * 3 * d, "o": 2 * M * d * d, "gu": 2 * M * d * 2 * f, "down": 2 * M * f * d,
-             "lm_head": 2 * M * d * w.n_item_tokens}
-    classes = {}
-    for k, (ms, nlaunch) in kt.items():
-        if nlaunch == 0:
-            continue
-        avg = ms / nlaunch
-        ent = dict(ms_per_step=ms / steps_kt, launches_per_step=nlaunch / steps_kt, avg_launch_ms=avg)
-        if k in flops:
-            ent["tflops"] = flops[k] / (avg * 1e-3) / 1e12
-            ent["mfma_frac"] = ent["tflops"] / PEAK_BF16_TFLOPS
-        if k == "attention":
-            kv = B * P * 2 * d * 2                      # prefix K and V of every user, read once
-            tree = M * d * 2 * 4                        # q, tree k/v and output rows (bf16)
-            ent["gbs"] = (kv + tree) / (avg * 1e-3) / 1e9
-            ent["hbm_frac"] = ent["gbs"] / PEAK_HBM_GBS
-        classes[k] = ent
-    gemm_ms = sum(kt[k][0] for k in flops) / steps_kt
-    gemm_flops = nl * sum(flops[k] for k in ("qkv", "o", "gu", "down")) + flops["lm_head"]
-    gu_avg = kt_gu[0] / kt_gu[1]                        # ms per gate/up launch in the timed region
-    gu_tflops = flops["gu"] / (gu_avg * 1e-3) / 1e12
-    roofline = dict(bound="mfma", kernel="gemm_bf16 gate/up (SiLU*up epilogue)",
+    # ---- headline: whole decode (prefill + draft/verify steps until every list is complete)
+    head, out0, gu, elapsed = timed_decodes(eng, w, prefix, args.steps, args.warmup)
+    value = head["lists_per_s"]
+    log(f"decode ({w.mode}, natural drafts): {head['ms_per_decode']:.1f} ms per decode (median "
+        f"{head['ms_per_decode_median']:.1f}) -> {value:.1f} lists/s; {head['steps']} steps")
+    gu_avg_ms = gu["ms"] / gu["launches"]
+    gu_flop = gu["gflop"] * 1e9 / gu["launches"]
+    gu_tflops = gu["gflop"] / gu["ms"]
+    log(f"roofline: target gate/up GEMM, {gu['launches']} launches in the timed region, {1e3 * gu_avg_ms:.1f} us and "
+        f"{gu_flop / 1e9:.1f} GFLOP per launch on average -> {gu_tflops:.0f} TFLOP/s")
+    roofline = dict(bound="mfma", kernel="target gate/up GEMM (SiLU*up epilogue), every launch of the timed decodes "
+                                         "(prefill and each verify step)",
                     achieved=round(gu_tflops, 2), peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
-                    frac=round(gu_tflops / PEAK_BF16_TFLOPS, 4), traffic=gemm_traffic("gate/up GEMM", w.name),
-                    per_launch_flops=flops["gu"], avg_launch_ms=round(gu_avg, 4),
-                    launches_timed=int(kt_gu[1]))
+                    frac=round(gu_tflops / PEAK_BF16_TFLOPS, 4),
+                    traffic=gemm_traffic("gate/up GEMM, natural decode", w.name),
+                    per_launch_flops=round(gu_flop), avg_launch_ms=round(gu_avg_ms, 5),
+                    launches_timed=gu["launches"])
 
-    probe = None if args.no_probe else decode_bound_probe(eng, w, prefix, levels, max(3, args.steps // 2))
+    extras = {}
+    levels = kids = None
+    if mode == 0 and sections & {"paper_as", "all_accept", "verify", "probe"}:
+        kids = catalog_children(cat)
+        levels = gpu_target_beam_search(eng, w, prefix, upload_tree)
+        assert (levels[-1][2] == out0[0]).all(), "speculative decode differs from the GPU's target beam search"
+
+    if mode == 0 and "schedule" in sections:
+        for start, reuse, name in ((1, 0, "decode_level1_start"), (0, 1, "decode_reuse"),
+                                   (1, 1, "decode_level1_start_reuse")):
+            e2 = Engine(w, tw, dw, cat, mode=mode, seed=seed, sd_start_level=start, reuse_tree_kv=reuse)
+            r, out, _, _ = timed_decodes(e2, w, prefix, args.steps, args.warmup, roofline=False)
+            e2.close()
+            for x, y in zip(out0, out):
+                assert (x == y).all(), f"{name} changed the lists"
+            extras[name] = r
+            log(f"{name}: {r['ms_per_decode']:.1f} ms ({r['lists_per_s']:.0f} lists/s), target rows "
+                f"{r['target_tree_rows']}")
+
+    if mode == 0 and "paper_as" in sections:
+        r = decode_replay_as(eng, w, prefix, levels, kids, reps=args.steps)
+        extras["decode_paper_as"] = r
+        log(f"decode, replay-paper-AS: {r['ms_per_decode']:.1f} ms ({r['lists_per_s']:.0f} lists/s), "
+            f"{r['steps']} steps, accepted levels per step {r['accepted_mean']:.2f}")
+
+    trees = replay_all_accept_tree(eng, kids, w, levels) if levels is not None else None
+    if mode == 0 and "all_accept" in sections:
+        # whole decode under replay-all-accept: prefill, the device draft, then its
+        # tree replaced by the replay tree -- one verify completes every list
+        n_, tok_, par_, dep_ = (torch.from_numpy(a).to(dev) for a in tree_arrays(eng, trees, B))
+        tn, tt, tp, td, tq = eng.tree_tensors(B)
+        acc = torch.zeros(B, dtype=torch.int32, device=dev)
+
+        def decode_all():
+            eng.atspeed_prefill(prefix)
+            eng.atspeed_draft()
+            tn.copy_(n_); tt.copy_(tok_); tp.copy_(par_); td.copy_(dep_); tq.zero_()
+            eng.atspeed_verify(acc)
+        decode_all()
+        assert (acc.cpu().numpy() == L).all() and (eng.atspeed_get_state(B)[2] == levels[-1][2]).all()
+        for _ in range(args.warmup):
+            decode_all()
+        torch.cuda.synchronize()
+        a = time.perf_counter()
+        for _ in range(args.steps):
+            decode_all()
+        torch.cuda.synchronize()
+        ms = 1e3 * (time.perf_counter() - a) / args.steps
+        extras["decode_all_accept"] = dict(lists_per_s=B / (ms * 1e-3), ms_per_decode=ms, steps=1,
+                                           profile="replay-all-accept (the drafted tree holds the target's TopK at "
+                                                   "every level; one verify completes the lists)")
+        log(f"decode, replay-all-accept: {ms:.1f} ms ({B / (ms * 1e-3):.0f} lists/s)")
+
+    if mode == 0 and "verify" in sections:
+        # the t = 0 verify step alone over the replay-all-accept tree (fixed shape)
+        eng.atspeed_prefill(prefix)
+        upload_tree(eng, trees, B)
+        M = sum(sum(1 for p in t if len(p) < L) for t in trees)
+        root_state = (np.zeros(B, np.int32), np.ones(B, np.int32), np.zeros((B, K, L), np.int32),
+                      np.zeros((B, K), np.float32))
+        acc = torch.zeros(B, dtype=torch.int32, device=dev)
+
+        def vstep():
+            eng.atspeed_set_state(*root_state)
+            eng.atspeed_verify(acc)
+        vstep()
+        assert (acc.cpu().numpy() == L).all() and (eng.atspeed_get_state(B)[2] == levels[-1][2]).all()
+        for _ in range(args.warmup):
+            vstep()
+        eng.atspeed_set_timing(["gu"])
+        torch.cuda.synchronize()
+        a = time.perf_counter()
+        for _ in range(args.steps):
+            vstep()
+        torch.cuda.synchronize()
+        ms_step = 1e3 * (time.perf_counter() - a) / args.steps
+        vgu = eng.atspeed_get_timing()["gu"]
+        steps_kt = max(3, args.steps // 2)
+        eng.atspeed_set_timing(True)                 # breakdown: every launch bracketed (a separate pass)
+        for _ in range(steps_kt):
+            vstep()
+        kt = eng.atspeed_get_timing()
+        eng.atspeed_set_timing(False)
+        d, f, P, nl = m.d_model, m.d_ffn, w.prefix_len, m.n_layers
+        classes = {}
+        for k_, (ms_, nlaunch, gf) in kt.items():
+            if nlaunch == 0:
+                continue
+            avg = ms_ / nlaunch
+            ent = dict(ms_per_step=ms_ / steps_kt, launches_per_step=nlaunch / steps_kt, avg_launch_ms=avg)
+            if gf:
+                ent["tflops"] = gf / ms_
+                ent["mfma_frac"] = ent["tflops"] / PEAK_BF16_TFLOPS
+            if k_ == "attention":
+                kv = B * P * 2 * d * 2                  # prefix K and V of every user, read once
+                tree = M * d * 2 * 4                    # q, tree k/v and output rows (bf16)
+                ent["gbs"] = (kv + tree) / (avg * 1e-3) / 1e9
+                ent["hbm_frac"] = ent["gbs"] / PEAK_HBM_GBS
+            classes[k_] = ent
+        gemm_ms = sum(kt[k_][0] for k_ in ("qkv", "o", "gu", "down", "lm_head")) / steps_kt
+        gemm_gf = sum(kt[k_][2] for k_ in ("qkv", "o", "gu", "down", "lm_head")) / steps_kt
+        extras["verify_step"] = dict(
+            what=f"one atspeed_verify at t=0 over the replay-all-accept tree ({M} target rows), "
+                 f"completing all {B} lists", ms_per_step=round(ms_step, 3), lists_per_s=B / (ms_step * 1e-3),
+            gate_up=dict(tflops=round(vgu[2] / vgu[0], 1), mfma_frac=round(vgu[2] / vgu[0] / PEAK_BF16_TFLOPS, 4),
+                         avg_launch_ms=round(vgu[0] / vgu[1], 5), traffic=gemm_traffic("gate/up GEMM", w.name)),
+            gemm=dict(tflops=gemm_gf / gemm_ms, mfma_frac=gemm_gf / gemm_ms / PEAK_BF16_TFLOPS, ms_per_step=gemm_ms),
+            kernels=classes)
+        log(f"verify step (t=0, all-accept tree, {M} rows): {ms_step:.2f} ms; GEMMs "
+            f"{gemm_gf / gemm_ms:.0f} TFLOP/s; gate/up {vgu[2] / vgu[0]:.0f} TFLOP/s")
+
+    if mode == 0 and "probe" in sections:
+        extras["decode_bound"] = decode_bound_probe(eng, w, prefix, levels, max(3, args.steps // 2))
+
+    eng.close()
+    if "relaxed" in sections and w.name == "b7":
+        wr = get_workload("b7_relaxed")
+        extras["relaxed_decode"] = relaxed_line(wr, tw, dw, cat, pre, dev, args.steps, args.warmup)
+    elif mode != 0 and "relaxed" in sections:
+        extras["relaxed_decode"] = relaxed_line(w, tw, dw, cat, pre, dev, args.steps, args.warmup)
 
     cpu = None
-    if not args.no_cpu_baseline:
-        cpu, _ = cpu_baseline(w, tw, pre, cat, trees[0])
+    if not args.no_cpu_baseline and mode == 0:
+        cpu = cpu_baseline(w, tw, dw, pre, cat, out0[0][0, :out0[2][0]])
         log(f"cpu baseline: {cpu['value']:.4f} lists/s ({cpu['sample']})")
 
     if args.copy_calibration_mib:
@@ -602,30 +597,24 @@ def main():
         torch.cuda.synchronize()
         log(f"copy calibration: {args.copy_calibration_mib} MiB read + write")
 
+    prof = {0: "natural drafts (random-init draft: the library's own draft and verify, no forced trees)"}
     out = {
         "metric": "top-K lists/sec/GPU at 7B shape K=10; verify-step MFMA util + HBM GB/s",
         "value": round(value, 2), "unit": "lists/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 3), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "bf16", "data": "synthetic (seeded catalog, Zipf histories, random-init N(0,0.02) weights)",
-        "config": {"workload": f"{w.name}: verify step at t=0 over the replay-all-accept tree; target 32L/4096/32h/"
-                               f"FFN 11008, V 33024 (1024 item tokens), B={B} users, P={P}, K={K}, N={w.N}, "
-                               f"gamma={w.gamma}, strict; {M} tree rows; prefill and drafting excluded",
-                   "global_batch": B, "seq_len": P, "parallelism": "none (1 GPU)"},
+        "ms_per_step": round(1e3 * elapsed / args.steps, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded catalog, Zipf histories, random-init N(0,0.02) weights)",
+        "config": {"workload": f"{w.name}: whole atspeed_decode_topk including prefill, {w.mode} verification, "
+                               f"acceptance profile {prof.get(mode, 'sampled drafts')}; target {m.n_layers}L/"
+                               f"{m.d_model}/{m.n_heads}h/FFN {m.d_ffn}, V {m.vocab} ({w.n_item_tokens} item tokens), "
+                               f"4L/768 draft, {w.n_items} items, B={B} users, P={w.prefix_len}, K={K}, N={w.N}, "
+                               f"gamma={w.gamma}",
+                   "global_batch": B, "seq_len": w.prefix_len, "parallelism": "none (1 GPU)"},
         "roofline": roofline,
         "cpu_baseline": cpu,
-        "kernels": classes,            # separate pass, every launch bracketed by events
-        "verify_gemm": dict(tflops=gemm_flops / (gemm_ms * 1e-3) / 1e12,
-                            mfma_frac=gemm_flops / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
-                            ms_per_step=gemm_ms),
-        "e2e_decode": e2e,
-        "e2e_decode_level1_start": e2e_l1,
-        "e2e_decode_paper_as": e2e_as,
-        "e2e_decode_reuse": e2e_reuse,
-        "e2e_decode_level1_start_reuse": e2e_l1_reuse,
-        "decode_bound": probe,
+        "decode": head,
     }
+    out.update(extras)
     print(json.dumps(out), flush=True)
-    eng.close()
 
 
 if __name__ == "__main__":

@@ -158,10 +158,14 @@ enum {
 };
 
 /* Stream time per kernel class, from HIP events recorded between consecutive
- * launches on the context's stream while timing is enabled. */
+ * launches on the context's stream while timing is enabled.  gflop: algorithmic
+ * GFLOP of the bracketed GEMM launches of the target model (2 x rows x n x k with
+ * the rows the launch forwards; the draft's launches, sized by a bound of their
+ * rows, and the non-GEMM classes count 0). */
 typedef struct {
   double ms[ATSPEED_K_COUNT];
   int64_t launches[ATSPEED_K_COUNT];
+  double gflop[ATSPEED_K_COUNT];
 } atspeed_kernel_times;
 
 typedef struct atspeed_ctx atspeed_ctx;
@@ -267,7 +271,8 @@ ATSPEED_API atspeed_status atspeed_set_state(atspeed_ctx* ctx, int32_t B, const 
                                  const int32_t* paths, const float* scores);
 
 /* Kernel timing (instrumentation for measurement).  enable is a bit mask of the
- * kernel classes to time (bit ATSPEED_K_x; ATSPEED_TIME_ALL for every class):
+ * kernel classes to time (bit ATSPEED_K_x; ATSPEED_TIME_ALL for every class),
+ * optionally or-ed with ATSPEED_TIME_TARGET_ONLY:
  * a HIP event is recorded on the context's stream before each launch of a
  * selected class and before the launch that follows it, and the totals are
  * cleared; 0 stops.  Each event adds a little stream time, so timing only the
@@ -275,6 +280,7 @@ ATSPEED_API atspeed_status atspeed_set_state(atspeed_ctx* ctx, int32_t B, const 
  * synchronises the stream, folds the recorded intervals into out (totals since
  * enabling). */
 #define ATSPEED_TIME_ALL ((1 << ATSPEED_K_COUNT) - 1)
+#define ATSPEED_TIME_TARGET_ONLY (1 << 16)  /* with a class mask: the draft model's launches are not bracketed */
 ATSPEED_API atspeed_status atspeed_set_timing(atspeed_ctx* ctx, int32_t enable);
 ATSPEED_API atspeed_status atspeed_get_timing(atspeed_ctx* ctx, atspeed_kernel_times* out);
 

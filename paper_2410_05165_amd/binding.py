@@ -60,7 +60,10 @@ class Stats(C.Structure):
 
 
 class KernelTimes(C.Structure):
-    _fields_ = [("ms", C.c_double * 8), ("launches", C.c_int64 * 8)]
+    _fields_ = [("ms", C.c_double * 8), ("launches", C.c_int64 * 8), ("gflop", C.c_double * 8)]
+
+
+TIME_TARGET_ONLY = 1 << 16
 
 
 class AtspeedError(RuntimeError):
@@ -246,21 +249,25 @@ class Engine:
         self._check(self.lib.atspeed_set_state(self.ctx, len(t), _np_ptr(t, C.c_int32), _np_ptr(nb, C.c_int32),
                                                _np_ptr(paths, C.c_int32), _np_ptr(scores, C.c_float)))
 
-    def atspeed_set_timing(self, enable=True):
+    def atspeed_set_timing(self, enable=True, target_only=False):
         """enable: True (every kernel class), False (off), or an iterable of
-        class names from KERNEL_CLASSES (only those launches are bracketed)."""
+        class names from KERNEL_CLASSES (only those launches are bracketed);
+        target_only: leave the draft model's launches out."""
         if enable is True:
             mask = (1 << len(KERNEL_CLASSES)) - 1
         elif not enable:
             mask = 0
         else:
             mask = sum(1 << KERNEL_CLASSES.index(k) for k in set(enable))
+        if mask and target_only:
+            mask |= TIME_TARGET_ONLY
         self._check(self.lib.atspeed_set_timing(self.ctx, mask))
 
     def atspeed_get_timing(self) -> Dict[str, tuple]:
+        """class -> (ms, launches, algorithmic GFLOP of the target's GEMM launches)."""
         kt = KernelTimes()
         self._check(self.lib.atspeed_get_timing(self.ctx, C.byref(kt)))
-        return {k: (kt.ms[i], kt.launches[i]) for i, k in enumerate(KERNEL_CLASSES)}
+        return {k: (kt.ms[i], kt.launches[i], kt.gflop[i]) for i, k in enumerate(KERNEL_CLASSES)}
 
     # -- tree upload / download (device SoA of the context)
     def tree_tensors(self, B: int):

@@ -138,11 +138,15 @@ struct atspeed_ctx {
   int64_t rows_fwd = 0;            // target tree rows forwarded (decode statistics)
   // timing instrumentation
   uint32_t timing_mask = 0;   // kernel classes whose launches are bracketed by events
+  bool timing_target_only = false;  // skip the draft model's launches
+  const ModelRt* fwd_model = nullptr;  // model of the forward being enqueued (null: none)
   std::vector<hipEvent_t> ev_pool;
   std::vector<int> ev_kind;   // kind of the interval that starts at event i (-1: end marker)
+  std::vector<double> ev_flops;  // algorithmic flops of that interval's launch
   size_t ev_used = 0;
   double t_ms[ATSPEED_K_COUNT] = {};
   int64_t t_n[ATSPEED_K_COUNT] = {};
+  double t_flop[ATSPEED_K_COUNT] = {};
   ~atspeed_ctx() {
     for (hipEvent_t e : ev_pool) hipEventDestroy(e);
   }
@@ -154,11 +158,12 @@ size_t esize(const atspeed_ctx& c) { return c.bf16 ? 2 : 4; }
 
 // Marks the start of a launch of class `kind` (or, with kind -1, the end of the
 // previous one) when timing is on.
-hipError_t mark(atspeed_ctx& c, int kind) {
+hipError_t mark(atspeed_ctx& c, int kind, double flops = 0.0) {
   if (!c.timing_mask) return hipSuccess;
   // An event opens a span before a launch of a selected class; the next mark
   // closes it (and opens a new span if its class is selected too).
-  const bool want = kind >= 0 && ((c.timing_mask >> kind) & 1u);
+  const bool draft = c.fwd_model != nullptr && c.fwd_model == &c.dft;
+  const bool want = kind >= 0 && ((c.timing_mask >> kind) & 1u) && !(draft && c.timing_target_only);
   const bool open = c.ev_used > 0 && c.ev_kind[c.ev_used - 1] >= 0;
   if (!want && !open) return hipSuccess;
   if (c.ev_used == c.ev_pool.size()) {
@@ -167,8 +172,10 @@ hipError_t mark(atspeed_ctx& c, int kind) {
     if (err != hipSuccess) return err;
     c.ev_pool.push_back(e);
     c.ev_kind.push_back(-1);
+    c.ev_flops.push_back(0.0);
   }
   c.ev_kind[c.ev_used] = want ? kind : -1;
+  c.ev_flops[c.ev_used] = want && !draft ? flops : 0.0;
   return hipEventRecord(c.ev_pool[c.ev_used++], c.st);
 }
 
@@ -184,12 +191,14 @@ hipError_t fold_timing(atspeed_ctx& c) {
     if (err != hipSuccess) return err;
     c.t_ms[k] += ms;
     c.t_n[k] += 1;
+    c.t_flop[k] += c.ev_flops[i];
   }
   c.ev_used = 0;
   return hipSuccess;
 }
 
 #define MARK(kind) HIP_TRY(mark(c, kind))
+#define MARK_F(kind, flops) HIP_TRY(mark(c, kind, flops))
 
 atspeed_status check_dims(const atspeed_model_dims& m, const atspeed_config& c, const char* who) {
   std::string w(who);
@@ -459,6 +468,14 @@ atspeed_status forward(atspeed_ctx& c, ModelRt& r, bool prefill, int Mmax, int T
   const int B = c.B, P = c.P;
   const size_t es = esize(c);
   hipStream_t st = c.st;
+  // the marks below know which model they bracket (target launches forward
+  // exactly Mmax rows, the draft's are sized by a bound)
+  struct Current {
+    atspeed_ctx& c;
+    Current(atspeed_ctx& cc, const ModelRt& r) : c(cc) { c.fwd_model = &r; }
+    ~Current() { c.fwd_model = nullptr; }
+  } current(c, r);
+  const double M = Mmax;
   MARK(ATSPEED_K_ROW);
   HIP_TRY(embed(c.bf16, r.emb, c.rows, Mmax, d, c.x, st));
   // bf16: the o and down projections split k at its midpoint (whole even
@@ -487,7 +504,7 @@ atspeed_status forward(atspeed_ctx& c, ModelRt& r, bool prefill, int Mmax, int T
     g.kv_mode = prefill ? 0 : 1;
     g.kdst = prefill ? (void*)pk : (void*)tk;
     g.vdst = prefill ? (void*)pv : (void*)tv;
-    MARK(ATSPEED_K_QKV);
+    MARK_F(ATSPEED_K_QKV, 2.0 * M * 3.0 * d * d);
     HIP_TRY(gemm(g, st));
     if (prefill && shared > 0 && B > 1) {  // users 1..B-1 take user 0's K/V of the shared positions
       launch_broadcast_prefix_kv(pk, pv, B, H, (size_t)c.cfg.max_prefix * dh * es, (size_t)shared * dh * es, st);
@@ -502,16 +519,16 @@ atspeed_status forward(atspeed_ctx& c, ModelRt& r, bool prefill, int Mmax, int T
     HIP_TRY(attention(at, st));
     g.kind = GEMM_RESID; g.A = c.ao; g.lda = d; g.N = d; g.K = d; g.w0 = w[4]; g.out = c.x; g.ldo = d;
     g.part = part_o;
-    MARK(ATSPEED_K_O);
+    MARK_F(ATSPEED_K_O, 2.0 * M * d * d);
     HIP_TRY(gemm(g, st));
     MARK(ATSPEED_K_ROW);
     HIP_TRY(rmsnorm(c.bf16, c.x, part_o, c.rows.M, Mmax, d, (const float*)w[5], c.xn, nullptr, st));
     g.kind = GEMM_GU; g.A = c.xn; g.lda = d; g.N = 2 * f; g.K = d; g.w0 = w[6]; g.w1 = w[7]; g.split = f; g.hout = c.h;
-    MARK(ATSPEED_K_GU);
+    MARK_F(ATSPEED_K_GU, 2.0 * M * 2.0 * f * d);
     HIP_TRY(gemm(g, st));
     g.kind = GEMM_RESID; g.A = c.h; g.lda = f; g.N = d; g.K = f; g.w0 = w[8]; g.out = c.x; g.ldo = d;
     g.part = part_down;
-    MARK(ATSPEED_K_DOWN);
+    MARK_F(ATSPEED_K_DOWN, 2.0 * M * f * d);
     HIP_TRY(gemm(g, st));
   }
   // final norm + item rows of the output head + log-softmax
@@ -522,7 +539,7 @@ atspeed_status forward(atspeed_ctx& c, ModelRt& r, bool prefill, int Mmax, int T
   GemmCall g{};
   g.kind = GEMM_STORE; g.bf16 = c.bf16; g.A = c.xn; g.lda = d; g.Mmax = Mmf; g.Mdev = Mfin;
   g.N = c.nitem; g.K = d; g.w0 = r.lm_head; g.out = c.logits; g.ldo = c.nitem; g.scratch = c.scratch;
-  MARK(ATSPEED_K_LMHEAD);
+  MARK_F(ATSPEED_K_LMHEAD, 2.0 * Mmf * c.nitem * d);
   HIP_TRY(gemm(g, st));
   MARK(ATSPEED_K_ROW);
   if (prefill) HIP_TRY(log_softmax_rows(c.logits, c.Mb, B, c.nitem, nullptr, r.root, dbg, st));
@@ -948,14 +965,19 @@ atspeed_status atspeed_set_timing(atspeed_ctx* c, int32_t enable) {
   if (!c) return fail(ATSPEED_E_INVALID, "ctx is null");
   HIP_TRY(fold_timing(*c));
   c->timing_mask = (uint32_t)enable & ATSPEED_TIME_ALL;
-  for (int k = 0; k < ATSPEED_K_COUNT; ++k) { c->t_ms[k] = 0; c->t_n[k] = 0; }
+  c->timing_target_only = (enable & ATSPEED_TIME_TARGET_ONLY) != 0;
+  for (int k = 0; k < ATSPEED_K_COUNT; ++k) { c->t_ms[k] = 0; c->t_n[k] = 0; c->t_flop[k] = 0; }
   return ATSPEED_OK;
 }
 
 atspeed_status atspeed_get_timing(atspeed_ctx* c, atspeed_kernel_times* out) {
   if (!c || !out) return fail(ATSPEED_E_INVALID, "null argument");
   HIP_TRY(fold_timing(*c));
-  for (int k = 0; k < ATSPEED_K_COUNT; ++k) { out->ms[k] = c->t_ms[k]; out->launches[k] = c->t_n[k]; }
+  for (int k = 0; k < ATSPEED_K_COUNT; ++k) {
+    out->ms[k] = c->t_ms[k];
+    out->launches[k] = c->t_n[k];
+    out->gflop[k] = c->t_flop[k] * 1e-9;
+  }
   return ATSPEED_OK;
 }
 
