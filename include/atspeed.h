@@ -237,6 +237,24 @@ ATSPEED_API atspeed_status atspeed_tree_logits(atspeed_ctx* ctx, float* logits_d
 ATSPEED_API atspeed_status atspeed_accept(atspeed_ctx* ctx, const float* logits_dev, const float* root_logits_dev,
                               int32_t* accepted_dev, int32_t* t_after_dev);
 
+/* Allocation-free accept, for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).
+ * Same arguments, checks and results as atspeed_accept, but the buffers that call
+ * takes from the workspace for its own use -- the log-prob rows of the caller's
+ * logits, the selection keys, the relaxed modes' candidate buffers and the
+ * tree-validation word -- live in a static device array of 64 MiB that the
+ * library holds on each GPU until the process ends (its address is taken at
+ * atspeed_create, on the context's device).  Needs 4*(B*max_nodes + B)*L*codebook
+ * + 8*B*N*codebook bytes (+ 20*B*N*codebook in a relaxed mode, plus alignment);
+ * a prefilled batch that needs more returns ATSPEED_E_WORKSPACE before any launch.
+ * Every call on a GPU shares that GPU's array and finds the last call's contents
+ * there (each call writes what it reads): calls that overlap on one GPU, from
+ * any context or stream, race.  No allocating call is made.  Synchronises the
+ * stream. */
+ATSPEED_API atspeed_status atspeed_accept_noalloc(atspeed_ctx* ctx, const float* logits_dev,
+                                                  const float* root_logits_dev, int32_t* accepted_dev,
+                                                  int32_t* t_after_dev);
+
 /* Whole decode: prefill, then draft/verify steps until every user holds L-token
  * items (Algorithm 1 / 2 repeated; the schedule options sd_start_level and
  * reuse_tree_kv of the config change the work, not the lists).  items_dev

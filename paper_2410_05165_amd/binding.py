@@ -21,7 +21,7 @@ STATUS = {0: "OK", 1: "E_INVALID", 2: "E_SHAPE", 3: "E_WORKSPACE", 4: "E_DEVICE"
 LAYER_ORDER = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down")
 SYMBOLS = ("atspeed_workspace_bytes", "atspeed_create", "atspeed_destroy", "atspeed_last_error",
            "atspeed_prefill", "atspeed_draft", "atspeed_get_tree", "atspeed_verify", "atspeed_tree_logits",
-           "atspeed_accept", "atspeed_decode_topk", "atspeed_logprobs", "atspeed_get_state", "atspeed_set_state",
+           "atspeed_accept", "atspeed_accept_noalloc", "atspeed_decode_topk", "atspeed_logprobs", "atspeed_get_state", "atspeed_set_state",
            "atspeed_set_timing", "atspeed_get_timing")
 KERNEL_CLASSES = ("qkv", "o", "gu", "down", "lm_head", "attention", "row", "select")
 
@@ -89,6 +89,7 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
     lib.atspeed_verify.argtypes = [vp, pi32, pi32, pf]
     lib.atspeed_tree_logits.argtypes = [vp, pf]
     lib.atspeed_accept.argtypes = [vp, pf, pf, pi32, pi32]
+    lib.atspeed_accept_noalloc.argtypes = [vp, pf, pf, pi32, pi32]
     lib.atspeed_decode_topk.argtypes = [vp, i32, i32, pi32, pi32, pf, pi32, C.POINTER(Stats)]
     lib.atspeed_logprobs.argtypes = [vp, i32, pf, pf]
     lib.atspeed_get_state.argtypes = [vp, i32, C.POINTER(C.c_int32), C.POINTER(C.c_int32), C.POINTER(C.c_int32),
@@ -222,6 +223,10 @@ class Engine:
 
     def atspeed_accept(self, logits, root_logits, accepted=None, t_after=None):
         self._check(self.lib.atspeed_accept(self.ctx, _ptr(logits), _ptr(root_logits), _ptr(accepted), _ptr(t_after)))
+
+    def atspeed_accept_noalloc(self, logits, root_logits, accepted=None, t_after=None):
+        self._check(self.lib.atspeed_accept_noalloc(self.ctx, _ptr(logits), _ptr(root_logits), _ptr(accepted),
+                                                    _ptr(t_after)))
 
     def atspeed_decode_topk(self, prefix, items, scores, n_items, stats: Optional[Stats] = None):
         B, P = prefix.shape

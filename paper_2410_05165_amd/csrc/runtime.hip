@@ -3,6 +3,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -129,6 +130,9 @@ struct atspeed_ctx {
   int kv_cur = 0;               // set holding the last verify's K/V and log-probs
   bool carry_ok = false;        // the last verify was the decode loop's own, since the prefill
   float* lp_set[2] = {nullptr, nullptr};
+  // device address of the static scratch of atspeed_accept_noalloc on the
+  // context's device (taken at create)
+  unsigned char* static_scratch = nullptr;
   uint32_t* prev_tpath = nullptr;  // [B*Tmax] path keys of the last verify's tree
   int* prev_depth = nullptr;       // [B*Tmax]
   int* prev_n = nullptr;           // [B] its forwarded (or carried) nodes: slots [0, prev_n)
@@ -617,6 +621,34 @@ atspeed_status tree_forward(atspeed_ctx& c, float* dbg_logits, bool carry = fals
 
 }  // namespace
 
+// ---------------------------------------------------------------- allocation-free accept
+// Scratch of atspeed_accept_noalloc: one copy per GPU, held until the process
+// ends.  In host code the name only stands for the symbol; its device address is
+// taken once per device with hipGetSymbolAddress and used everywhere instead.
+constexpr size_t kStaticScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+namespace {
+std::mutex g_scratch_mu;
+constexpr int kMaxDevices = 64;
+unsigned char* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's address of the static scratch (taken on first use).
+atspeed_status static_scratch_address(unsigned char** out) {
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(ATSPEED_E_DEVICE, "device index out of range for the static scratch");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    g_scratch_ptr[dev] = static_cast<unsigned char*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return ATSPEED_OK;
+}
+}  // namespace
+
 // ====================================================================== ABI
 
 extern "C" {
@@ -673,12 +705,15 @@ atspeed_status atspeed_create(const atspeed_config* cfg, const atspeed_weights* 
   if (e != hipSuccess) return bail(fail(ATSPEED_E_DEVICE, std::string("create: ") + hipGetErrorString(e)));
   s = upload_rope(*c, c->tgt);
   if (s == ATSPEED_OK && c->dft.present) s = upload_rope(*c, c->dft);
+  if (s == ATSPEED_OK) s = static_scratch_address(&c->static_scratch);
   if (s != ATSPEED_OK) return bail(s);
   *out = c;
   return ATSPEED_OK;
 }
 
 void atspeed_destroy(atspeed_ctx* ctx) { delete ctx; }
+
+
 
 atspeed_status atspeed_prefill(atspeed_ctx* c, int32_t B, int32_t P, const int32_t* prefix, float* root_logits) {
   if (!c) return fail(ATSPEED_E_INVALID, "ctx is null");
@@ -827,6 +862,60 @@ atspeed_status atspeed_accept(atspeed_ctx* c, const float* logits, const float* 
   HIP_TRY(log_softmax_rows(logits, c->Mall, c->B * c->Tmax, c->nitem, nullptr, c->tgt.lp, nullptr, c->st));
   HIP_TRY(log_softmax_rows(root_logits, c->Mb, c->B, c->nitem, nullptr, c->tgt.root, nullptr, c->st));
   ST_TRY(accept_on(c, c->tgt.lp, c->tgt.root, accepted, t_after));
+  HIP_TRY(hipStreamSynchronize(c->st));
+  return ATSPEED_OK;
+}
+
+atspeed_status atspeed_accept_noalloc(atspeed_ctx* c, const float* logits, const float* root_logits,
+                                      int32_t* accepted, int32_t* t_after) {
+  if (!c || !logits || !root_logits) return fail(ATSPEED_E_INVALID, "null argument");
+  if (!c->prefilled) return fail(ATSPEED_E_STATE, "accept before prefill");
+  const atspeed_config& cf = c->cfg;
+  const bool relaxed = cf.mode != ATSPEED_STRICT;
+  if (relaxed && !c->drafted) return fail(ATSPEED_E_STATE, "relaxed verification needs the context's own draft of this step");
+  if (!c->static_scratch) return fail(ATSPEED_E_DEVICE, "static scratch address unknown");
+  // carve the static scratch: error word, log-prob rows by slot, root rows,
+  // selection keys, relaxed candidate buffers
+  const size_t B = c->B, rows = B * c->Tmax, nc = B * c->max_cand;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { const size_t o = off; off = (off + bytes + 255) & ~size_t(255); return o; };
+  const size_t o_err = take(sizeof(int)), o_lp = take(rows * c->nitem * 4), o_root = take(B * c->nitem * 4);
+  const size_t o_keys = take(nc * 8);
+  size_t o_cand[5] = {0, 0, 0, 0, 0};
+  if (relaxed)
+    for (size_t& o : o_cand) o = take(nc * 4);
+  if (off > kStaticScratchBytes)
+    return fail(ATSPEED_E_WORKSPACE, "accept_noalloc needs " + std::to_string(off) + " bytes of scratch for this batch; " +
+                                         "the static scratch holds " + std::to_string(kStaticScratchBytes));
+  unsigned char* base = c->static_scratch;
+  int* err = reinterpret_cast<int*>(base + o_err);
+  float* lp = reinterpret_cast<float*>(base + o_lp);
+  float* root = reinterpret_cast<float*>(base + o_root);
+  unsigned long long* keys = reinterpret_cast<unsigned long long*>(base + o_keys);
+  HIP_TRY(hipMemsetAsync(err, 0, sizeof(int), c->st));
+  launch_tree_index(c->tree, c->trie, c->state, c->B, cf.target.item_base, cf.codebook, cf.L, err, c->st);
+  HIP_TRY(hipGetLastError());
+  int bad = 0;
+  HIP_TRY(hipMemcpyAsync(&bad, err, sizeof(int), hipMemcpyDeviceToHost, c->st));
+  HIP_TRY(hipStreamSynchronize(c->st));
+  if (bad) return fail(ATSPEED_E_INVALID, "malformed tree (code " + std::to_string(bad) + ")");
+  HIP_TRY(log_softmax_rows(logits, c->Mall, c->B * c->Tmax, c->nitem, nullptr, lp, nullptr, c->st));
+  HIP_TRY(log_softmax_rows(root_logits, c->Mb, c->B, c->nitem, nullptr, root, nullptr, c->st));
+  int* acc = accepted ? accepted : c->acc_tmp;
+  int* ta = t_after ? t_after : c->tafter_tmp;
+  if (!relaxed) {
+    launch_verify_strict(c->state, c->tree, c->trie, lp, root, c->nitem, cf.codebook, cf.L, keys, c->max_cand, acc,
+                         ta, c->B, c->st);
+  } else {
+    RelaxArgs ra = c->relax;
+    ra.keys = keys;
+    CandBuf cb{reinterpret_cast<uint32_t*>(base + o_cand[0]), reinterpret_cast<int*>(base + o_cand[1]),
+               reinterpret_cast<int*>(base + o_cand[2]), reinterpret_cast<float*>(base + o_cand[3]),
+               reinterpret_cast<float*>(base + o_cand[4])};
+    launch_verify_relaxed(c->state, c->tree, c->trie, lp, root, c->dft.lp, c->dft.root, c->nitem, cf.codebook, cf.L,
+                          cb, c->max_cand, ra, acc, ta, c->B, c->st);
+  }
+  HIP_TRY(hipGetLastError());
   HIP_TRY(hipStreamSynchronize(c->st));
   return ATSPEED_OK;
 }
