@@ -2,8 +2,9 @@
 //
 // bf16 path: MFMA v_mfma_f32_32x32x16_bf16 (fp32 accumulate), block tile
 // BM x BN x 64 fetched by direct global->LDS DMA into two LDS stages
-// (XOR-swizzled 16-byte chunks), wave tile TM x TN blocks of 32x32, tile shape
-// chosen by the row count.  Epilogues are fused:
+// (XOR-swizzled 16-byte chunks), or three for small row counts, wave tile
+// TM x TN blocks of 32x32, tile shape chosen by the row count.  Epilogues are
+// fused:
 //   QKV   rotary embedding on q and k, rounding to bf16, q to its row buffer,
 //         k/v scattered into the prefix cache or the tree KV buffer.  The tile's
 //         weight rows are interleaved (qkv_logical) so that a column's
@@ -111,6 +112,33 @@ __device__ __forceinline__ void load_stage(unsigned char* stage, int wave, const
         (lds_void_t*)(stage + a_bytes + (wave * NB + j) * 1024), 16, 0, 0);
 }
 
+// The same stage load as untracked inline-asm DMA, for the pipelines with more
+// than two stages: the compiler counts only a few LDS-DMA stores in flight and
+// would drain all of them once per round, so these loads are issued where it
+// does not see them and the pipeline waits with an explicit vmcnt.
+__device__ __forceinline__ const void* uniform_ptr(const void* p) {
+  const uint64_t v = (uint64_t)(uintptr_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v), hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return (const void*)(uintptr_t)(((uint64_t)hi << 32) | lo);
+}
+template <int NA, int NB>
+__device__ __forceinline__ void load_stage_u(unsigned char* stage, int wave, const bf16_t* A, const int* a_off,
+                                             const bf16_t* const* Bp, const int* b_off, int k0, int a_bytes) {
+  const void* Au = uniform_ptr(A);
+#pragma unroll
+  for (int j = 0; j < NA; ++j) {
+    const uint32_t lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_t*)(stage + (wave * NA + j) * 1024));
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"((uint32_t)(a_off[j] + k0) * 2u),
+                 "s"(Au) : "memory", "m0");
+  }
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const uint32_t lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_t*)(stage + a_bytes + (wave * NB + j) * 1024));
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"((uint32_t)(b_off[j] + k0) * 2u),
+                 "s"(uniform_ptr(Bp[j])) : "memory", "m0");
+  }
+}
+
 // One LDS stage (64 columns of k) through the MFMAs.  Fragments of k-step kk+1
 // are read into a second register set while the MFMAs of step kk issue, so the
 // LDS latency hides behind matrix work instead of stalling every step.
@@ -157,17 +185,20 @@ __device__ __forceinline__ void mma_stage(const unsigned char* stage, int wave_m
   });
 }
 
-template <int WM, int WN, int TM, int TN, int BMAP, int EPI>
+template <int WM, int WN, int TM, int TN, int BMAP, int EPI, int NS>
 __global__ void __launch_bounds__(64 * WM * WN)
 gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ Mdev, int Mt, int N, int K,
                  BArgs b, EpiArgs e) {
   using T = Tile<WM, WN, TM, TN>;
   constexpr int NW = WM * WN;
   static_assert(NW == 2 || NW == 4 || NW == 8, "two, four or eight waves");
+  static_assert(NS >= 2 && NS <= 4, "two to four LDS stages");
   constexpr int NA = T::BM / (8 * NW);   // wave instructions per stage for A (8 rows of 128 B each)
   constexpr int NB = T::BN / (8 * NW);
   __shared__ __align__(1024) unsigned char st0[T::STAGE];
   __shared__ __align__(1024) unsigned char st1[T::STAGE];
+  __shared__ __align__(1024) unsigned char st2[NS >= 3 ? T::STAGE : 16];
+  __shared__ __align__(1024) unsigned char st3[NS >= 4 ? T::STAGE : 16];
   const int M = *Mdev;
   // XCD-aware tile order: workgroup L is dispatched to XCD L % 8; XCD x owns the
   // contiguous range x*per .. x*per+per-1 of the tiles.  Tiles are numbered in
@@ -263,11 +294,55 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
   // Two-stage pipeline: while the MFMAs consume one LDS stage, the DMA of the
   // next k-tile fills the other.  Each stage is its own LDS array, named at
   // compile time, so the compiler sees that a step's DMA and fragment reads
-  // touch different objects and inserts no waits between them.  (A third stage
-  // was slower on every shape measured: the compiler tracks only a few
-  // in-flight LDS-DMA stores, so with two stages in flight it drained them all
-  // once per round.)
+  // touch different objects and inserts no waits between them.
   // nk is even (each k-range is a multiple of 128, checked on the host)
+  if constexpr (NS > 2) {
+  // NS-stage pipeline (small row counts, where each k-tile's weights arrive
+  // cold from HBM): stage s of round kt0 computes k-tile kt0+s while the DMA of
+  // k-tiles up to kt0+s+NS-1 is in flight; at each stage end the wave waits
+  // until only the newest NS-2 stages' loads are outstanding, then a bare
+  // barrier makes every wave's share of the next stage visible.  Empty asm with
+  // a memory clobber on both sides keeps fragment reads and DMA issue from
+  // moving across the barrier (the barrier intrinsic does not order memory).
+  auto stage = [&](auto S) -> unsigned char* {
+    constexpr int s_ = decltype(S)::value % NS;
+    return s_ == 0 ? st0 : (s_ == 1 ? st1 : (s_ == 2 ? st2 : st3));
+  };
+  constexpr int NLOADS = NA + NB;                 // DMA instructions per stage per lane
+  constexpr int ALLOW = NLOADS * (NS - 2);        // loads that may stay in flight at a stage boundary
+  constexpr int WAITCNT = (ALLOW & 0xF) | (((ALLOW >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8);
+  constexpr int WAITALL = (0x7 << 4) | (0xF << 8);  // vmcnt(0)
+  static_assert(ALLOW < 64, "vmcnt holds 6 bits");
+  static_for<NS - 1>([&](auto S) {
+    constexpr int s_ = decltype(S)::value;
+    if (s_ < nk) load_stage_u<NA, NB>(stage(S), wave, A, a_off, Bp, b_off, s_ * 64, T::A_BYTES);
+  });
+  asm volatile("" ::: "memory");
+  if (NS - 2 < nk) __builtin_amdgcn_s_waitcnt(WAITCNT);
+  else __builtin_amdgcn_s_waitcnt(WAITALL);
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+  for (int kt0 = 0; kt0 < nk; kt0 += NS) {
+    static_for<NS>([&](auto S) {
+      constexpr int s_ = decltype(S)::value;
+      const int kt = kt0 + s_;
+      if (kt < nk) {
+        if (kt + NS - 1 < nk)
+          load_stage_u<NA, NB>(stage(std::integral_constant<int, s_ + NS - 1>{}), wave, A, a_off, Bp, b_off,
+                               (kt + NS - 1) * 64, T::A_BYTES);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_stage<WM, WN, TM, TN>(stage(S), wave_m, wave_n, fr, fc, acc, T::A_BYTES);
+        asm volatile("" ::: "memory");
+        if (kt + NS - 1 < nk) __builtin_amdgcn_s_waitcnt(WAITCNT);
+        else __builtin_amdgcn_s_waitcnt(WAITALL);
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+      }
+    });
+  }
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  } else {
   load_stage<NA, NB>(st0, wave, A, a_off, Bp, b_off, 0, T::A_BYTES);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
@@ -285,6 +360,7 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
     mma_stage<WM, WN, TM, TN>(st1, wave_m, wave_n, fr, fc, acc, T::A_BYTES);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
+  }
   }
 
   // ---- epilogue.  acc[i][j][r] is row (r/4)*8 + (lane/32)*4 + r%4, column lane%32 of block (i, j).
@@ -554,7 +630,7 @@ __global__ void epi_f32_kernel(const float* __restrict__ C, const int* __restric
 // Launch of one instantiation over the tiles of a call.  The widest tiles,
 // 256x256 of 8 waves (64x128 each, two waves per SIMD), let one wave's LDS and
 // barrier waits hide behind the other's MFMAs.
-template <int BMAP, int EPI, int WMW, int WNW, int TMW, int TNW>
+template <int BMAP, int EPI, int WMW, int WNW, int TMW, int TNW, int NS = 2>
 static hipError_t launch_bf16(const GemmCall& g, hipStream_t st) {
   using T = Tile<WMW, WNW, TMW, TNW>;
   BArgs b{(const bf16_t*)g.w0, (const bf16_t*)g.w1, (const bf16_t*)g.w2, g.split};
@@ -570,7 +646,7 @@ static hipError_t launch_bf16(const GemmCall& g, hipStream_t st) {
   const int Mt = (g.Mmax + T::BM - 1) / T::BM, Nt = (g.N + T::BN - 1) / T::BN;
   const int per = (kparts * Mt * Nt + 7) / 8;
   dim3 grid(8 * per);
-  auto kern = gemm_bf16_kernel<WMW, WNW, TMW, TNW, BMAP, EPI>;
+  auto kern = gemm_bf16_kernel<WMW, WNW, TMW, TNW, BMAP, EPI, NS>;
   hipLaunchKernelGGL(kern, grid, dim3(T::NT), 0, st, (const bf16_t*)g.A, g.lda, g.Mdev, Mt, g.N, g.K, b, e);
   return hipGetLastError();
 }
@@ -595,8 +671,17 @@ struct Shape { int bm, bn, per_cu; float t0, t4k; };
 // (fitted warm); gate/up: the first three, fitted with the weights arriving cold
 // from HBM as they do in a forward (picks the fastest measured shape at every
 // one of 13 row counts from 320 to 4,096)
+// and 64x256 of 8 waves with three stages (one per CU).  The 128x256 and
+// 64x256 tiles of 8 waves run three LDS stages (144 and 120 KB), which hides
+// the cold weight fetch at a few hundred rows: q/k/v at 320 rows 86 -> 59 us,
+// 128x256 q/k/v at 400-640 rows 85-90 -> 70-78 us and gate/up 143-152 ->
+// 120-135 us, with cold weights.  The q/k/v constants are scaled from those
+// measurements (256x192 keeps 960 rows and more); gate/up keeps its two-stage
+// constant, with which the 128x256 tile is picked only where it was already
+// fastest (about 640 rows: 152 -> 135 us)
 constexpr Shape kQkvShapes[] = {
-    {256, 256, 1, 0.f, 98.f}, {128, 256, 1, 0.f, 67.f}, {64, 256, 2, 0.f, 73.f}, {256, 192, 1, 0.f, 83.f}};
+    {256, 256, 1, 0.f, 98.f}, {128, 256, 1, 0.f, 57.f}, {64, 256, 2, 0.f, 73.f}, {256, 192, 1, 0.f, 83.f},
+    {64, 256, 1, 0.f, 46.f}};
 constexpr Shape kGuShapes[] = {{256, 256, 1, 0.f, 104.f}, {128, 256, 1, 0.f, 70.f}, {64, 256, 2, 0.f, 78.f}};
 // o, down, output head: 256x256, 256x128 (8 waves), 128x128 (4 waves, two per
 // CU), 64x64 (2 waves, four per CU)
@@ -604,6 +689,12 @@ constexpr Shape kGuShapes[] = {{256, 256, 1, 0.f, 104.f}, {128, 256, 1, 0.f, 70.
 // measured shape at all 12 row counts from 320 to 4,096, for o and for down)
 constexpr Shape kRowShapes[] = {
     {256, 256, 1, 25.f, 97.5f}, {256, 128, 1, 10.5f, 70.f}, {128, 128, 2, 14.f, 59.f}, {64, 64, 4, 6.f, 50.f}};
+// residual projections also: 128x128 of 4 waves with three stages (one per CU;
+// 320 rows: o 33 -> 26 us, down 72 -> 56 us with cold weights; constants from
+// those two measurements)
+constexpr Shape kResidShapes[] = {
+    {256, 256, 1, 25.f, 97.5f}, {256, 128, 1, 10.5f, 70.f}, {128, 128, 2, 14.f, 59.f}, {64, 64, 4, 6.f, 50.f},
+    {128, 128, 1, 4.4f, 36.f}};
 
 template <int NSH>
 int pick_shape(const Shape (&sh)[NSH], int M, int N, int K, int kparts, float partial) {
@@ -628,22 +719,24 @@ hipError_t gemm(const GemmCall& g, hipStream_t st) {
       case GEMM_QKV:
         switch (pick_shape(kQkvShapes, M, g.N, g.K, 1, 1.f)) {
           case 0: return launch_bf16<BMAP_QKV, EPI_QKV, 4, 2, 2, 4>(g, st);
-          case 1: return launch_bf16<BMAP_QKV, EPI_QKV, 4, 2, 1, 4>(g, st);
+          case 1: return launch_bf16<BMAP_QKV, EPI_QKV, 4, 2, 1, 4, 3>(g, st);
           case 2: return launch_bf16<BMAP_QKV, EPI_QKV, 1, 2, 2, 4>(g, st);
-          default: return launch_bf16<BMAP_QKV, EPI_QKV, 4, 2, 2, 3>(g, st);
+          case 3: return launch_bf16<BMAP_QKV, EPI_QKV, 4, 2, 2, 3>(g, st);
+          default: return launch_bf16<BMAP_QKV, EPI_QKV, 2, 4, 1, 2, 3>(g, st);
         }
       case GEMM_GU:
         switch (pick_shape(kGuShapes, M, g.N, g.K, 1, 1.f)) {
           case 0: return launch_bf16<BMAP_GU, EPI_GU, 4, 2, 2, 4>(g, st);
-          case 1: return launch_bf16<BMAP_GU, EPI_GU, 4, 2, 1, 4>(g, st);
+          case 1: return launch_bf16<BMAP_GU, EPI_GU, 4, 2, 1, 4, 3>(g, st);
           default: return launch_bf16<BMAP_GU, EPI_GU, 1, 2, 2, 4>(g, st);
         }
       case GEMM_RESID:
-        switch (pick_shape(kRowShapes, M, g.N, g.K, g.part ? 2 : 1, 0.5f)) {
+        switch (pick_shape(kResidShapes, M, g.N, g.K, g.part ? 2 : 1, 0.5f)) {
           case 0: return launch_bf16<BMAP_PLAIN, EPI_RESID, 4, 2, 2, 4>(g, st);
           case 1: return launch_bf16<BMAP_PLAIN, EPI_RESID, 4, 2, 2, 2>(g, st);
           case 2: return launch_bf16<BMAP_PLAIN, EPI_RESID, 2, 2, 2, 2>(g, st);
-          default: return launch_bf16<BMAP_PLAIN, EPI_RESID, 1, 2, 2, 1>(g, st);
+          case 3: return launch_bf16<BMAP_PLAIN, EPI_RESID, 1, 2, 2, 1>(g, st);
+          default: return launch_bf16<BMAP_PLAIN, EPI_RESID, 2, 2, 2, 2, 3>(g, st);
         }
       default:
         switch (pick_shape(kRowShapes, M, g.N, g.K, 1, 0.5f)) {
