@@ -16,6 +16,8 @@ Modules
             strict top-K verification (Algorithm 1), speculative decode loop
   philox    Philox4x32-10 counter-based generator (Salmon et al., SC'11)
   relaxed   relaxed sampling verification (Sec. 3.2, Algorithm 2)
+  align     draft alignment objectives AtSpeed-S / AtSpeed-R (Sec. 3.1, 3.2),
+            their gradients and the item-head gradient
 
 Parity status of each function is stated in its module docstring.
 """

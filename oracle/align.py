@@ -1,0 +1,143 @@
+"""Draft alignment objectives of AtSpeed (Sec. 3.1 and 3.2), fp64.
+
+TEST INFRASTRUCTURE ONLY (see the package docstring).
+
+Per training context c = (x, y_<t) -- a user's prefix followed by the first t-1
+codes of a sequence y -- the draft's token distribution q(.|c) and the target's
+p(.|c) are softmaxes over the item-token columns (the normaliser of the pinned
+reading), and V_c = ConstrainedTopK(q) is the set of the K trie-valid codes of
+level t with the largest q (ties: smaller code first).
+
+AtSpeed-S, per context (the bracket of the Align-S loss of Sec. 3.1): the
+reverse KL over V_c minus the density regulariser,
+    sum_{v in V_c} q(v) log(q(v)/p(v)) - sum_{v in V_c} q(v) log(q(v)/p_K),
+where p_K = p(y_{K,t} | y_{K,<t}) is the target's probability of the t-th code
+of the K-th sequence of the context's user given that sequence's own prefix.
+The q log q terms cancel, leaving sum_{v in V_c} q(v) (log p_K - log p(v)).
+
+AtSpeed-R, per context (Sec. 3.2): TVD(p', q') = 1/2 sum_{v in V_c} |p'(v) - q'(v)|
+with p', q' the distributions p, q truncated to V_c and renormalised.  The
+paper's "top-K valid tokens" is read as the same V_c as AtSpeed-S.
+
+Aggregation: L = (1 / |D'|) sum_{(x, Y) in D'} sum_{y in Y} (1/|y|) sum_t l(c_t).
+A context shared by several sequences of Y (a common prefix) counts once per
+sequence through it.  D' holds, per user, the target's top-K sequences
+(AtSpeed-R) or the top-K of beam search under the mixture (1-lambda) q + lambda p
+of the two models' token distributions (AtSpeed-S; lambda = 1 gives the target's
+top-K).  The recommendation loss L_Rec of the overall objective needs the
+dataset's labels, which synthetic histories do not have: alpha = 1.
+
+Gradients with respect to the draft's item logits z (q = softmax(z)), V_c held
+fixed (the selection is piecewise constant in z):
+    S: dl/dz_j = q_j (a_j [j in V_c] - sum_{v in V_c} q_v a_v),  a_v = log p_K - log p(v)
+    R: dl/dz_j = [j in V_c] q'_j (s_j - sum_{v in V_c} s_v q'_v) / 2,  s_v = sign(q'_v - p'_v)
+Training the draft's item-head rows W (z = W h for the normed final hidden h of
+the context) then has dL/dW = sum_c w_c (dl/dz)(c) h(c)^T.
+
+Parity: pinned in tests/test_oracle_align.py -- the gradients against central
+finite differences of the losses, a hand-worked context for each loss
+(tests/golden/align_example.json), the regulariser's sign (negative when every
+code of V_c is more probable under the target than the K-th sequence's code,
+positive when every one is less), TVD's range and its Eq. 6 identity
+(1 - TVD = sum of minima), and the dataset weights against a hand count.
+"""
+from __future__ import annotations
+
+import math
+from typing import Dict, List, Sequence, Tuple
+
+import numpy as np
+
+Path = Tuple[int, ...]
+
+
+def softmax(z: np.ndarray) -> np.ndarray:
+    e = np.exp(z - np.max(z))
+    return e / e.sum()
+
+
+def constrained_topk(lq: np.ndarray, cols: Sequence[int], K: int) -> List[int]:
+    """The K columns of ``cols`` with the largest draft log-prob (ties: smaller column)."""
+    return sorted(cols, key=lambda c: (-lq[c], c))[:K]
+
+
+def align_s(lq: np.ndarray, lp: np.ndarray, cols: Sequence[int], K: int, log_pK: float):
+    """AtSpeed-S loss of one context and its gradient with respect to the draft's logits.
+
+    lq, lp: log-probabilities over the item columns (draft, target); cols: the
+    trie-valid columns of the level; log_pK: log p(y_{K,t} | y_{K,<t}).
+    """
+    q = np.exp(lq)
+    vc = constrained_topk(lq, cols, K)
+    a = {v: log_pK - lp[v] for v in vc}
+    loss = sum(q[v] * a[v] for v in vc)
+    grad = -q * loss
+    for v in vc:
+        grad[v] += q[v] * a[v]
+    return float(loss), grad, vc
+
+
+def align_r(lq: np.ndarray, lp: np.ndarray, cols: Sequence[int], K: int):
+    """AtSpeed-R loss (TVD over V_c) of one context and its gradient."""
+    vc = constrained_topk(lq, cols, K)
+    qv = np.exp(np.array([lq[v] for v in vc]))
+    pv = np.exp(np.array([lp[v] for v in vc]))
+    qn, pn = qv / qv.sum(), pv / pv.sum()
+    loss = 0.5 * float(np.abs(pn - qn).sum())
+    s = np.sign(qn - pn)
+    g = 0.5 * qn * (s - float((s * qn).sum()))
+    grad = np.zeros_like(lq)
+    for i, v in enumerate(vc):
+        grad[v] = g[i]
+    return loss, grad, vc
+
+
+def context_weights(Y: Sequence[Sequence[Path]], L: int) -> List[Dict[Path, float]]:
+    """Per user, the weight of every context (a prefix of length 0..L-1) in the
+    aggregated loss: (sequences of Y through it) / (|y| x number of users)."""
+    B = len(Y)
+    out = []
+    for seqs in Y:
+        w: Dict[Path, float] = {}
+        for y in seqs:
+            for t in range(len(y)):
+                w[tuple(y[:t])] = w.get(tuple(y[:t]), 0.0) + 1.0 / (len(y) * B)
+        out.append(w)
+    return out
+
+
+def log_pK_of(Y: Sequence[Path], lp_of, codebook: int) -> List[float]:
+    """log p(y_{K,t} | y_{K,<t}) for t = 1..L of the K-th (last) sequence of one user's Y."""
+    yk = Y[-1]
+    return [float(lp_of(tuple(yk[:t]))[codebook * t + yk[t]]) for t in range(len(yk))]
+
+
+def aligned_loss(mode: str, lq_of, lp_of, trie, Y: Sequence[Sequence[Path]], K: int, L: int, codebook: int):
+    """Aggregated loss over all users and the gradient of every context.
+
+    lq_of / lp_of(u, path) -> item log-probs of the draft / target at that
+    context of user u.  Returns (loss, {(u, path): (weight, grad)}).
+    """
+    W = context_weights(Y, L)
+    total, grads = 0.0, {}
+    for u, wu in enumerate(W):
+        lpk = log_pK_of(Y[u], lambda p: lp_of(u, p), codebook)
+        for path, w in wu.items():
+            t = len(path)
+            cols = [codebook * t + c for c in trie.children(path)]
+            lq, lp = lq_of(u, path), lp_of(u, path)
+            if mode == "S":
+                l, g, _ = align_s(lq, lp, cols, K, lpk[t])
+            else:
+                l, g, _ = align_r(lq, lp, cols, K)
+            total += w * l
+            grads[(u, path)] = (w, g)
+    return total, grads
+
+
+def head_gradient(grads: Dict, hidden: Dict) -> np.ndarray:
+    """dL/dW for the item head: sum over contexts of w * grad ⊗ h (hidden: (u, path) -> h)."""
+    keys = list(grads)
+    G = np.stack([grads[k][0] * grads[k][1] for k in keys])      # [C, n_item]
+    Hm = np.stack([np.asarray(hidden[k], dtype=np.float64) for k in keys])   # [C, d]
+    return G.T @ Hm

@@ -1,0 +1,105 @@
+"""Pins for the oracle's draft alignment objectives (Sec. 3.1 Align-S, Sec. 3.2 Align-R), CPU."""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+from oracle.align import (align_r, align_s, aligned_loss, constrained_topk, context_weights, head_gradient,
+                          log_pK_of)
+from oracle.search import table_scorer
+from oracle.trie import Trie
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def test_hand_worked_context():
+    with open(os.path.join(GOLDEN, "align_example.json")) as f:
+        g = json.load(f)
+    lq, lp = np.log(g["q"]), np.log(g["p"])
+    assert constrained_topk(lq, g["valid_cols"], g["K"]) == g["V_c"]
+    ls, _, vc = align_s(lq, lp, g["valid_cols"], g["K"], math.log(g["p_K"]))
+    assert vc == g["V_c"]
+    assert abs(ls - 0.4 * math.log(1.25)) < 1e-12
+    lr, _, _ = align_r(lq, lp, g["valid_cols"], g["K"])
+    assert abs(lr - g["loss_R"][0] / g["loss_R"][1]) < 1e-12
+
+
+@pytest.mark.parametrize("mode", ["S", "R"])
+def test_gradients_match_finite_differences(mode):
+    rng = np.random.default_rng(3)
+    n, cols, K = 24, [1, 3, 4, 8, 9, 12, 17, 20], 4
+    for trial in range(5):
+        z = rng.standard_normal(n) * 2
+        lp = np.log(np.exp(rng.standard_normal(n)) / np.exp(rng.standard_normal(n)).sum())
+        lpk = float(rng.normal(-3, 1))
+
+        def f(zz):
+            lq = zz - (np.max(zz) + np.log(np.exp(zz - np.max(zz)).sum()))
+            return (align_s(lq, lp, cols, K, lpk) if mode == "S" else align_r(lq, lp, cols, K))[:2]
+        l0, g = f(z)
+        vc0 = constrained_topk(z, cols, K)
+        for j in range(n):
+            e = np.zeros(n)
+            e[j] = 1e-6
+            # V_c is piecewise constant: only compare where the step keeps it
+            if constrained_topk(z + e, cols, K) != vc0 or constrained_topk(z - e, cols, K) != vc0:
+                continue
+            fd = (f(z + e)[0] - f(z - e)[0]) / 2e-6
+            assert abs(fd - g[j]) < 1e-6 * max(1.0, abs(fd)), (mode, trial, j, fd, g[j])
+
+
+def test_density_regulariser_sign():
+    q = np.array([0.5, 0.3, 0.1, 0.1])
+    lp = np.log(np.array([0.4, 0.3, 0.2, 0.1]))
+    cols = [0, 1, 2, 3]
+    # V_c = {0, 1}; both more probable under the target than p_K = 0.15: negative
+    assert align_s(np.log(q), lp, cols, 2, math.log(0.15))[0] < 0
+    # both less probable than p_K = 0.5: positive
+    assert align_s(np.log(q), lp, cols, 2, math.log(0.5))[0] > 0
+
+
+def test_tvd_range_and_sum_of_minima():
+    rng = np.random.default_rng(5)
+    cols = list(range(10))
+    for _ in range(20):
+        lq = np.log(rng.dirichlet(np.ones(10)))
+        lp = np.log(rng.dirichlet(np.ones(10)))
+        t, _, vc = align_r(lq, lp, cols, 10)
+        qn, pn = np.exp(lq), np.exp(lp)
+        assert 0.0 <= t <= 1.0
+        assert abs((1 - t) - np.minimum(qn, pn).sum()) < 1e-12     # Eq. 6: b = 1 - TVD
+        assert align_r(lq, lq, cols, 4)[0] == 0.0
+
+
+def test_context_weights_hand_count():
+    Y = [[(0, 0), (0, 1), (1, 0)]]
+    w = context_weights(Y, 2)[0]
+    assert w == {(): 1.5, (0,): 1.0, (1,): 0.5}
+    w2 = context_weights([[(0, 0)], [(1, 1), (1, 0)]], 2)
+    assert w2[0] == {(): 0.25, (0,): 0.25} and w2[1] == {(): 0.5, (1,): 0.5}
+
+
+def test_log_pK_is_the_kth_sequence_along_its_own_prefix():
+    cb = 3
+    rows = {(): np.log([0.5, 0.3, 0.2, 0.1, 0.1, 0.8]), (1,): np.log([0.2, 0.2, 0.6, 0.7, 0.2, 0.1])}
+    got = log_pK_of([(0, 2), (1, 0)], lambda p: rows[p], cb)
+    assert np.allclose(got, [math.log(0.3), math.log(0.7)])
+
+
+def test_aggregate_and_head_gradient():
+    # two users, one level: the aggregate is the weighted sum of the contexts and
+    # the head gradient is the weighted sum of outer products
+    cb, L, K = 3, 1, 1
+    trie = Trie(np.array([[0], [1], [2]]))
+    rng = np.random.default_rng(1)
+    lq = {u: np.log(rng.dirichlet(np.ones(3))) for u in range(2)}
+    lp = {u: np.log(rng.dirichlet(np.ones(3))) for u in range(2)}
+    Y = [[(int(np.argmax(lp[u])),)] for u in range(2)]
+    loss, grads = aligned_loss("R", lambda u, p: lq[u], lambda u, p: lp[u], trie, Y, K, L, cb)
+    assert abs(loss - sum(0.5 * align_r(lq[u], lp[u], [0, 1, 2], K)[0] for u in range(2))) < 1e-12
+    h = {k: rng.standard_normal(4) for k in grads}
+    G = head_gradient(grads, h)
+    want = sum(grads[k][0] * np.outer(grads[k][1], h[k]) for k in grads)
+    assert np.allclose(G, want)
