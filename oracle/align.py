@@ -34,12 +34,18 @@ fixed (the selection is piecewise constant in z):
 Training the draft's item-head rows W (z = W h for the normed final hidden h of
 the context) then has dL/dW = sum_c w_c (dl/dz)(c) h(c)^T.
 
+The optimizer is AdamW (the paper's implementation details) with decoupled
+weight decay: w <- w - lr wd w - lr m_hat / (sqrt(v_hat) + eps), m_hat and v_hat
+the bias-corrected first and second moments.
+
 Parity: pinned in tests/test_oracle_align.py -- the gradients against central
 finite differences of the losses, a hand-worked context for each loss
 (tests/golden/align_example.json), the regulariser's sign (negative when every
 code of V_c is more probable under the target than the K-th sequence's code,
 positive when every one is less), TVD's range and its Eq. 6 identity
-(1 - TVD = sum of minima), and the dataset weights against a hand count.
+(1 - TVD = sum of minima), the dataset weights against a hand count, and AdamW
+against torch.optim.AdamW (fp64, CPU) over several steps and against its
+first-step closed form (a step of lr times the gradient's sign without decay).
 """
 from __future__ import annotations
 
@@ -141,3 +147,15 @@ def head_gradient(grads: Dict, hidden: Dict) -> np.ndarray:
     G = np.stack([grads[k][0] * grads[k][1] for k in keys])      # [C, n_item]
     Hm = np.stack([np.asarray(hidden[k], dtype=np.float64) for k in keys])   # [C, d]
     return G.T @ Hm
+
+
+def adamw_step(w: np.ndarray, m: np.ndarray, v: np.ndarray, g: np.ndarray, step: int, lr: float,
+               beta1: float, beta2: float, eps: float, weight_decay: float):
+    """One AdamW step (1-based ``step``); returns the new (w, m, v)."""
+    m = beta1 * m + (1.0 - beta1) * g
+    v = beta2 * v + (1.0 - beta2) * g * g
+    m_hat = m / (1.0 - beta1 ** step)
+    v_hat = v / (1.0 - beta2 ** step)
+    w = w - lr * weight_decay * w
+    w = w - lr * m_hat / (np.sqrt(v_hat) + eps)
+    return w, m, v

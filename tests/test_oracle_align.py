@@ -6,7 +6,7 @@ import os
 import numpy as np
 import pytest
 
-from oracle.align import (align_r, align_s, aligned_loss, constrained_topk, context_weights, head_gradient,
+from oracle.align import (adamw_step, align_r, align_s, aligned_loss, constrained_topk, context_weights, head_gradient,
                           log_pK_of)
 from oracle.search import table_scorer
 from oracle.trie import Trie
@@ -103,3 +103,33 @@ def test_aggregate_and_head_gradient():
     G = head_gradient(grads, h)
     want = sum(grads[k][0] * np.outer(grads[k][1], h[k]) for k in grads)
     assert np.allclose(G, want)
+
+
+def test_adamw_matches_torch_adamw():
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(3)
+    w0 = rng.standard_normal((5, 4))
+    grads = [rng.standard_normal((5, 4)) for _ in range(4)]
+    hp = dict(lr=1e-2, beta1=0.8, beta2=0.95, eps=1e-6, weight_decay=0.1)
+    p = torch.tensor(w0, dtype=torch.float64, requires_grad=True)
+    opt = torch.optim.AdamW([p], lr=hp["lr"], betas=(hp["beta1"], hp["beta2"]), eps=hp["eps"],
+                            weight_decay=hp["weight_decay"])
+    w, m, v = w0.copy(), np.zeros_like(w0), np.zeros_like(w0)
+    for step, g in enumerate(grads, 1):
+        p.grad = torch.tensor(g, dtype=torch.float64)
+        opt.step()
+        w, m, v = adamw_step(w, m, v, g, step, **hp)
+        np.testing.assert_allclose(w, p.detach().numpy(), rtol=0, atol=1e-14)
+
+
+def test_adamw_first_step_closed_form():
+    # step 1 without decay: the bias-corrected moments are g and g^2, so the step
+    # is lr * g / (|g| + eps), i.e. lr times the sign for |g| >> eps
+    g = np.array([3.0, -0.5, 1e-3, -2e-3])
+    w, m, v = adamw_step(np.zeros(4), np.zeros(4), np.zeros(4), g, 1, 0.1, 0.9, 0.999, 1e-12, 0.0)
+    np.testing.assert_allclose(w, -0.1 * np.sign(g), rtol=1e-8)
+    np.testing.assert_allclose(m, 0.1 * g)
+    np.testing.assert_allclose(v, 0.001 * g * g)
+    # decay alone shrinks by lr * wd
+    w2, _, _ = adamw_step(np.full(4, 2.0), np.zeros(4), np.zeros(4), np.zeros(4), 1, 0.1, 0.9, 0.999, 1e-8, 0.5)
+    np.testing.assert_allclose(w2, 2.0 * (1 - 0.05))
