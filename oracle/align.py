@@ -24,8 +24,19 @@ A context shared by several sequences of Y (a common prefix) counts once per
 sequence through it.  D' holds, per user, the target's top-K sequences
 (AtSpeed-R) or the top-K of beam search under the mixture (1-lambda) q + lambda p
 of the two models' token distributions (AtSpeed-S; lambda = 1 gives the target's
-top-K).  The recommendation loss L_Rec of the overall objective needs the
-dataset's labels, which synthetic histories do not have: alpha = 1.
+top-K): the last beam-search step's sequences by default, or those of every step
+(the multi-step data the paper compares against; sequences of length 1..L, the
+K-th full-length sequence last, which fixes p_K).
+
+Overall objective (Eq. 5 and its AtSpeed-R counterpart): alpha L_Align +
+(1 - alpha) L_Rec.  L_Rec, the recommender's own loss (the NLL of the next
+item's tokens), may be substituted by the recommender's loss of choice; the
+synthetic histories have no ground-truth next item, so its labels are the
+training sequences themselves:
+    L_Rec = (1 / |D'|) sum sum_{y in Y} (1/|y|) sum_t -log q(y_t | c_t),
+i.e. per context c with weight w_c and label distribution pi_c (the sequences'
+next codes, each counted with 1/|y|, normalised): -sum_v pi_c(v) log q(v), with
+gradient q - pi_c.
 
 Gradients with respect to the draft's item logits z (q = softmax(z)), V_c held
 fixed (the selection is piecewise constant in z):
@@ -43,7 +54,10 @@ finite differences of the losses, a hand-worked context for each loss
 (tests/golden/align_example.json), the regulariser's sign (negative when every
 code of V_c is more probable under the target than the K-th sequence's code,
 positive when every one is less), TVD's range and its Eq. 6 identity
-(1 - TVD = sum of minima), the dataset weights against a hand count, and AdamW
+(1 - TVD = sum of minima), the dataset weights and label distributions against
+hand counts, the recommendation loss against torch's cross-entropy with class
+probabilities and the aggregate at alpha = 0 against the per-sequence NLL summed
+token by token, and AdamW
 against torch.optim.AdamW (fp64, CPU) over several steps and against its
 first-step closed form (a step of lr times the gradient's sign without decay).
 """
@@ -98,6 +112,29 @@ def align_r(lq: np.ndarray, lp: np.ndarray, cols: Sequence[int], K: int):
     return loss, grad, vc
 
 
+def rec_loss(lq: np.ndarray, pi: Dict[int, float]):
+    """Recommendation (NLL) loss of one context with label distribution ``pi``
+    (column -> probability) and its gradient with respect to the draft's logits."""
+    q = np.exp(lq)
+    loss = -sum(w * lq[c] for c, w in pi.items())
+    grad = q * sum(pi.values())
+    for c, w in pi.items():
+        grad[c] -= w
+    return float(loss), grad
+
+
+def label_distributions(Y: Sequence[Path], codebook: int) -> Dict[Path, Dict[int, float]]:
+    """Per context of one user: the next codes of the sequences through it, each
+    counted with 1/|y|, as a distribution over item columns."""
+    acc: Dict[Path, Dict[int, float]] = {}
+    for y in Y:
+        for t in range(len(y)):
+            d = acc.setdefault(tuple(y[:t]), {})
+            col = codebook * t + y[t]
+            d[col] = d.get(col, 0.0) + 1.0 / len(y)
+    return {c: {k: v / sum(d.values()) for k, v in d.items()} for c, d in acc.items()}
+
+
 def context_weights(Y: Sequence[Sequence[Path]], L: int) -> List[Dict[Path, float]]:
     """Per user, the weight of every context (a prefix of length 0..L-1) in the
     aggregated loss: (sequences of Y through it) / (|y| x number of users)."""
@@ -118,16 +155,22 @@ def log_pK_of(Y: Sequence[Path], lp_of, codebook: int) -> List[float]:
     return [float(lp_of(tuple(yk[:t]))[codebook * t + yk[t]]) for t in range(len(yk))]
 
 
-def aligned_loss(mode: str, lq_of, lp_of, trie, Y: Sequence[Sequence[Path]], K: int, L: int, codebook: int):
-    """Aggregated loss over all users and the gradient of every context.
+def aligned_loss(mode: str, lq_of, lp_of, trie, Y: Sequence[Sequence[Path]], K: int, L: int, codebook: int,
+                 alpha: float = 1.0):
+    """Aggregated loss alpha L_Align + (1 - alpha) L_Rec over all users and the
+    gradient of every context.
 
     lq_of / lp_of(u, path) -> item log-probs of the draft / target at that
-    context of user u.  Returns (loss, {(u, path): (weight, grad)}).
+    context of user u.  Returns (loss, {(u, path): (weight, grad)}), grad the
+    per-context gradient alpha dl/dz + (1 - alpha)(q - pi).
     """
     W = context_weights(Y, L)
     total, grads = 0.0, {}
     for u, wu in enumerate(W):
+        if len(Y[u][-1]) != L:
+            raise ValueError("the K-th (last) sequence of a user must be a whole item")
         lpk = log_pK_of(Y[u], lambda p: lp_of(u, p), codebook)
+        pis = label_distributions(Y[u], codebook)
         for path, w in wu.items():
             t = len(path)
             cols = [codebook * t + c for c in trie.children(path)]
@@ -136,8 +179,9 @@ def aligned_loss(mode: str, lq_of, lp_of, trie, Y: Sequence[Sequence[Path]], K: 
                 l, g, _ = align_s(lq, lp, cols, K, lpk[t])
             else:
                 l, g, _ = align_r(lq, lp, cols, K)
-            total += w * l
-            grads[(u, path)] = (w, g)
+            lr, gr = rec_loss(lq, pis[path])
+            total += w * (alpha * l + (1.0 - alpha) * lr)
+            grads[(u, path)] = (w, alpha * g + (1.0 - alpha) * gr)
     return total, grads
 
 

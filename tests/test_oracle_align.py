@@ -6,7 +6,7 @@ import os
 import numpy as np
 import pytest
 
-from oracle.align import (adamw_step, align_r, align_s, aligned_loss, constrained_topk, context_weights, head_gradient,
+from oracle.align import (adamw_step, label_distributions, rec_loss, align_r, align_s, aligned_loss, constrained_topk, context_weights, head_gradient,
                           log_pK_of)
 from oracle.search import table_scorer
 from oracle.trie import Trie
@@ -133,3 +133,72 @@ def test_adamw_first_step_closed_form():
     # decay alone shrinks by lr * wd
     w2, _, _ = adamw_step(np.full(4, 2.0), np.zeros(4), np.zeros(4), np.zeros(4), 1, 0.1, 0.9, 0.999, 1e-8, 0.5)
     np.testing.assert_allclose(w2, 2.0 * (1 - 0.05))
+
+
+def test_rec_loss_matches_torch_cross_entropy():
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(4)
+    z = rng.standard_normal(12)
+    pi = {2: 0.25, 7: 0.5, 11: 0.25}
+    lq = z - np.log(np.exp(z).sum())
+    loss, grad = rec_loss(lq, pi)
+    zt = torch.tensor(z, dtype=torch.float64, requires_grad=True)
+    target = torch.zeros(12, dtype=torch.float64)
+    for c, v in pi.items():
+        target[c] = v
+    ce = torch.nn.functional.cross_entropy(zt[None], target[None])
+    ce.backward()
+    assert abs(loss - ce.item()) < 1e-13
+    np.testing.assert_allclose(grad, zt.grad.numpy(), atol=1e-14)
+
+
+def test_label_distributions_and_weights_of_mixed_lengths():
+    # multi-step data: a whole item and a one-code beam
+    Y = [(0, 0), (0, 1), (1,)]
+    pis = label_distributions(Y, 2)
+    assert pis == {(): {0: 0.5, 1: 0.5}, (0,): {2: 0.5, 3: 0.5}}
+    w = context_weights([[(0, 0), (1,)]], 2)[0]
+    assert w == {(): 1.5, (0,): 0.5}
+
+
+def test_aggregate_alpha_zero_is_sequence_nll():
+    cb, L, K = 3, 2, 2
+    cat = np.array([[a, b] for a in range(3) for b in range(3)])
+    trie = Trie(cat)
+    rng = np.random.default_rng(6)
+    lq = {(u, p): np.log(rng.dirichlet(np.ones(6))) for u in range(2) for p in [(), (0,), (1,), (2,)]}
+    lp = {k: np.log(rng.dirichlet(np.ones(6))) for k in lq}
+    Y = [[(0, 1), (2,), (1, 2)], [(2, 0), (2, 2)]]
+    loss, _ = aligned_loss("S", lambda u, p: lq[(u, p)], lambda u, p: lp[(u, p)], trie, Y, K, L, cb, alpha=0.0)
+    want = 0.0
+    for u, ys in enumerate(Y):
+        for y in ys:
+            want += sum(-lq[(u, tuple(y[:t]))][cb * t + y[t]] for t in range(len(y))) / len(y)
+    assert abs(loss - want / len(Y)) < 1e-12
+
+
+@pytest.mark.parametrize("mode", ["S", "R"])
+def test_aggregate_gradient_finite_differences(mode):
+    # the combined per-context gradient times its weight is d(total)/dz of that context
+    cb, L, K, alpha = 3, 2, 2, 0.4
+    cat = np.array([[a, b] for a in range(3) for b in range(3) if (a + b) % 4 != 3])
+    trie = Trie(cat)
+    rng = np.random.default_rng(8)
+    keys = [(u, p) for u in range(2) for p in [(), (0,), (1,), (2,)]]
+    z = {k: rng.standard_normal(6) for k in keys}
+    lp = {k: np.log(rng.dirichlet(np.ones(6))) for k in keys}
+    Y = [[(0, 1), (2,), (1, 0)], [(2, 0), (0, 0)]]
+
+    def total(zz):
+        lq = lambda u, p: zz[(u, p)] - np.log(np.exp(zz[(u, p)]).sum())
+        return aligned_loss(mode, lq, lambda u, p: lp[(u, p)], trie, Y, K, L, cb, alpha)
+    _, grads = total(z)
+    h = 1e-6
+    for k, (w, g) in grads.items():
+        for j in range(6):
+            zp = {kk: v.copy() for kk, v in z.items()}
+            zm = {kk: v.copy() for kk, v in z.items()}
+            zp[k][j] += h
+            zm[k][j] -= h
+            fd = (total(zp)[0] - total(zm)[0]) / (2 * h)
+            assert abs(fd - w * g[j]) < 1e-7, (k, j, fd, w * g[j])
