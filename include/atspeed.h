@@ -281,7 +281,87 @@ ATSPEED_API atspeed_status atspeed_decode_topk(atspeed_ctx* ctx, int32_t B, int3
  * the stream.  ATSPEED_E_STATE before prefill, or model 1 without a draft. */
 ATSPEED_API atspeed_status atspeed_logprobs(atspeed_ctx* ctx, int32_t model, float* lp_dev, float* root_dev);
 
-/* State access (host arrays; synchronise the stream).  t [B]; nbeams [B];
+/* Draft alignment: training of the draft's item head on the overall objectives
+ * of AtSpeed-S (Sec. 3.1, Eq. 5: alpha L_Align-S + (1 - alpha) L_Rec, for strict
+ * top-K verification) and AtSpeed-R (Sec. 3.2: alpha L_Align-R + (1 - alpha)
+ * L_Rec, for relaxed sampling verification), with AdamW (the optimizer of the
+ * paper's implementation details).
+ *
+ * A batch is the prefilled users with up to S training sequences each: for D'
+ * of Sec. 3.1 with lambda = 1, the target's top-K lists (atspeed_decode_topk in
+ * strict mode) -- the last beam-search step's sequences -- or, for the
+ * multi-step data the paper also evaluates, the target's K beams of every
+ * beam-search step (lengths 1..L).  The last sequence of a user must be a whole
+ * item: it is the K-th sequence of the p_K term.  The contexts are each user's
+ * root and every distinct proper prefix of its sequences; for a context c with
+ * draft and target item distributions q, p and V_c the K trie-valid codes of
+ * the next level with the largest q (ties: smaller code):
+ *   AtSpeed-S: l(c) = sum_{v in V_c} q(v) (log p_K - log p(v)), the reverse KL
+ *     over V_c minus the density regulariser, p_K the target's probability of
+ *     the last sequence's code at that level given its own prefix;
+ *   AtSpeed-R: l(c) = TVD of p and q, both truncated to V_c and renormalised;
+ *   L_Rec: -sum over the sequences through c of log q(next code) (the NLL of the
+ *     training sequences: the recommender's loss, whose dataset labels
+ *     synthetic histories do not have).
+ * Every sequence y adds 1 / (|y| B) to the weight of each of its contexts; the
+ * loss is the weighted sum.  The gradient holds V_c fixed.
+ *
+ * Buffers (device, caller-owned, fp32):
+ *   ctx_weight, label_weight [B, max_nodes] (a node's weight as a context and
+ *   as the label of its parent context), root_weight [B], log_pK [B, L],
+ *   lp_target [B, max_nodes, L*codebook], root_target [B, L*codebook]:
+ *     the batch, written by atspeed_align_data and read by atspeed_align_step;
+ *   master, adam_m, adam_v, grad [L*codebook, d_model of the draft]: the head's
+ *     fp32 master copy (the caller initialises it to the head's values), the
+ *     AdamW moments (zero before step 1) and the last step's gradient dL/dW.
+ *   hidden_out (nullable) [B * (1 + max_nodes), d_model of the draft]: the
+ *     final-normed hidden states the gradient used, roots at rows [0, B), each
+ *     context at row B + its tree slot (other rows untouched). */
+typedef struct {
+  int32_t mode;          /* 0: AtSpeed-S, 1: AtSpeed-R                              */
+  float alpha;           /* alignment strength in [0, 1] (1: L_Align alone)         */
+  float* ctx_weight;
+  float* label_weight;
+  float* root_weight;
+  float* log_pK;
+  float* lp_target;
+  float* root_target;
+  float* master;
+  float* adam_m;
+  float* adam_v;
+  float* grad;
+  float* hidden_out;
+  float lr, beta1, beta2, eps, weight_decay;  /* AdamW (decoupled decay: w -= lr wd w) */
+  int32_t step;          /* 1-based step number (bias correction)                   */
+} atspeed_align_args;
+
+/* Builds the context tree of the prefilled batch from items_dev [B, S, L] int32
+ * codes (each user's sequences, a whole item last), lens_dev [B, S] (nullable:
+ * every length L) and n_items_dev [B] (1..S) into the context's tree, level
+ * ordered, leaves of depth L included (read it with atspeed_get_tree; every
+ * distinct prefix must fit max_nodes: the K beams of each of the L steps do),
+ * forwards the target over the contexts and writes the batch buffers of args.
+ * Resets every user to t = 0.  ATSPEED_E_INVALID (nothing written but the
+ * tree) if a sequence prefix is not in the catalog, a count or a length is out
+ * of range, a user's last sequence is shorter than L or the prefixes overflow
+ * max_nodes; ATSPEED_E_STATE before prefill or without a draft.  Synchronises
+ * the stream. */
+ATSPEED_API atspeed_status atspeed_align_data(atspeed_ctx* ctx, int32_t S, const int32_t* items_dev,
+                                              const int32_t* lens_dev, const int32_t* n_items_dev,
+                                              const atspeed_align_args* args);
+
+/* One training step on the batch of the last atspeed_align_data: the draft's
+ * forward over the contexts (its prefix caches are the last prefill's), its root
+ * log-probs with the current head, the losses and their gradient, dL/dW of the
+ * item head into args.grad, and one AdamW step on args.master whose result,
+ * rounded to the configured dtype, overwrites the draft's lm_head_item (the
+ * caller's weights).  loss_host (nullable): the loss before the update.  The
+ * draft's log-probs of this step are readable with atspeed_logprobs (model 1).
+ * ATSPEED_E_STATE unless atspeed_align_data ran after the last prefill or
+ * draft.  Synchronises the stream. */
+ATSPEED_API atspeed_status atspeed_align_step(atspeed_ctx* ctx, const atspeed_align_args* args, double* loss_host);
+
+/* State access (host arrays; synchronise the stream)./* State access (host arrays; synchronise the stream).  t [B]; nbeams [B];
  * paths [B, K, L] codes (entries past depth t undefined); scores [B, K] fp32. */
 ATSPEED_API atspeed_status atspeed_get_state(atspeed_ctx* ctx, int32_t B, int32_t* t, int32_t* nbeams,
                                  int32_t* paths, float* scores);

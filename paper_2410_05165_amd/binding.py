@@ -22,7 +22,7 @@ LAYER_ORDER = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up"
 SYMBOLS = ("atspeed_workspace_bytes", "atspeed_create", "atspeed_destroy", "atspeed_last_error",
            "atspeed_prefill", "atspeed_draft", "atspeed_get_tree", "atspeed_verify", "atspeed_tree_logits",
            "atspeed_accept", "atspeed_accept_noalloc", "atspeed_decode_topk", "atspeed_logprobs", "atspeed_get_state", "atspeed_set_state",
-           "atspeed_set_timing", "atspeed_get_timing")
+           "atspeed_set_timing", "atspeed_get_timing", "atspeed_align_data", "atspeed_align_step")
 KERNEL_CLASSES = ("qkv", "o", "gu", "down", "lm_head", "attention", "row", "select")
 
 
@@ -66,6 +66,14 @@ class KernelTimes(C.Structure):
 TIME_TARGET_ONLY = 1 << 16
 
 
+class AlignArgs(C.Structure):
+    _fields_ = [("mode", C.c_int32), ("alpha", C.c_float), ("ctx_weight", C.c_void_p), ("label_weight", C.c_void_p),
+                ("root_weight", C.c_void_p), ("log_pK", C.c_void_p), ("lp_target", C.c_void_p),
+                ("root_target", C.c_void_p), ("master", C.c_void_p), ("adam_m", C.c_void_p), ("adam_v", C.c_void_p),
+                ("grad", C.c_void_p), ("hidden_out", C.c_void_p), ("lr", C.c_float), ("beta1", C.c_float),
+                ("beta2", C.c_float), ("eps", C.c_float), ("weight_decay", C.c_float), ("step", C.c_int32)]
+
+
 class AtspeedError(RuntimeError):
     def __init__(self, status: int, msg: str):
         super().__init__(f"{STATUS.get(status, status)}: {msg}")
@@ -98,6 +106,8 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
                                       C.POINTER(C.c_float)]
     lib.atspeed_set_timing.argtypes = [vp, i32]
     lib.atspeed_get_timing.argtypes = [vp, C.POINTER(KernelTimes)]
+    lib.atspeed_align_data.argtypes = [vp, i32, pi32, pi32, pi32, C.POINTER(AlignArgs)]
+    lib.atspeed_align_step.argtypes = [vp, C.POINTER(AlignArgs), C.POINTER(C.c_double)]
     for name in SYMBOLS:
         fn = getattr(lib, name)
         if fn.restype is C.c_int:  # default
@@ -148,7 +158,9 @@ class Engine:
         self.cfg = cfg
         self._keep = []
         self.tw = self._upload(target_w, w.target.n_layers)
+        self.target_dev = self._keep[-2]
         self.dw = self._upload(draft_w, w.draft.n_layers) if draft_w is not None else None
+        self.draft_dev = self._keep[-2] if draft_w is not None else None   # device tensors of the draft
         cat = np.ascontiguousarray(catalog, dtype=np.int32)
         self._cat_arr = cat
         self.cat = Catalog(cat.shape[0], _np_ptr(cat, C.c_int32))
@@ -235,6 +247,16 @@ class Engine:
 
     def atspeed_logprobs(self, model, lp, root):
         self._check(self.lib.atspeed_logprobs(self.ctx, model, _ptr(lp), _ptr(root)))
+
+    def atspeed_align_data(self, items, lens, n_items, args: AlignArgs):
+        """items [B, S, L] int32, lens [B, S] int32 or None, n_items [B] int32 (device)."""
+        self._check(self.lib.atspeed_align_data(self.ctx, items.shape[1], _ptr(items), _ptr(lens), _ptr(n_items),
+                                                C.byref(args)))
+
+    def atspeed_align_step(self, args: AlignArgs) -> float:
+        loss = C.c_double(0.0)
+        self._check(self.lib.atspeed_align_step(self.ctx, C.byref(args), C.byref(loss)))
+        return loss.value
 
     def atspeed_get_state(self, B: int):
         K, L = self.w.K, self.w.L

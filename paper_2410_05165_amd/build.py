@@ -8,7 +8,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libatspeed.so")
-SOURCES = ["runtime.hip", "gemm.hip", "attention.hip", "misc.hip", "select.hip", "relaxed.hip"]
+SOURCES = ["runtime.hip", "gemm.hip", "attention.hip", "misc.hip", "select.hip", "relaxed.hip", "align.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

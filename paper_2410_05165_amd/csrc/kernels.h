@@ -2,6 +2,7 @@
 #pragma once
 #include <hip/hip_runtime.h>
 #include "common.h"
+#include "select.h"
 
 namespace atspeed {
 
@@ -48,5 +49,34 @@ hipError_t rmsnorm(bool bf16, float* x, const float* add, const int* Mdev, int M
                    const int* row_index, hipStream_t st);
 hipError_t log_softmax_rows(const float* logits, const int* Mdev, int Mmax, int n, const int* dst_index,
                             float* lp, float* logits_copy, hipStream_t st);
+
+// Draft alignment (AtSpeed-S / AtSpeed-R training of the draft's item head).
+struct AlignRows {
+  const int* Mdev;           // [1] context rows of the draft forward
+  const int* user;           // [Mmax] user of each row
+  const int* slot;           // [Mmax] tree slot (u * max_nodes + s) of each row
+  const float* lq;           // draft log-probs by slot [B * max_nodes, nitem]
+  const float* lq_root;      // [B, nitem]
+  const float* lp;           // target log-probs by slot
+  const float* lp_root;
+  const float* ctx_weight;   // [B * max_nodes] weight of each node as a context
+  const float* label_weight; // [B * max_nodes] weight of each node as its parent's label
+  const float* root_weight;  // [B]
+  const float* log_pK;       // [B, L]
+};
+void launch_align_tree(const int* items, const int* lens, const int* n_items, int S, const TreeDev& tr,
+                       const TrieDev& trie, int B, int L, int item_base, int codebook, float* ctx_weight,
+                       float* label_weight, float* root_weight, int* kslot, int* err, hipStream_t st);
+void launch_align_logpk(const int* items, const int* n_items, const int* kslot, const float* lp, const float* root,
+                        int B, int S, int L, int codebook, int nitem, float* log_pK, hipStream_t st);
+void launch_align_grad(const AlignRows& ar, const TrieDev& trie, const TreeDev& tr, int B, int M, int nitem,
+                       int codebook, int L, int K, int mode, float alpha, float* dz, float* loss_rows,
+                       hipStream_t st);
+void launch_head_grad(bool bf16, const float* dz, const void* h_root, const void* h_rows, const int* Mdev, int B,
+                      int nitem, int d, float* dW, hipStream_t st);
+void launch_align_hidden(bool bf16, const void* h_root, const void* h_rows, const int* slot, const int* Mdev, int B,
+                         int M, int d, float* out, hipStream_t st);
+void launch_adamw(bool bf16, float* master, float* m, float* v, const float* g, void* head, size_t n, float lr,
+                  float b1, float b2, float eps, float wd, int step, hipStream_t st);
 
 }  // namespace atspeed

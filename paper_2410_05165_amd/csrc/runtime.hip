@@ -133,6 +133,11 @@ struct atspeed_ctx {
   // device address of the static scratch of atspeed_accept_noalloc on the
   // context's device (taken at create)
   unsigned char* static_scratch = nullptr;
+  // draft alignment
+  void* root_h = nullptr;          // [B, d_draft] the draft's final-normed hidden state at each user's root
+  int* align_kslot = nullptr;      // [B, L] slot of the last training sequence's depth-t prefix
+  float* loss_rows = nullptr;      // [Mmax] weighted loss of each context row
+  bool align_ready = false;        // the tree holds the contexts of the last atspeed_align_data
   uint32_t* prev_tpath = nullptr;  // [B*Tmax] path keys of the last verify's tree
   int* prev_depth = nullptr;       // [B*Tmax]
   int* prev_n = nullptr;           // [B] its forwarded (or carried) nodes: slots [0, prev_n)
@@ -420,6 +425,9 @@ void layout(atspeed_ctx& c, const atspeed_config& cfg, int trie_nodes, Arena& a)
   c.relax.zq = a.take<float>((size_t)B * (L + 1));
   c.relax.slot_node = a.take<int>((size_t)B * (L + 1) * K);
   c.relax.keys = c.keys;
+  c.root_h = a.take<char>((size_t)B * std::max(cfg.draft.d_model, 1) * es);
+  c.align_kslot = a.take<int>((size_t)B * L);
+  c.loss_rows = a.take<float>(M);
 }
 
 atspeed_status bind_weights(ModelRt& r, const atspeed_weights* w, const char* who) {
@@ -549,6 +557,9 @@ atspeed_status forward(atspeed_ctx& c, ModelRt& r, bool prefill, int Mmax, int T
   if (prefill) HIP_TRY(log_softmax_rows(c.logits, c.Mb, B, c.nitem, nullptr, r.root, dbg, st));
   else HIP_TRY(log_softmax_rows(c.logits, c.rows.M, Mmax, c.nitem, c.rows.slot, r.lp, dbg, st));
   MARK(-1);
+  // the draft's root hidden states, for recomputing its root log-probs when its
+  // item head is trained (atspeed_align_step)
+  if (prefill && &r == &c.dft) HIP_TRY(hipMemcpyAsync(c.root_h, c.xn, (size_t)B * d * es, hipMemcpyDeviceToDevice, st));
   return ATSPEED_OK;
 }
 
@@ -755,6 +766,7 @@ atspeed_status atspeed_prefill(atspeed_ctx* c, int32_t B, int32_t P, const int32
   c->prefilled = true;
   c->drafted = false;
   c->carry_ok = false;
+  c->align_ready = false;
   return ATSPEED_OK;
 }
 
@@ -776,6 +788,7 @@ atspeed_status atspeed_draft(atspeed_ctx* c) {
   // paper's relaxed draft keep at most N; the exact relaxed draft keeps the
   // distinct winners of K draws, and N >= K).  The bounds size the launches and
   // choose the GEMM tiles, so they are kept tight.
+  c->align_ready = false;  // the tree is rebuilt below
   const int path_rows = std::max(1, cf.K * (L - 1)), level_rows = std::max(1, cf.N);
   ST_TRY(forward(*c, c->dft, false, B * path_rows, path_rows, nullptr));
   launch_draft_beam_scores(c->state, c->tree, c->dft.lp, c->dft.root, c->nitem, cf.codebook, L, B, c->st);
@@ -1047,6 +1060,109 @@ atspeed_status atspeed_decode_topk(atspeed_ctx* c, int32_t B, int32_t P, const i
   HIP_TRY(hipMemcpyAsync(scores, sc.data(), sc.size() * 4, hipMemcpyHostToDevice, c->st));
   HIP_TRY(hipMemcpyAsync(n_items, nb.data(), B * 4, hipMemcpyHostToDevice, c->st));
   HIP_TRY(hipStreamSynchronize(c->st));
+  return ATSPEED_OK;
+}
+
+atspeed_status atspeed_align_data(atspeed_ctx* c, int32_t S, const int32_t* items, const int32_t* lens,
+                                  const int32_t* n_items, const atspeed_align_args* a) {
+  if (!c || !items || !n_items || !a) return fail(ATSPEED_E_INVALID, "null argument");
+  if (!a->ctx_weight || !a->label_weight || !a->root_weight || !a->log_pK || !a->lp_target || !a->root_target)
+    return fail(ATSPEED_E_INVALID, "align_data: null batch buffer");
+  if (S < 1) return fail(ATSPEED_E_SHAPE, "align_data: S must be positive");
+  if (!c->prefilled) return fail(ATSPEED_E_STATE, "align_data before prefill");
+  if (!c->dft.present) return fail(ATSPEED_E_STATE, "context has no draft model");
+  const atspeed_config& cf = c->cfg;
+  const int B = c->B, L = cf.L;
+  c->align_ready = false;
+  c->drafted = false;
+  // every user back at t = 0 with the empty beam (the tree carries no beams)
+  std::vector<int> ones(B, 1);
+  HIP_TRY(hipMemsetAsync(c->state.t, 0, sizeof(int) * B, c->st));
+  HIP_TRY(hipMemcpyAsync(c->state.nb, ones.data(), B * 4, hipMemcpyHostToDevice, c->st));
+  HIP_TRY(hipMemsetAsync(c->err, 0, sizeof(int), c->st));
+  launch_align_tree(items, lens, n_items, S, c->tree, c->trie, B, L, cf.target.item_base, cf.codebook, a->ctx_weight,
+                    a->label_weight, a->root_weight, c->align_kslot, c->err, c->st);
+  HIP_TRY(hipGetLastError());
+  int err = 0;
+  ST_TRY(read_err(*c, &err));   // synchronises: the host vector above is consumed
+  if (err)
+    return fail(ATSPEED_E_INVALID, "align_data: a count outside 1..S, a length outside 1..L, a last sequence "
+                                   "shorter than L, a prefix outside the catalog, or more prefixes than max_nodes");
+  // the target over every context (validated again by the tree walk of the forward)
+  ST_TRY(tree_forward(*c, nullptr));
+  const size_t row = (size_t)c->nitem * sizeof(float);
+  HIP_TRY(hipMemcpyAsync(a->lp_target, c->tgt.lp, (size_t)B * c->Tmax * row, hipMemcpyDeviceToDevice, c->st));
+  HIP_TRY(hipMemcpyAsync(a->root_target, c->tgt.root, (size_t)B * row, hipMemcpyDeviceToDevice, c->st));
+  launch_align_logpk(items, n_items, c->align_kslot, a->lp_target, a->root_target, B, S, L, cf.codebook, c->nitem,
+                     a->log_pK, c->st);
+  HIP_TRY(hipGetLastError());
+  HIP_TRY(hipStreamSynchronize(c->st));
+  c->align_ready = true;
+  return ATSPEED_OK;
+}
+
+atspeed_status atspeed_align_step(atspeed_ctx* c, const atspeed_align_args* a, double* loss) {
+  if (!c || !a) return fail(ATSPEED_E_INVALID, "null argument");
+  if (!a->ctx_weight || !a->label_weight || !a->root_weight || !a->log_pK || !a->lp_target || !a->root_target ||
+      !a->master || !a->adam_m || !a->adam_v || !a->grad)
+    return fail(ATSPEED_E_INVALID, "align_step: null buffer");
+  if (a->mode != 0 && a->mode != 1) return fail(ATSPEED_E_INVALID, "align_step: mode must be 0 (S) or 1 (R)");
+  if (!(a->alpha >= 0.f && a->alpha <= 1.f)) return fail(ATSPEED_E_INVALID, "align_step: alpha outside [0, 1]");
+  if (a->step < 1) return fail(ATSPEED_E_INVALID, "align_step: step counts from 1");
+  if (!(a->lr >= 0.f) || !(a->beta1 >= 0.f && a->beta1 < 1.f) || !(a->beta2 >= 0.f && a->beta2 < 1.f) ||
+      !(a->eps > 0.f) || !(a->weight_decay >= 0.f))
+    return fail(ATSPEED_E_INVALID, "align_step: optimizer hyper-parameter out of range");
+  if (!c->align_ready) return fail(ATSPEED_E_STATE, "align_step needs atspeed_align_data after the last prefill or draft");
+  const atspeed_config& cf = c->cfg;
+  ModelRt& r = c->dft;
+  const int B = c->B, L = cf.L, d = r.dims.d_model;
+  // the draft's root log-probs with the current head
+  {
+    GemmCall g{};
+    g.kind = GEMM_STORE; g.bf16 = c->bf16; g.A = c->root_h; g.lda = d; g.Mmax = B; g.Mdev = c->Mb;
+    g.N = c->nitem; g.K = d; g.w0 = r.lm_head; g.out = c->logits; g.ldo = c->nitem; g.scratch = c->scratch;
+    HIP_TRY(gemm(g, c->st));
+    HIP_TRY(log_softmax_rows(c->logits, c->Mb, B, c->nitem, nullptr, r.root, nullptr, c->st));
+  }
+  // the context rows: every tree node of depth < L (the leaves of depth L are
+  // labels only)
+  HIP_TRY(hipMemsetAsync(c->err, 0, sizeof(int), c->st));
+  HIP_TRY(hipMemsetAsync(c->lo, 0, sizeof(int) * B, c->st));
+  launch_tree_index(c->tree, c->trie, c->state, B, cf.target.item_base, cf.codebook, L, c->err, c->st);
+  HIP_TRY(hipGetLastError());
+  launch_plan_tree(c->tree, c->lo, c->state.nfwd, B, c->P, c->rows, c->plan_max, c->st);
+  HIP_TRY(hipGetLastError());
+  int info[3] = {0, 0, 0};
+  HIP_TRY(hipMemcpyAsync(&info[0], c->err, sizeof(int), hipMemcpyDeviceToHost, c->st));
+  HIP_TRY(hipMemcpyAsync(&info[1], c->rows.M, sizeof(int), hipMemcpyDeviceToHost, c->st));
+  HIP_TRY(hipMemcpyAsync(&info[2], c->plan_max, sizeof(int), hipMemcpyDeviceToHost, c->st));
+  HIP_TRY(hipStreamSynchronize(c->st));
+  if (info[0]) return fail(ATSPEED_E_INVALID, "align_step: the context tree is malformed (code " + std::to_string(info[0]) + ")");
+  const int M = info[1];
+  if (B + M > c->Mmax) return fail(ATSPEED_E_SHAPE, "align_step: more context rows than the forward holds");
+  if (M > 0) ST_TRY(forward(*c, r, false, M, info[2], nullptr));   // hidden rows in c->xn, log-probs by slot
+  AlignRows ar{c->rows.M, c->rows.user, c->rows.slot, r.lp, r.root, a->lp_target, a->root_target, a->ctx_weight,
+               a->label_weight, a->root_weight, a->log_pK};
+  launch_align_grad(ar, c->trie, c->tree, B, M, c->nitem, cf.codebook, L, cf.K, a->mode, a->alpha, c->logits,
+                    c->loss_rows, c->st);
+  HIP_TRY(hipGetLastError());
+  launch_head_grad(c->bf16, c->logits, c->root_h, c->xn, c->rows.M, B, c->nitem, d, a->grad, c->st);
+  HIP_TRY(hipGetLastError());
+  if (a->hidden_out) {
+    launch_align_hidden(c->bf16, c->root_h, c->xn, c->rows.slot, c->rows.M, B, M, d, a->hidden_out, c->st);
+    HIP_TRY(hipGetLastError());
+  }
+  launch_adamw(c->bf16, a->master, a->adam_m, a->adam_v, a->grad, const_cast<void*>(r.lm_head), (size_t)c->nitem * d,
+               a->lr, a->beta1, a->beta2, a->eps, a->weight_decay, a->step, c->st);
+  HIP_TRY(hipGetLastError());
+  std::vector<float> lr((size_t)B + M);
+  HIP_TRY(hipMemcpyAsync(lr.data(), c->loss_rows, lr.size() * 4, hipMemcpyDeviceToHost, c->st));
+  HIP_TRY(hipStreamSynchronize(c->st));
+  if (loss) {
+    double sum = 0.0;
+    for (float v : lr) sum += v;
+    *loss = sum;
+  }
   return ATSPEED_OK;
 }
 

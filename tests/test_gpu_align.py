@@ -1,0 +1,259 @@
+"""Draft alignment on the GPU (AtSpeed-S, Sec. 3.1; AtSpeed-R, Sec. 3.2) against
+the oracle, on the small workload (16 users, K = 20, a 2-layer bf16 draft).
+
+The batch is every user's K target lists (a strict decode, lossless: the
+target's own top-K, i.e. D' with lambda = 1); the contexts are the users' roots
+and the distinct prefixes of depth 1..L-1 of those lists.
+
+* atspeed_align_data: the context tree holds exactly those prefixes, level
+  ordered, each node's parent its own prefix; node and root weights equal the
+  oracle's dataset weights; log p_K is the target's log-prob of the K-th list's
+  code at its own prefix, read from the same target rows; the target rows equal
+  the oracle target's log-probs at those contexts (bf16 logit bar, doubled for
+  the log-normaliser).
+* atspeed_align_step: the loss and the item-head gradient equal the oracle's
+  on the GPU's own draft and target log-probs and hidden states; the hidden
+  rows reproduce the draft's log-probs through the head (so each row sits at
+  its context's slot); the AdamW update equals the oracle's on the GPU's
+  gradient; the head the draft reads is the master copy rounded to bf16, bit
+  for bit.
+* training: the loss falls, the decoded lists stay the target's (strict
+  verification is lossless whatever the draft), and acceptance rises.
+"""
+import ctypes as C
+
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+from _gpu_common import LOGIT_TOL, env, oracle_user, upload_tree  # noqa: E402
+from oracle.align import adamw_step, aligned_loss, head_gradient  # noqa: E402
+from oracle.model import item_log_softmax  # noqa: E402
+from oracle.numerics import round_bf16  # noqa: E402
+
+DEV = "cuda:0"
+
+
+def _decode(eng, w, prefix):
+    from paper_2410_05165_amd.binding import Stats
+    B = prefix.shape[0]
+    items = torch.zeros((B, w.K, w.L), dtype=torch.int32, device=DEV)
+    scores = torch.zeros((B, w.K), dtype=torch.float32, device=DEV)
+    n = torch.zeros(B, dtype=torch.int32, device=DEV)
+    acc = np.full((w.L, B), -9, np.int32)
+    st = Stats()
+    st.accepted = acc.ctypes.data_as(C.POINTER(C.c_int32))
+    eng.atspeed_decode_topk(prefix, items, scores, n, st)
+    torch.cuda.synchronize()
+    return items, n, acc[:st.n_steps].copy()
+
+
+def _mean_accepted(acc):
+    a = acc[acc >= 0]
+    return float(a.mean()) if a.size else 0.0
+
+
+def _level_beams(eng, w, prefix):
+    """Multi-step data: the target's K beams of every beam-search step (GPU
+    target-only beam search: verifies of trees holding only the Y_t paths), as
+    items [B, K*L, L], lens, n; levels in order, so a whole item comes last."""
+    B, K, L = prefix.shape[0], w.K, w.L
+    eng.atspeed_prefill(prefix)
+    levels = []
+    for _ in range(L):
+        t, nb, paths, _ = eng.atspeed_get_state(B)
+        trees = [[tuple(int(c) for c in paths[u, k, :t[u]]) for k in range(nb[u])] if t[u] > 0 else []
+                 for u in range(B)]
+        upload_tree(eng, trees, B)
+        eng.atspeed_verify()
+        levels.append(eng.atspeed_get_state(B))
+    items = np.zeros((B, K * L, L), np.int32)
+    lens = np.zeros((B, K * L), np.int32)
+    n = np.zeros(B, np.int32)
+    for u in range(B):
+        for t_, nb, paths, _ in levels:
+            for k in range(nb[u]):
+                items[u, n[u], :t_[u]] = paths[u, k, :t_[u]]
+                lens[u, n[u]] = t_[u]
+                n[u] += 1
+    return tuple(torch.from_numpy(a).to(DEV) for a in (items, lens, n))
+
+
+def _setup(mode, multistep=False, **hp):
+    from paper_2410_05165_amd.align import AlignTrainer
+    from paper_2410_05165_amd.binding import Engine
+    e = env("small")
+    w = e["w"]
+    eng = Engine(w, e["tw"], e["dw"], e["cat"])
+    prefix = torch.from_numpy(e["pre"]).to(DEV)
+    print(f"[align {mode}] strict decode for the target lists", flush=True)
+    items, n, acc = _decode(eng, w, prefix)
+    decoded = (items, n)
+    lens = None
+    if multistep:
+        items_l, lens, n_l = _level_beams(eng, w, prefix)
+        # the last step's beams are the decoded lists
+        whole, ms = _lists((items, None, n)), _lists((items_l, lens, n_l))
+        assert all(ms[u][len(ms[u]) - len(whole[u]):] == whole[u] for u in range(len(whole)))
+        items, n = items_l, n_l
+    eng.atspeed_prefill(prefix)
+    tr = AlignTrainer(eng, mode, **hp)
+    tr.data(items, n, lens)
+    torch.cuda.synchronize()
+    return e, eng, prefix, tr, (items, lens, n), acc, decoded
+
+
+def _contexts(eng, B):
+    """Per user: {path: slot} of the context tree (paths rebuilt through the parents)."""
+    w = eng.w
+    tn, tt, tp, td, _ = (x.cpu().numpy() for x in eng.tree_tensors(B))
+    out = []
+    for u in range(B):
+        paths = []
+        for i in range(tn[u]):
+            code = tt[u, i] - w.target.item_base - w.codebook * (td[u, i] - 1)
+            paths.append((paths[tp[u, i]] if tp[u, i] >= 0 else ()) + (int(code),))
+        out.append(paths)
+    return out, td, tn
+
+
+def _lists(data):
+    items, lens, n = data
+    it, nn = items.cpu().numpy(), n.cpu().numpy()
+    ln = lens.cpu().numpy() if lens is not None else np.full(it.shape[:2], it.shape[2])
+    return [[tuple(int(c) for c in it[u, k, :ln[u, k]]) for k in range(nn[u])] for u in range(len(nn))]
+
+
+@pytest.mark.parametrize("multistep", [False, True], ids=["last_step", "multi_step"])
+def test_align_data_small(multistep):
+    e, eng, prefix, tr, data, _, _ = _setup("S", multistep)
+    try:
+        w = e["w"]
+        B, T, L, cb, nit = w.batch, eng.max_nodes, w.L, w.codebook, eng.n_item
+        Y = _lists(data)
+        paths, depth, nn = _contexts(eng, B)
+        cw = tr.ctx_weight.view(B, T).cpu().numpy()
+        lw = tr.label_weight.view(B, T).cpu().numpy()
+        rw = tr.root_weight.cpu().numpy()
+        lpk = tr.log_pK.view(B, L).cpu().numpy()
+        LPT = tr.lp_target.view(B, T, nit).cpu().numpy()
+        RT = tr.root_target.view(B, nit).cpu().numpy()
+        from oracle.align import context_weights, label_distributions
+        W = context_weights(Y, L)
+        for u in range(B):
+            want = {y[:t] for y in Y[u] for t in range(1, len(y) + 1)}
+            got = paths[u]
+            assert len(got) == len(set(got)) == len(want) and set(got) == want, u
+            assert all(depth[u, i] <= depth[u, i + 1] for i in range(nn[u] - 1)), u
+            pis = label_distributions(Y[u], cb)
+            for i, p in enumerate(got):
+                assert cw[u, i] == pytest.approx(W[u].get(p, 0.0), rel=1e-6, abs=1e-9), (u, p)
+                parent_w = W[u][p[:-1]]
+                assert lw[u, i] == pytest.approx(parent_w * pis[p[:-1]][cb * (len(p) - 1) + p[-1]], rel=1e-5), (u, p)
+            assert rw[u] == pytest.approx(W[u][()], rel=1e-6), u
+            yk = Y[u][-1]
+            slot = {p: i for i, p in enumerate(got)}
+            for t in range(L):
+                row = RT[u] if t == 0 else LPT[u, slot[yk[:t]]]
+                assert lpk[u, t] == row[cb * t + yk[t]], (u, t)
+        if multistep:
+            return
+        bar = 2 * LOGIT_TOL[w.dtype]
+        for u in (0, 7):
+            o = oracle_user("small", u)
+            ctx = [()] + [p for p in paths[u] if len(p) == 1][:2] + [p for p in paths[u] if len(p) == 3][:2]
+            want = o["lp"](ctx)
+            for p, row in zip(ctx, want):
+                got = RT[u] if p == () else LPT[u, paths[u].index(p)]
+                err = np.abs(got - row).max()
+                print(f"[align data] user {u} context {p}: target log-prob max|err| = {err:.3e}")
+                assert err <= bar
+    finally:
+        eng.close()
+
+
+@pytest.mark.parametrize("mode,alpha,multistep", [("S", 1.0, False), ("R", 1.0, False), ("S", 0.5, False),
+                                                  ("S", 0.5, True), ("R", 0.5, True)])
+def test_align_step_matches_oracle(mode, alpha, multistep):
+    hp = dict(alpha=alpha, lr=2e-3, betas=(0.9, 0.99), eps=1e-8, weight_decay=0.01)
+    e, eng, prefix, tr, data, _, _ = _setup(mode, multistep, **hp)
+    try:
+        w = e["w"]
+        B, T, L, cb, nit, K = w.batch, eng.max_nodes, w.L, w.codebook, eng.n_item, w.K
+        d = w.draft.d_model
+        head0 = tr.head.float().cpu().numpy().astype(np.float64)
+        master0 = tr.master.cpu().numpy().astype(np.float64).reshape(nit, d)
+        hidden = torch.full((B * (1 + T), d), float("nan"), dtype=torch.float32, device=DEV)
+        loss = tr.step(hidden_out=hidden)
+        dl = torch.empty((B, T, nit), dtype=torch.float32, device=DEV)
+        dr = torch.empty((B, nit), dtype=torch.float32, device=DEV)
+        eng.atspeed_logprobs(1, dl, dr)
+        DL, DR = dl.cpu().numpy().astype(np.float64), dr.cpu().numpy().astype(np.float64)
+        LPT = tr.lp_target.view(B, T, nit).cpu().numpy().astype(np.float64)
+        RT = tr.root_target.view(B, nit).cpu().numpy().astype(np.float64)
+        H = hidden.cpu().numpy().astype(np.float64)
+        G = tr.grad.view(nit, d).cpu().numpy().astype(np.float64)
+        master = tr.master.view(nit, d).cpu().numpy().astype(np.float64)
+        head = tr.head.float().cpu().numpy().astype(np.float64)
+        paths, _, _ = _contexts(eng, B)
+        slot = [{p: i for i, p in enumerate(ps)} for ps in paths]
+        Y = _lists(data)
+
+        def lq_of(u, p):
+            return DR[u] if p == () else DL[u, slot[u][p]]
+
+        def lp_of(u, p):
+            return RT[u] if p == () else LPT[u, slot[u][p]]
+
+        def h_of(u, p):
+            return H[u] if p == () else H[B + u * T + slot[u][p]]
+
+        want_loss, grads = aligned_loss(mode, lq_of, lp_of, e["trie"], Y, K, L, cb, alpha)
+        tag = f"[align {mode} alpha {alpha}{' multi-step' if multistep else ''}]"
+        print(f"{tag} loss GPU {loss:.8f} oracle {want_loss:.8f}; {len(grads)} contexts", flush=True)
+        assert abs(loss - want_loss) <= 1e-5 * abs(want_loss) + 1e-7
+        hid = {k: h_of(*k) for k in grads}
+        want_G = head_gradient(grads, hid)
+        scale = np.abs(want_G).max()
+        err = np.abs(G - want_G).max()
+        print(f"{tag} head gradient max|err| = {err:.3e} (max|dW| {scale:.3e})")
+        assert scale > 0 and err <= 1e-4 * scale
+        # the hidden rows are the contexts' own: through the head they give the draft's log-probs
+        worst = 0.0
+        for (u, p), h in list(hid.items())[::7]:
+            lq = item_log_softmax(head0 @ h)
+            worst = max(worst, np.abs(lq - lq_of(u, p)).max())
+        print(f"{tag} log_softmax(head h) vs draft log-probs max|err| = {worst:.3e}")
+        assert worst <= 1e-3
+        # AdamW on the GPU's gradient, then the bf16 head
+        want_w, _, _ = adamw_step(master0, 0.0, 0.0, G, 1, hp["lr"], hp["betas"][0], hp["betas"][1], hp["eps"],
+                                  hp["weight_decay"])
+        np.testing.assert_allclose(master, want_w, rtol=1e-6, atol=1e-6 * hp["lr"])
+        assert np.array_equal(head, round_bf16(master))
+        assert not np.array_equal(head, head0)
+    finally:
+        eng.close()
+
+
+@pytest.mark.parametrize("mode", ["S", "R"])
+def test_align_training_small(mode):
+    from paper_2410_05165_amd.align import cosine_lr
+    steps, peak = 200, 1e-2
+    e, eng, prefix, tr, data, acc0, (items0, n0) = _setup(mode, True, alpha=0.5, lr=peak, weight_decay=0.01)
+    try:
+        w = e["w"]
+        losses = []
+        for s in range(1, steps + 1):
+            losses.append(tr.step(lr=cosine_lr(s, steps, peak, 10)))
+        print(f"[align {mode}] loss {losses[0]:.5f} -> {losses[steps // 2]:.5f} -> {losses[-1]:.5f}")
+        assert losses[-1] < losses[0]
+        items1, n1, acc1 = _decode(eng, w, prefix)
+        assert torch.equal(items0, items1) and torch.equal(n0, n1)   # lossless whatever the draft
+        m0, m1 = _mean_accepted(acc0), _mean_accepted(acc1)
+        print(f"[align {mode}] strict decode: mean accepted levels per step {m0:.3f} -> {m1:.3f}; "
+              f"steps {acc0.shape[0]} -> {acc1.shape[0]}")
+    finally:
+        eng.close()
