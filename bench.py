@@ -13,9 +13,11 @@ acceptance) until every user's top-K list is complete, with the library's own
 drafts (natural acceptance; random weights accept about nothing).  value =
 users x steps / time.  Beside it: the same decode with the level-1 start and
 tree-KV reuse, under the replay-paper-AS and replay-all-accept profiles, the
-t = 0 verify step alone, the decode-bound probe and the relaxed (config-4)
-decode; the roofline kernel is the target's gate/up GEMM over the timed
-decodes.
+t = 0 verify step alone, the decode-bound probe, the relaxed (config-4)
+decode, and the strict and relaxed decodes after draft alignment (AtSpeed-S /
+AtSpeed-R training of the draft's item head on the benchmark users, measured on
+them and on held-out users); the roofline kernel is the target's gate/up GEMM
+over the timed decodes.
 
 Prints ONE JSON line.  Progress goes to stderr.
 """
@@ -398,6 +400,86 @@ def relaxed_line(w, tw, dw, cat, pre, dev, steps, warmup):
     return res
 
 
+def multistep_data(levels, K, L, dev):
+    """The target's K beams of every beam-search step (GPU target-only beam
+    search), per user in level order: items [B, K*L, L], lens [B, K*L], n [B]."""
+    import numpy as np
+    import torch
+    B = len(levels[0][0])
+    items = np.zeros((B, K * L, L), np.int32)
+    lens = np.zeros((B, K * L), np.int32)
+    n = np.zeros(B, np.int32)
+    for u in range(B):
+        for t, nb, paths, _ in levels:
+            for k in range(nb[u]):
+                items[u, n[u], :t[u]] = paths[u, k, :t[u]]
+                lens[u, n[u]] = t[u]
+                n[u] += 1
+    return tuple(torch.from_numpy(a).to(dev) for a in (items, lens, n))
+
+
+def aligned_line(w, tw, dw, cat, pre, dev, steps, warmup, ref_lists=None, train_steps=300, alpha=0.5, peak_lr=1e-2):
+    """Draft alignment, then natural decodes: AtSpeed-S for strict verification,
+    AtSpeed-R for relaxed, on the multi-step data of the benchmark users (the
+    target's K beams of every step), alpha 0.5, AdamW with a cosine schedule.
+    The decodes run the aligned draft on the same users (in-sample) and on as
+    many held-out users (same catalog and prompt, their own histories)."""
+    import numpy as np
+    import torch
+    from paper_2410_05165_amd.align import AlignTrainer, cosine_lr
+    from paper_2410_05165_amd.binding import Engine
+    from synth import make_prefixes, philox_key
+    B, K, L = w.batch, w.K, w.L
+    strict = w.mode == "strict"
+    ws = w if strict else w.with_(mode="strict")
+    prefix = torch.from_numpy(pre).to(dev)
+    seng = Engine(ws, tw, dw, cat)
+    levels = gpu_target_beam_search(seng, ws, prefix, upload_tree)
+    items, lens, n = multistep_data(levels, K, L, dev)
+    if strict:
+        eng = seng
+    else:
+        seng.close()
+        key = [int(x) for x in philox_key(w)]
+        eng = Engine(w, tw, dw, cat, mode={"relaxed_exact": 1, "relaxed_paper": 2}[w.mode],
+                     seed=key[0] | (key[1] << 32))
+    held = torch.from_numpy(np.ascontiguousarray(make_prefixes(w.with_(batch=2 * B), cat)[B:])).to(dev)
+    before_held, _, _, _ = timed_decodes(eng, w, held, 1, 0, roofline=False)
+    eng.atspeed_prefill(prefix)
+    tr = AlignTrainer(eng, "S" if strict else "R", alpha=alpha, lr=peak_lr, weight_decay=0.01)
+    tr.data(items, n, lens)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    losses = [tr.step(lr=cosine_lr(s, train_steps, peak_lr, 20)) for s in range(1, train_steps + 1)]
+    torch.cuda.synchronize()
+    ms_train = 1e3 * (time.perf_counter() - t0) / train_steps
+    r_in, out_in, _, _ = timed_decodes(eng, w, prefix, steps, warmup, roofline=False)
+    r_held, out_held, _, _ = timed_decodes(eng, w, held, steps, warmup, roofline=False)
+    eng.close()
+    if ref_lists is not None:
+        assert (out_in[0] == ref_lists).all(), "the aligned draft changed the strict lists"
+
+    def accept(r):
+        a = np.array(r["accepted_levels"])
+        return float(a[a >= 0].mean())
+    res = dict(
+        objective=f"AtSpeed-{'S' if strict else 'R'}: {alpha} L_Align + {1 - alpha} L_Rec (NLL of the training "
+                  f"sequences), multi-step data ({int(n.sum().item())} sequences of the {B} users), draft item head "
+                  f"trained, AdamW lr {peak_lr} cosine, {train_steps} steps",
+        train=dict(ms_per_step=round(ms_train, 3), loss_first=round(losses[0], 4), loss_last=round(losses[-1], 4)),
+        trained_users=dict(lists_per_s=r_in["lists_per_s"], ms_per_decode=r_in["ms_per_decode"], steps=r_in["steps"],
+                           accepted_per_step=accept(r_in), lists_mean=float(out_in[2].mean())),
+        held_out_users=dict(lists_per_s=r_held["lists_per_s"], ms_per_decode=r_held["ms_per_decode"],
+                            steps=r_held["steps"], accepted_per_step=accept(r_held),
+                            accepted_per_step_before=accept(before_held), lists_mean=float(out_held[2].mean())),
+        workload=f"{w.name}: {w.mode} verification, B={B}, K={K}, N={w.N}")
+    log(f"aligned draft ({w.name}, {res['objective'].split(':')[0]}): training {ms_train:.2f} ms/step; trained users "
+        f"{r_in['ms_per_decode']:.1f} ms ({r_in['lists_per_s']:.0f} lists/s, {r_in['steps']} steps, accepted/step "
+        f"{accept(r_in):.2f}); held-out users {r_held['ms_per_decode']:.1f} ms (accepted/step "
+        f"{accept(before_held):.2f} -> {accept(r_held):.2f})")
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -408,7 +490,7 @@ def main():
     ap.add_argument("--no-extras", action="store_true",
                     help="only the headline decode (profiling runs): no other profiles, verify step, probe or relaxed line")
     ap.add_argument("--only", default="",
-                    help="comma list of extra sections to run: schedule,paper_as,all_accept,verify,probe,relaxed")
+                    help="comma list of extra sections to run: schedule,paper_as,all_accept,verify,probe,relaxed,aligned")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one plain device copy of this size (HBM counter calibration)")
     args = ap.parse_args()
@@ -422,7 +504,7 @@ def main():
     from synth import get_workload, make_catalog, make_prefixes, make_weights
     from paper_2410_05165_amd.binding import Engine
 
-    sections = {"schedule", "paper_as", "all_accept", "verify", "probe", "relaxed"}
+    sections = {"schedule", "paper_as", "all_accept", "verify", "probe", "relaxed", "aligned"}
     if args.no_extras:
         sections = set()
     elif args.only:
@@ -578,9 +660,14 @@ def main():
         extras["decode_bound"] = decode_bound_probe(eng, w, prefix, levels, max(3, args.steps // 2))
 
     eng.close()
+    if "aligned" in sections:
+        extras["decode_aligned"] = aligned_line(w, tw, dw, cat, pre, dev, args.steps, args.warmup,
+                                                ref_lists=out0[0] if mode == 0 else None)
     if "relaxed" in sections and w.name == "b7":
         wr = get_workload("b7_relaxed")
         extras["relaxed_decode"] = relaxed_line(wr, tw, dw, cat, pre, dev, args.steps, args.warmup)
+        if "aligned" in sections:
+            extras["relaxed_decode_aligned"] = aligned_line(wr, tw, dw, cat, pre, dev, args.steps, args.warmup)
     elif mode != 0 and "relaxed" in sections:
         extras["relaxed_decode"] = relaxed_line(w, tw, dw, cat, pre, dev, args.steps, args.warmup)
 

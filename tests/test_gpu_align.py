@@ -2,8 +2,9 @@
 the oracle, on the small workload (16 users, K = 20, a 2-layer bf16 draft).
 
 The batch is every user's K target lists (a strict decode, lossless: the
-target's own top-K, i.e. D' with lambda = 1); the contexts are the users' roots
-and the distinct prefixes of depth 1..L-1 of those lists.
+target's own top-K, i.e. D' with lambda = 1), or the multi-step data below;
+the contexts are the users' roots and the distinct proper prefixes of those
+sequences.
 
 * atspeed_align_data: the context tree holds exactly those prefixes, level
   ordered, each node's parent its own prefix; node and root weights equal the
@@ -18,7 +19,12 @@ and the distinct prefixes of depth 1..L-1 of those lists.
   gradient; the head the draft reads is the master copy rounded to bf16, bit
   for bit.
 * training: the loss falls, the decoded lists stay the target's (strict
-  verification is lossless whatever the draft), and acceptance rises.
+  verification is lossless whatever the draft), and acceptance rises (strict
+  decoding after AtSpeed-S, relaxed sampling decoding after AtSpeed-R).
+
+Multi-step data (the target's K beams of every beam-search step, which the
+paper compares with last-step data) come from the GPU's target-only beam
+search: verifies of trees that hold only the Y_t paths.
 """
 import ctypes as C
 
@@ -238,22 +244,48 @@ def test_align_step_matches_oracle(mode, alpha, multistep):
         eng.close()
 
 
+def _relaxed_decode(eng, w, prefix):
+    items, n, acc = _decode(eng, w, prefix)
+    return n.float().mean().item(), acc
+
+
 @pytest.mark.parametrize("mode", ["S", "R"])
 def test_align_training_small(mode):
-    from paper_2410_05165_amd.align import cosine_lr
+    """200 AdamW steps on the multi-step data (alpha 0.5).  S: the strict decode's
+    lists stay the target's and the trained users' accepted levels rise.  R: the
+    head is trained on the relaxed engine (its draft), whose sampled decode then
+    accepts more levels per step and yields no fewer lists."""
+    from paper_2410_05165_amd.align import AlignTrainer, cosine_lr
+    from paper_2410_05165_amd.binding import Engine
     steps, peak = 200, 1e-2
     e, eng, prefix, tr, data, acc0, (items0, n0) = _setup(mode, True, alpha=0.5, lr=peak, weight_decay=0.01)
+    w = e["w"]
+    reng = None
     try:
-        w = e["w"]
-        losses = []
-        for s in range(1, steps + 1):
-            losses.append(tr.step(lr=cosine_lr(s, steps, peak, 10)))
+        if mode == "R":
+            reng = Engine(w, e["tw"], e["dw"], e["cat"], mode=2, seed=11)
+            lists0, racc0 = _relaxed_decode(reng, w, prefix)
+            reng.atspeed_prefill(prefix)
+            tr = AlignTrainer(reng, "R", alpha=0.5, lr=peak, weight_decay=0.01)
+            items, lens, n = data
+            tr.data(items, n, lens)
+        losses = [tr.step(lr=cosine_lr(s, steps, peak, 10)) for s in range(1, steps + 1)]
         print(f"[align {mode}] loss {losses[0]:.5f} -> {losses[steps // 2]:.5f} -> {losses[-1]:.5f}")
         assert losses[-1] < losses[0]
-        items1, n1, acc1 = _decode(eng, w, prefix)
-        assert torch.equal(items0, items1) and torch.equal(n0, n1)   # lossless whatever the draft
-        m0, m1 = _mean_accepted(acc0), _mean_accepted(acc1)
-        print(f"[align {mode}] strict decode: mean accepted levels per step {m0:.3f} -> {m1:.3f}; "
-              f"steps {acc0.shape[0]} -> {acc1.shape[0]}")
+        if mode == "S":
+            items1, n1, acc1 = _decode(eng, w, prefix)
+            assert torch.equal(items0, items1) and torch.equal(n0, n1)   # lossless whatever the draft
+            m0, m1 = _mean_accepted(acc0), _mean_accepted(acc1)
+            print(f"[align S] strict decode: accepted levels per step {m0:.3f} -> {m1:.3f}; "
+                  f"steps {acc0.shape[0]} -> {acc1.shape[0]}")
+            assert m1 > m0
+        else:
+            lists1, racc1 = _relaxed_decode(reng, w, prefix)
+            m0, m1 = _mean_accepted(racc0), _mean_accepted(racc1)
+            print(f"[align R] relaxed decode: accepted levels per step {m0:.3f} -> {m1:.3f}; "
+                  f"lists per user {lists0:.2f} -> {lists1:.2f}")
+            assert m1 > m0 and lists1 >= lists0
     finally:
+        if reng is not None:
+            reng.close()
         eng.close()
