@@ -14,10 +14,12 @@ drafts (natural acceptance; random weights accept about nothing).  value =
 users x steps / time.  Beside it: the same decode with the level-1 start and
 tree-KV reuse, under the replay-paper-AS and replay-all-accept profiles, the
 t = 0 verify step alone, the decode-bound probe, the relaxed (config-4)
-decode, and the strict and relaxed decodes after draft alignment (AtSpeed-S /
+decode, the strict and relaxed decodes after draft alignment (AtSpeed-S /
 AtSpeed-R training of the draft's item head on the benchmark users, measured on
-them and on held-out users); the roofline kernel is the target's gate/up GEMM
-over the timed decodes.
+them and on held-out users), and the target-only beam search that the paper's
+walltime speedup WS is measured against (with the speedup of each decode, and
+WS at batch sizes 1, 4 and 32 with the random and the aligned draft); the
+roofline kernel is the target's gate/up GEMM over the timed decodes.
 
 Prints ONE JSON line.  Progress goes to stderr.
 """
@@ -400,22 +402,102 @@ def relaxed_line(w, tw, dw, cat, pre, dev, steps, warmup):
     return res
 
 
-def multistep_data(levels, K, L, dev):
-    """The target's K beams of every beam-search step (GPU target-only beam
-    search), per user in level order: items [B, K*L, L], lens [B, K*L], n [B]."""
+def target_search_line(w, tw, cat, pre, dev, steps, warmup):
+    """The paper's walltime-speedup baseline: target-only constrained beam search
+    (atspeed_target_search: target prefill, then one target forward and TopK per
+    level; with tree-KV reuse each level forwards only its new nodes, as a
+    KV-cached beam search does).  Returns its figures and lists."""
     import numpy as np
     import torch
-    B = len(levels[0][0])
-    items = np.zeros((B, K * L, L), np.int32)
-    lens = np.zeros((B, K * L), np.int32)
-    n = np.zeros(B, np.int32)
-    for u in range(B):
-        for t, nb, paths, _ in levels:
-            for k in range(nb[u]):
-                items[u, n[u], :t[u]] = paths[u, k, :t[u]]
-                lens[u, n[u]] = t[u]
-                n[u] += 1
-    return tuple(torch.from_numpy(a).to(dev) for a in (items, lens, n))
+    from paper_2410_05165_amd.binding import Engine
+    B, K, L = w.batch, w.K, w.L
+    prefix = torch.from_numpy(pre).to(dev)
+    res, outs = {}, []
+    for reuse in (1, 0):
+        eng = Engine(w.with_(mode="strict"), tw, None, cat, reuse_tree_kv=reuse)
+        items = torch.zeros((B, K, L), dtype=torch.int32, device=dev)
+        scores = torch.zeros((B, K), dtype=torch.float32, device=dev)
+        n = torch.zeros(B, dtype=torch.int32, device=dev)
+        for _ in range(warmup):
+            eng.atspeed_target_search(prefix, items, scores, n)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            eng.atspeed_target_search(prefix, items, scores, n)
+        torch.cuda.synchronize()
+        ms = 1e3 * (time.perf_counter() - t0) / steps
+        eng.close()
+        outs.append(items.cpu().numpy())
+        res["kv_cached" if reuse else "recompute_paths"] = dict(ms_per_decode=ms, lists_per_s=B / (ms * 1e-3))
+        log(f"target-only beam search ({w.name}, {'earlier levels carried' if reuse else 'paths recomputed'}): "
+            f"{ms:.1f} ms per {B} lists ({B / (ms * 1e-3):.0f} lists/s)")
+    assert (outs[0] == outs[1]).all()
+    return res, outs[0]
+
+
+def ws_by_batch(w, tw, dw, cat, pre, dev, steps, warmup, batches=(1, 4, 32), train_steps=300):
+    """Walltime speedup WS (Sec. 4.1: the target-only beam search's time over the
+    speculative decode's) at several batch sizes, first users of the workload:
+    the KV-cached target-only search (atspeed_target_search with tree-KV reuse),
+    the speculative decode with the random-init draft, and with the draft
+    aligned on those users (AtSpeed-S or -R, multi-step data, alpha 0.5)."""
+    import numpy as np
+    import torch
+    from paper_2410_05165_amd.align import AlignTrainer, cosine_lr
+    from paper_2410_05165_amd.binding import Engine
+    from synth import philox_key
+    K, L = w.K, w.L
+    strict = w.mode == "strict"
+    key = [int(x) for x in philox_key(w)]
+    mode = {"strict": 0, "relaxed_exact": 1, "relaxed_paper": 2}[w.mode]
+    search_eng = Engine(w.with_(mode="strict"), tw, dw, cat, reuse_tree_kv=1)
+    sd_eng = Engine(w, tw, dw, cat, mode=mode, seed=key[0] | (key[1] << 32))
+    head0 = sd_eng.draft_dev["lm_head_item"].clone()
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            fn()
+        torch.cuda.synchronize()
+        return 1e3 * (time.perf_counter() - t0) / steps
+
+    rows = []
+    for B in batches:
+        prefix = torch.from_numpy(np.ascontiguousarray(pre[:B])).to(dev)
+        items = torch.zeros((B, K, L), dtype=torch.int32, device=dev)
+        scores = torch.zeros((B, K), dtype=torch.float32, device=dev)
+        n = torch.zeros(B, dtype=torch.int32, device=dev)
+        si = torch.zeros((B, K * L, L), dtype=torch.int32, device=dev)
+        sl = torch.zeros((B, K * L), dtype=torch.int32, device=dev)
+        sn = torch.zeros(B, dtype=torch.int32, device=dev)
+        ms_search = timed(lambda: search_eng.atspeed_target_search(prefix, items, scores, n))
+        search_eng.atspeed_target_search(prefix, items, scores, n, si, sl, sn)
+        ref = items.clone()
+        sd_eng.draft_dev["lm_head_item"].copy_(head0)
+        ms_sd = timed(lambda: sd_eng.atspeed_decode_topk(prefix, items, scores, n))
+        if strict:
+            assert torch.equal(items, ref), "speculative decode differs from the target-only search"
+        sd_eng.atspeed_prefill(prefix)
+        tr = AlignTrainer(sd_eng, "S" if strict else "R", alpha=0.5, lr=1e-2, weight_decay=0.01)
+        tr.data(si, sn, sl)
+        for s_ in range(1, train_steps + 1):
+            tr.step(lr=cosine_lr(s_, train_steps, 1e-2, 20))
+        ms_al = timed(lambda: sd_eng.atspeed_decode_topk(prefix, items, scores, n))
+        if strict:
+            assert torch.equal(items, ref), "aligned speculative decode differs from the target-only search"
+        r = dict(batch=B, target_search_ms=round(ms_search, 3), sd_random_draft_ms=round(ms_sd, 3),
+                 sd_aligned_in_sample_ms=round(ms_al, 3), ws_random_draft=round(ms_search / ms_sd, 3),
+                 ws_aligned_in_sample=round(ms_search / ms_al, 3))
+        rows.append(r)
+        log(f"WS at B={B} ({w.name}): target search {ms_search:.1f} ms, SD random draft {ms_sd:.1f} ms "
+            f"(WS {ms_search / ms_sd:.2f}), SD aligned in-sample {ms_al:.1f} ms (WS {ms_search / ms_al:.2f})")
+    sd_eng.close()
+    search_eng.close()
+    return dict(rows=rows, what="WS = target-only beam search time / speculative decode time (prefill included "
+                                "in both), first B users; the aligned draft is trained on those users")
 
 
 def aligned_line(w, tw, dw, cat, pre, dev, steps, warmup, ref_lists=None, train_steps=300, alpha=0.5, peak_lr=1e-2):
@@ -434,8 +516,12 @@ def aligned_line(w, tw, dw, cat, pre, dev, steps, warmup, ref_lists=None, train_
     ws = w if strict else w.with_(mode="strict")
     prefix = torch.from_numpy(pre).to(dev)
     seng = Engine(ws, tw, dw, cat)
-    levels = gpu_target_beam_search(seng, ws, prefix, upload_tree)
-    items, lens, n = multistep_data(levels, K, L, dev)
+    lists = (torch.zeros((B, K, L), dtype=torch.int32, device=dev), torch.zeros((B, K), device=dev),
+             torch.zeros(B, dtype=torch.int32, device=dev))
+    items = torch.zeros((B, K * L, L), dtype=torch.int32, device=dev)
+    lens = torch.zeros((B, K * L), dtype=torch.int32, device=dev)
+    n = torch.zeros(B, dtype=torch.int32, device=dev)
+    seng.atspeed_target_search(prefix, *lists, items, lens, n)
     if strict:
         eng = seng
     else:
@@ -490,7 +576,8 @@ def main():
     ap.add_argument("--no-extras", action="store_true",
                     help="only the headline decode (profiling runs): no other profiles, verify step, probe or relaxed line")
     ap.add_argument("--only", default="",
-                    help="comma list of extra sections to run: schedule,paper_as,all_accept,verify,probe,relaxed,aligned")
+                    help="comma list of extra sections to run: "
+                         "schedule,paper_as,all_accept,verify,probe,relaxed,aligned,search,ws")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one plain device copy of this size (HBM counter calibration)")
     args = ap.parse_args()
@@ -504,7 +591,7 @@ def main():
     from synth import get_workload, make_catalog, make_prefixes, make_weights
     from paper_2410_05165_amd.binding import Engine
 
-    sections = {"schedule", "paper_as", "all_accept", "verify", "probe", "relaxed", "aligned"}
+    sections = {"schedule", "paper_as", "all_accept", "verify", "probe", "relaxed", "aligned", "search", "ws"}
     if args.no_extras:
         sections = set()
     elif args.only:
@@ -660,14 +747,44 @@ def main():
         extras["decode_bound"] = decode_bound_probe(eng, w, prefix, levels, max(3, args.steps // 2))
 
     eng.close()
+
+    def ws(search, ms):
+        # walltime speedup over the KV-cached target-only beam search
+        return round(search["kv_cached"]["ms_per_decode"] / ms, 3)
+    search = None
+    if "search" in sections:
+        search, search_lists = target_search_line(w, tw, cat, pre, dev, args.steps, args.warmup)
+        if mode == 0:
+            assert (search_lists == out0[0]).all(), "target-only beam search differs from the speculative decode"
+        search["ws_headline_decode"] = ws(search, head["ms_per_decode"])
+        for k_ in ("decode_level1_start", "decode_reuse", "decode_level1_start_reuse", "decode_paper_as",
+                   "decode_all_accept"):
+            if k_ in extras:
+                search[f"ws_{k_}"] = ws(search, extras[k_]["ms_per_decode"])
+        extras["target_search"] = search
     if "aligned" in sections:
-        extras["decode_aligned"] = aligned_line(w, tw, dw, cat, pre, dev, args.steps, args.warmup,
-                                                ref_lists=out0[0] if mode == 0 else None)
+        al = aligned_line(w, tw, dw, cat, pre, dev, args.steps, args.warmup, ref_lists=out0[0] if mode == 0 else None)
+        if search is not None:
+            for k_ in ("trained_users", "held_out_users"):
+                al[k_]["ws"] = ws(search, al[k_]["ms_per_decode"])
+        extras["decode_aligned"] = al
+    if "ws" in sections:
+        extras["ws_by_batch"] = ws_by_batch(w, tw, dw, cat, pre, dev, args.steps, args.warmup)
     if "relaxed" in sections and w.name == "b7":
         wr = get_workload("b7_relaxed")
-        extras["relaxed_decode"] = relaxed_line(wr, tw, dw, cat, pre, dev, args.steps, args.warmup)
+        extras["relaxed_decode"] = rl = relaxed_line(wr, tw, dw, cat, pre, dev, args.steps, args.warmup)
+        rsearch = None
+        if "search" in sections:
+            rsearch, _ = target_search_line(wr, tw, cat, pre, dev, args.steps, args.warmup)
+            for k_ in ("plain", "reuse"):
+                rsearch[f"ws_relaxed_{k_}"] = ws(rsearch, rl[k_]["ms_per_decode"])
+            extras["target_search_k20"] = rsearch
         if "aligned" in sections:
-            extras["relaxed_decode_aligned"] = aligned_line(wr, tw, dw, cat, pre, dev, args.steps, args.warmup)
+            al = aligned_line(wr, tw, dw, cat, pre, dev, args.steps, args.warmup)
+            if rsearch is not None:
+                for k_ in ("trained_users", "held_out_users"):
+                    al[k_]["ws"] = ws(rsearch, al[k_]["ms_per_decode"])
+            extras["relaxed_decode_aligned"] = al
     elif mode != 0 and "relaxed" in sections:
         extras["relaxed_decode"] = relaxed_line(w, tw, dw, cat, pre, dev, args.steps, args.warmup)
 

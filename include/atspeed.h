@@ -269,6 +269,24 @@ ATSPEED_API atspeed_status atspeed_decode_topk(atspeed_ctx* ctx, int32_t B, int3
                                    int32_t* items_dev, float* scores_dev, int32_t* n_items_dev,
                                    atspeed_stats* stats_host);
 
+/* Target-only constrained beam search (task formulation, Sec. 2): the standard
+ * inference that speculative decoding accelerates, and the baseline of the
+ * paper's walltime speedup WS@K (Sec. 4.1).  Prefill of the target alone (the
+ * draft's caches are left stale: atspeed_draft and atspeed_align_data need
+ * atspeed_prefill again), then L levels, each a verify of the tree of the Y_t
+ * paths with no drafted level -- one target forward (with reuse_tree_kv, only
+ * the new level's nodes: the earlier levels' K/V is carried) and the target's
+ * TopK of the next level, strict whatever the configured mode.  Outputs as
+ * atspeed_decode_topk (the same lists as its strict decode).  step_items_dev
+ * [B, K*L, L], step_lens_dev [B, K*L], step_n_dev [B] (all nullable, given
+ * together): every level's beams in level order (codes past a beam's length
+ * zero) -- the multi-step data of draft alignment, whose last rows are the
+ * final lists.  Synchronises once per level. */
+ATSPEED_API atspeed_status atspeed_target_search(atspeed_ctx* ctx, int32_t B, int32_t P, const int32_t* prefix_dev,
+                                                 int32_t* items_dev, float* scores_dev, int32_t* n_items_dev,
+                                                 int32_t* step_items_dev, int32_t* step_lens_dev,
+                                                 int32_t* step_n_dev);
+
 /* Log-probabilities a verify step consumes (parity and inspection access).
  * model 0: the target's log p(. | x, path) of every node the last verify (or
  * tree_logits) forwarded; model 1: the draft's log q(. | x, path) of every node

@@ -138,6 +138,7 @@ struct atspeed_ctx {
   int* align_kslot = nullptr;      // [B, L] slot of the last training sequence's depth-t prefix
   float* loss_rows = nullptr;      // [Mmax] weighted loss of each context row
   bool align_ready = false;        // the tree holds the contexts of the last atspeed_align_data
+  bool dft_prefilled = false;      // the draft's prefix caches hold the last prefill's users
   uint32_t* prev_tpath = nullptr;  // [B*Tmax] path keys of the last verify's tree
   int* prev_depth = nullptr;       // [B*Tmax]
   int* prev_n = nullptr;           // [B] its forwarded (or carried) nodes: slots [0, prev_n)
@@ -726,7 +727,8 @@ void atspeed_destroy(atspeed_ctx* ctx) { delete ctx; }
 
 
 
-atspeed_status atspeed_prefill(atspeed_ctx* c, int32_t B, int32_t P, const int32_t* prefix, float* root_logits) {
+static atspeed_status prefill_impl(atspeed_ctx* c, int32_t B, int32_t P, const int32_t* prefix, float* root_logits,
+                                   bool with_draft) {
   if (!c) return fail(ATSPEED_E_INVALID, "ctx is null");
   if (!prefix) return fail(ATSPEED_E_INVALID, "prefix is null");
   if (B < 1 || B > c->cfg.max_batch) return fail(ATSPEED_E_SHAPE, "B out of range");
@@ -754,8 +756,9 @@ atspeed_status atspeed_prefill(atspeed_ctx* c, int32_t B, int32_t P, const int32
   HIP_TRY(hipMemcpyAsync(c->Mall, &sizes[1], 4, hipMemcpyHostToDevice, c->st));
   launch_plan_prefix(prefix, B, P, S, c->rows, c->st);
   HIP_TRY(hipGetLastError());
+  c->dft_prefilled = false;
   ST_TRY(forward(*c, c->tgt, true, M, P, root_logits, S));
-  if (c->dft.present) ST_TRY(forward(*c, c->dft, true, M, P, nullptr, S));
+  if (with_draft && c->dft.present) ST_TRY(forward(*c, c->dft, true, M, P, nullptr, S));
   c->shared_prefix = S;
   HIP_TRY(hipMemsetAsync(c->state.t, 0, sizeof(int) * B, c->st));
   HIP_TRY(hipMemsetAsync(c->state.steps, 0, sizeof(int) * B, c->st));
@@ -764,16 +767,22 @@ atspeed_status atspeed_prefill(atspeed_ctx* c, int32_t B, int32_t P, const int32
   HIP_TRY(hipMemsetAsync(c->tree.n_nodes, 0, sizeof(int) * B, c->st));
   HIP_TRY(hipStreamSynchronize(c->st));  // host vectors above go out of scope
   c->prefilled = true;
+  c->dft_prefilled = with_draft && c->dft.present;
   c->drafted = false;
   c->carry_ok = false;
   c->align_ready = false;
   return ATSPEED_OK;
 }
 
+atspeed_status atspeed_prefill(atspeed_ctx* c, int32_t B, int32_t P, const int32_t* prefix, float* root_logits) {
+  return prefill_impl(c, B, P, prefix, root_logits, true);
+}
+
 atspeed_status atspeed_draft(atspeed_ctx* c) {
   if (!c) return fail(ATSPEED_E_INVALID, "ctx is null");
   if (!c->dft.present) return fail(ATSPEED_E_STATE, "context has no draft model");
   if (!c->prefilled) return fail(ATSPEED_E_STATE, "draft before prefill");
+  if (!c->dft_prefilled) return fail(ATSPEED_E_STATE, "draft after a target-only prefill (atspeed_target_search)");
   const atspeed_config& cf = c->cfg;
   const int B = c->B, L = cf.L;
   launch_tree_from_beams(c->state, c->tree, c->trie, B, cf.target.item_base, cf.codebook, L, c->st);
@@ -939,6 +948,7 @@ atspeed_status atspeed_logprobs(atspeed_ctx* c, int32_t model, float* lp, float*
   if (!c->prefilled) return fail(ATSPEED_E_STATE, "logprobs before prefill");
   const ModelRt& m = model == 0 ? c->tgt : c->dft;
   if (!m.present) return fail(ATSPEED_E_STATE, "context has no draft model");
+  if (model == 1 && !c->dft_prefilled) return fail(ATSPEED_E_STATE, "the last prefill did not run the draft");
   const size_t row = (size_t)c->nitem * sizeof(float);
   HIP_TRY(hipMemcpyAsync(lp, m.lp, (size_t)c->B * c->Tmax * row, hipMemcpyDeviceToDevice, c->st));
   HIP_TRY(hipMemcpyAsync(root, m.root, (size_t)c->B * row, hipMemcpyDeviceToDevice, c->st));
@@ -991,6 +1001,19 @@ atspeed_status atspeed_set_state(atspeed_ctx* c, int32_t B, const int32_t* t, co
   HIP_TRY(hipMemcpyAsync(c->state.path, pk.data(), pk.size() * 4, hipMemcpyHostToDevice, c->st));
   HIP_TRY(hipMemcpyAsync(c->state.trie, tr.data(), tr.size() * 4, hipMemcpyHostToDevice, c->st));
   HIP_TRY(hipMemcpyAsync(c->state.score, scores, (size_t)B * K * 4, hipMemcpyHostToDevice, c->st));
+  HIP_TRY(hipStreamSynchronize(c->st));
+  return ATSPEED_OK;
+}
+
+// The users' final beams as lists: items [B, K, L] codes, scores [B, K], counts [B] (device).
+static atspeed_status write_lists(atspeed_ctx* c, int32_t B, int32_t* items, float* scores, int32_t* n_items) {
+  const int K = c->cfg.K, L = c->cfg.L;
+  std::vector<int> t(B), nb(B), paths((size_t)B * K * L);
+  std::vector<float> sc((size_t)B * K);
+  ST_TRY(atspeed_get_state(c, B, t.data(), nb.data(), paths.data(), sc.data()));
+  HIP_TRY(hipMemcpyAsync(items, paths.data(), paths.size() * 4, hipMemcpyHostToDevice, c->st));
+  HIP_TRY(hipMemcpyAsync(scores, sc.data(), sc.size() * 4, hipMemcpyHostToDevice, c->st));
+  HIP_TRY(hipMemcpyAsync(n_items, nb.data(), B * 4, hipMemcpyHostToDevice, c->st));
   HIP_TRY(hipStreamSynchronize(c->st));
   return ATSPEED_OK;
 }
@@ -1051,16 +1074,35 @@ atspeed_status atspeed_decode_topk(atspeed_ctx* c, int32_t B, int32_t P, const i
     hipEventDestroy(ev[0]);
     hipEventDestroy(ev[1]);
   }
-  // outputs from the final state
-  const int K = c->cfg.K;
-  std::vector<int> t(B), nb(B), paths((size_t)B * K * L);
-  std::vector<float> sc((size_t)B * K);
-  ST_TRY(atspeed_get_state(c, B, t.data(), nb.data(), paths.data(), sc.data()));
-  HIP_TRY(hipMemcpyAsync(items, paths.data(), paths.size() * 4, hipMemcpyHostToDevice, c->st));
-  HIP_TRY(hipMemcpyAsync(scores, sc.data(), sc.size() * 4, hipMemcpyHostToDevice, c->st));
-  HIP_TRY(hipMemcpyAsync(n_items, nb.data(), B * 4, hipMemcpyHostToDevice, c->st));
-  HIP_TRY(hipStreamSynchronize(c->st));
-  return ATSPEED_OK;
+  return write_lists(c, B, items, scores, n_items);
+}
+
+atspeed_status atspeed_target_search(atspeed_ctx* c, int32_t B, int32_t P, const int32_t* prefix, int32_t* items,
+                                     float* scores, int32_t* n_items, int32_t* step_items, int32_t* step_lens,
+                                     int32_t* step_n) {
+  if (!c) return fail(ATSPEED_E_INVALID, "ctx is null");
+  if (!items || !scores || !n_items) return fail(ATSPEED_E_INVALID, "null output");
+  if ((step_items != nullptr) != (step_lens != nullptr) || (step_items != nullptr) != (step_n != nullptr))
+    return fail(ATSPEED_E_INVALID, "step_items, step_lens and step_n are given together or not at all");
+  ST_TRY(prefill_impl(c, B, P, prefix, nullptr, false));
+  const atspeed_config& cf = c->cfg;
+  const int L = cf.L;
+  if (step_n) HIP_TRY(hipMemsetAsync(step_n, 0, sizeof(int) * B, c->st));
+  for (int l = 0; l < L; ++l) {
+    // the tree of the Y_t paths alone: the verify has no drafted level, so it
+    // takes the target's TopK of level t + 1 (at t = 0 from the prefill's root)
+    launch_tree_from_beams(c->state, c->tree, c->trie, B, cf.target.item_base, cf.codebook, L, c->st);
+    HIP_TRY(hipGetLastError());
+    ST_TRY(tree_forward(*c, nullptr, true));
+    launch_verify_strict(c->state, c->tree, c->trie, c->tgt.lp, c->tgt.root, c->nitem, cf.codebook, L, c->keys,
+                         c->max_cand, c->acc_tmp, c->tafter_tmp, B, c->st);
+    HIP_TRY(hipGetLastError());
+    if (step_items) {
+      launch_append_beams(c->state, B, L, step_items, step_lens, step_n, c->st);
+      HIP_TRY(hipGetLastError());
+    }
+  }
+  return write_lists(c, B, items, scores, n_items);
 }
 
 atspeed_status atspeed_align_data(atspeed_ctx* c, int32_t S, const int32_t* items, const int32_t* lens,
@@ -1069,7 +1111,7 @@ atspeed_status atspeed_align_data(atspeed_ctx* c, int32_t S, const int32_t* item
   if (!a->ctx_weight || !a->label_weight || !a->root_weight || !a->log_pK || !a->lp_target || !a->root_target)
     return fail(ATSPEED_E_INVALID, "align_data: null batch buffer");
   if (S < 1) return fail(ATSPEED_E_SHAPE, "align_data: S must be positive");
-  if (!c->prefilled) return fail(ATSPEED_E_STATE, "align_data before prefill");
+  if (!c->prefilled || !c->dft_prefilled) return fail(ATSPEED_E_STATE, "align_data needs atspeed_prefill first");
   if (!c->dft.present) return fail(ATSPEED_E_STATE, "context has no draft model");
   const atspeed_config& cf = c->cfg;
   const int B = c->B, L = cf.L;

@@ -73,6 +73,9 @@ void launch_verify_relaxed(const StateDev& s, const TreeDev& tr, const TrieDev& 
 
 void launch_tree_from_beams(const StateDev& s, const TreeDev& tr, const TrieDev& trie, int B, int item_base,
                             int codebook, int L, hipStream_t st);
+// Appends the current beams Y_t of every user to a [B][K*L][L] sequence buffer
+// (codes, lengths t) at the user's count n[u] and advances it.
+void launch_append_beams(const StateDev& s, int B, int L, int* items, int* lens, int* n, hipStream_t st);
 void launch_tree_index(const TreeDev& tr, const TrieDev& trie, const StateDev& s, int B, int item_base, int codebook,
                        int L, int* err, hipStream_t st);
 // Row plan of one forward: nodes with slot in [lo[u], hi[u]) of every user, users

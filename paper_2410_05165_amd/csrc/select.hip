@@ -501,10 +501,31 @@ verify_strict_kernel(StateDev s, TreeDev tr, TrieDev trie, const float* lpt, con
   }
 }
 
+// Appends each user's current beams Y_t (codes of depths 1..t, zero past t) to
+// items [B][K*L][L] / lens [B][K*L] at the user's count n[u], which it advances
+// (one level of a target-only beam search; K*L rows hold every level).
+__global__ void append_beams_kernel(StateDev s, int L, int* __restrict__ items, int* __restrict__ lens,
+                                    int* __restrict__ n) {
+  const int u = blockIdx.x, K = s.K;
+  const int t = s.t[u], nb = s.nb[u], base = n[u];
+  const size_t rb = (size_t)u * K * L;
+  for (int k = threadIdx.x; k < nb; k += blockDim.x) {
+    if (base + k >= K * L) break;
+    const uint32_t p = s.path[u * K + k];
+    for (int l = 0; l < L; ++l) items[(rb + base + k) * L + l] = l < t ? path_code(p, l) : 0;
+    lens[rb + base + k] = t;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) n[u] = min(base + nb, K * L);
+}
+
 // ---------------------------------------------------------------- launchers
 void launch_tree_from_beams(const StateDev& s, const TreeDev& tr, const TrieDev& trie, int B, int item_base,
                             int codebook, int L, hipStream_t st) {
   hipLaunchKernelGGL(tree_from_beams_kernel, dim3(B), dim3(64), 0, st, s, tr, trie, item_base, codebook, L);
+}
+void launch_append_beams(const StateDev& s, int B, int L, int* items, int* lens, int* n, hipStream_t st) {
+  hipLaunchKernelGGL(append_beams_kernel, dim3(B), dim3(64), 0, st, s, L, items, lens, n);
 }
 void launch_tree_index(const TreeDev& tr, const TrieDev& trie, const StateDev& s, int B, int item_base, int codebook,
                        int L, int* err, hipStream_t st) {

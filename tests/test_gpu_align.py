@@ -23,8 +23,10 @@ sequences.
   decoding after AtSpeed-S, relaxed sampling decoding after AtSpeed-R).
 
 Multi-step data (the target's K beams of every beam-search step, which the
-paper compares with last-step data) come from the GPU's target-only beam
-search: verifies of trees that hold only the Y_t paths.
+paper compares with last-step data) come from atspeed_target_search, the
+GPU's target-only beam search, whose lists and per-level beams are checked
+against the strict decode and against a host-driven route (verifies of
+uploaded trees that hold only the Y_t paths).
 """
 import ctypes as C
 
@@ -62,10 +64,10 @@ def _mean_accepted(acc):
     return float(a.mean()) if a.size else 0.0
 
 
-def _level_beams(eng, w, prefix):
-    """Multi-step data: the target's K beams of every beam-search step (GPU
-    target-only beam search: verifies of trees holding only the Y_t paths), as
-    items [B, K*L, L], lens, n; levels in order, so a whole item comes last."""
+def _py_level_beams(eng, w, prefix):
+    """Multi-step data built on the host: per level, the tree of the Y_t paths
+    uploaded through the tree pointers and verified (an independent route to
+    the target-only beam search)."""
     B, K, L = prefix.shape[0], w.K, w.L
     eng.atspeed_prefill(prefix)
     levels = []
@@ -85,7 +87,21 @@ def _level_beams(eng, w, prefix):
                 items[u, n[u], :t_[u]] = paths[u, k, :t_[u]]
                 lens[u, n[u]] = t_[u]
                 n[u] += 1
-    return tuple(torch.from_numpy(a).to(DEV) for a in (items, lens, n))
+    return items, lens, n
+
+
+def _level_beams(eng, w, prefix):
+    """Multi-step data: the target's K beams of every beam-search step
+    (atspeed_target_search), items [B, K*L, L], lens, n; levels in order."""
+    B, K, L = prefix.shape[0], w.K, w.L
+    items = torch.zeros((B, K, L), dtype=torch.int32, device=DEV)
+    scores = torch.zeros((B, K), dtype=torch.float32, device=DEV)
+    n = torch.zeros(B, dtype=torch.int32, device=DEV)
+    si = torch.full((B, K * L, L), -1, dtype=torch.int32, device=DEV)
+    sl = torch.full((B, K * L), -1, dtype=torch.int32, device=DEV)
+    sn = torch.full((B,), -1, dtype=torch.int32, device=DEV)
+    eng.atspeed_target_search(prefix, items, scores, n, si, sl, sn)
+    return si, sl, sn
 
 
 def _setup(mode, multistep=False, **hp):
@@ -131,6 +147,39 @@ def _lists(data):
     it, nn = items.cpu().numpy(), n.cpu().numpy()
     ln = lens.cpu().numpy() if lens is not None else np.full(it.shape[:2], it.shape[2])
     return [[tuple(int(c) for c in it[u, k, :ln[u, k]]) for k in range(nn[u])] for u in range(len(nn))]
+
+
+@pytest.mark.parametrize("reuse", [0, 1])
+def test_target_search_small(reuse):
+    """atspeed_target_search: the lists equal the strict speculative decode's
+    (and so the oracle's beam search, by the decode's own parity tests); every
+    level's beams equal those of the host-driven route, bitwise."""
+    from paper_2410_05165_amd.binding import Engine
+    e = env("small")
+    w = e["w"]
+    B, K, L = w.batch, w.K, w.L
+    eng = Engine(w, e["tw"], e["dw"], e["cat"], reuse_tree_kv=reuse)
+    try:
+        prefix = torch.from_numpy(e["pre"]).to(DEV)
+        items0, n0, _ = _decode(eng, w, prefix)
+        items = torch.zeros((B, K, L), dtype=torch.int32, device=DEV)
+        scores = torch.zeros((B, K), dtype=torch.float32, device=DEV)
+        n = torch.zeros(B, dtype=torch.int32, device=DEV)
+        eng.atspeed_target_search(prefix, items, scores, n)
+        assert torch.equal(items, items0) and torch.equal(n, n0)
+        si, sl, sn = (x.cpu().numpy() for x in _level_beams(eng, w, prefix))
+        pi, pl, pn = _py_level_beams(eng, w, prefix)
+        assert np.array_equal(sn, pn)
+        for u in range(B):
+            assert np.array_equal(si[u, :sn[u]], pi[u, :pn[u]]) and np.array_equal(sl[u, :sn[u]], pl[u, :pn[u]]), u
+        assert (sl[:, :K] == 1).all() and all((sl[u, sn[u] - n0[u].item():sn[u]] == L).all() for u in range(B))
+        # a target-only prefill leaves the draft's caches stale
+        with pytest.raises(Exception, match="prefill"):
+            eng.atspeed_target_search(prefix, items, scores, n)
+            eng.atspeed_draft()
+        print(f"[target search, reuse {reuse}] {int(sn.sum())} beams over {L} levels, lists equal the decode's")
+    finally:
+        eng.close()
 
 
 @pytest.mark.parametrize("multistep", [False, True], ids=["last_step", "multi_step"])
