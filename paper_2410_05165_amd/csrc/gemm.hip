@@ -2,8 +2,8 @@
 //
 // bf16 path: MFMA v_mfma_f32_32x32x16_bf16 (fp32 accumulate), block tile
 // BM x BN x 64 fetched by direct global->LDS DMA into two LDS stages
-// (XOR-swizzled 16-byte chunks), or three for small row counts, wave tile
-// TM x TN blocks of 32x32, tile shape chosen by the row count.  Epilogues are
+// (XOR-swizzled 16-byte chunks), or three to six for small row counts, wave
+// tile TM x TN blocks of 32x32, tile shape chosen by the row count.  Epilogues are
 // fused:
 //   QKV   rotary embedding on q and k, rounding to bf16, q to its row buffer,
 //         k/v scattered into the prefix cache or the tree KV buffer.  The tile's
@@ -191,14 +191,14 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
                  BArgs b, EpiArgs e) {
   using T = Tile<WM, WN, TM, TN>;
   constexpr int NW = WM * WN;
-  static_assert(NW == 2 || NW == 4 || NW == 8, "two, four or eight waves");
-  static_assert(NS >= 2 && NS <= 4, "two to four LDS stages");
+  static_assert(NW == 1 || NW == 2 || NW == 4 || NW == 8, "one, two, four or eight waves");
+  static_assert(NS >= 2 && NS <= 8, "two to eight LDS stages");
   constexpr int NA = T::BM / (8 * NW);   // wave instructions per stage for A (8 rows of 128 B each)
   constexpr int NB = T::BN / (8 * NW);
-  __shared__ __align__(1024) unsigned char st0[T::STAGE];
-  __shared__ __align__(1024) unsigned char st1[T::STAGE];
-  __shared__ __align__(1024) unsigned char st2[NS >= 3 ? T::STAGE : 16];
-  __shared__ __align__(1024) unsigned char st3[NS >= 4 ? T::STAGE : 16];
+  // two stages: two named arrays (see the pipeline below); more: one array of NS
+  __shared__ __align__(1024) unsigned char st0[NS == 2 ? T::STAGE : 16];
+  __shared__ __align__(1024) unsigned char st1[NS == 2 ? T::STAGE : 16];
+  __shared__ __align__(1024) unsigned char stn[NS > 2 ? NS : 1][NS > 2 ? T::STAGE : 16];
   const int M = *Mdev;
   // XCD-aware tile order: workgroup L is dispatched to XCD L % 8; XCD x owns the
   // contiguous range x*per .. x*per+per-1 of the tiles.  Tiles are numbered in
@@ -304,10 +304,7 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
   // barrier makes every wave's share of the next stage visible.  Empty asm with
   // a memory clobber on both sides keeps fragment reads and DMA issue from
   // moving across the barrier (the barrier intrinsic does not order memory).
-  auto stage = [&](auto S) -> unsigned char* {
-    constexpr int s_ = decltype(S)::value % NS;
-    return s_ == 0 ? st0 : (s_ == 1 ? st1 : (s_ == 2 ? st2 : st3));
-  };
+  auto stage = [&](auto S) -> unsigned char* { return stn[decltype(S)::value % NS]; };
   constexpr int NLOADS = NA + NB;                 // DMA instructions per stage per lane
   constexpr int ALLOW = NLOADS * (NS - 2);        // loads that may stay in flight at a stage boundary
   constexpr int WAITCNT = (ALLOW & 0xF) | (((ALLOW >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8);
@@ -421,13 +418,15 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
     // buffers are free now), then written out in 16-byte chunks along rows.
     constexpr int OUTC = EPI == EPI_GU ? T::BN / 2 : T::BN;  // output columns of the tile
     constexpr int OROW = OUTC * 2;                            // bytes per LDS row
-    // The whole output tile in st0 when it fits a stage buffer; otherwise its
-    // first half of rows in st0 and the second in st1.
+    // The whole output tile in the first stage buffer when it fits; otherwise
+    // its first half of rows there and the second in the next one.
     constexpr bool ONEBUF = T::BM * OROW <= T::STAGE;
     constexpr int HROWS = ONEBUF ? T::BM : T::BM / 2;
     constexpr int WMH = ONEBUF ? WM : WM / 2;       // wave rows per buffer
     static_assert(ONEBUF || (HROWS * OROW <= T::STAGE && WM % 2 == 0), "each half of the output tile fits a stage");
-    bf16_t* ob = reinterpret_cast<bf16_t*>(wave_m < WMH ? st0 : st1);
+    unsigned char* const ob0 = NS == 2 ? st0 : stn[0];
+    unsigned char* const ob1 = NS == 2 ? st1 : stn[NS > 2 ? 1 : 0];
+    bf16_t* ob = reinterpret_cast<bf16_t*>(wave_m < WMH ? ob0 : ob1);
     const int hrow0 = (wave_m % WMH) * TM * 32;
     if constexpr (EPI == EPI_GU) {
       constexpr int half = TN / 2;
@@ -512,7 +511,7 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const int* __restrict__ 
       const int lr = c / CPRW, cc = (c % CPRW) * 8;
       const int row = m0 + lr;
       if (row >= M) continue;
-      const unsigned char* src = (lr < HROWS ? st0 : st1) + (lr % HROWS) * OROW + cc * 2;
+      const unsigned char* src = (lr < HROWS ? ob0 : ob1) + (lr % HROWS) * OROW + cc * 2;
       const u32x4_t v = *reinterpret_cast<const u32x4_t*>(src);
       if constexpr (EPI == EPI_GU) {
         const int fcol = tile_n * (T::BN / 2) + cc;
@@ -696,6 +695,18 @@ constexpr Shape kResidShapes[] = {
     {256, 256, 1, 25.f, 97.5f}, {256, 128, 1, 10.5f, 70.f}, {128, 128, 2, 14.f, 59.f}, {64, 64, 4, 6.f, 50.f},
     {128, 128, 1, 4.4f, 36.f}};
 
+// Few rows (a decode level of a few users, the verify tree of one user): the
+// weight stream is the whole cost, and the tiles above leave most CUs idle (a
+// 256-column tile gives q/k/v 48 workgroups).  Narrow tiles of two waves with
+// four to six LDS stages give 190-380 workgroups, each streaming a thin weight
+// slice; their crossover row counts against the shapes above, measured at the
+// 7B projections with cold weights (1-192 rows): q/k/v 32x64 (six stages) to
+// 32 rows, 27 instead of 54 us, and 64x64 (four) to 128 rows; gate/up 64x64
+// (four) to 32 rows, 42-45 instead of 60-64 us, 64x128 (four) to 64, 64x64
+// (three) to 128; o and down 64x32 (six) to 128 rows, 15 and 30 instead of 22
+// and 50 us at 1-64 rows.
+constexpr int kFewRowsQkv = 128, kFewRowsGu = 128, kFewRowsResid = 128;
+
 template <int NSH>
 int pick_shape(const Shape (&sh)[NSH], int M, int N, int K, int kparts, float partial) {
   int best = 0;
@@ -717,6 +728,8 @@ hipError_t gemm(const GemmCall& g, hipStream_t st) {
     const int M = g.Mmax > 0 ? g.Mmax : 1;
     switch (g.kind) {
       case GEMM_QKV:
+        if (M <= 32) return launch_bf16<BMAP_QKV, EPI_QKV, 1, 2, 1, 1, 6>(g, st);
+        if (M <= kFewRowsQkv) return launch_bf16<BMAP_QKV, EPI_QKV, 2, 1, 1, 2, 4>(g, st);
         switch (pick_shape(kQkvShapes, M, g.N, g.K, 1, 1.f)) {
           case 0: return launch_bf16<BMAP_QKV, EPI_QKV, 4, 2, 2, 4>(g, st);
           case 1: return launch_bf16<BMAP_QKV, EPI_QKV, 4, 2, 1, 4, 3>(g, st);
@@ -725,12 +738,16 @@ hipError_t gemm(const GemmCall& g, hipStream_t st) {
           default: return launch_bf16<BMAP_QKV, EPI_QKV, 2, 4, 1, 2, 3>(g, st);
         }
       case GEMM_GU:
+        if (M <= 32) return launch_bf16<BMAP_GU, EPI_GU, 2, 1, 1, 2, 4>(g, st);
+        if (M <= 64) return launch_bf16<BMAP_GU, EPI_GU, 2, 2, 1, 2, 4>(g, st);
+        if (M <= kFewRowsGu) return launch_bf16<BMAP_GU, EPI_GU, 2, 1, 1, 2, 3>(g, st);
         switch (pick_shape(kGuShapes, M, g.N, g.K, 1, 1.f)) {
           case 0: return launch_bf16<BMAP_GU, EPI_GU, 4, 2, 2, 4>(g, st);
           case 1: return launch_bf16<BMAP_GU, EPI_GU, 4, 2, 1, 4, 3>(g, st);
           default: return launch_bf16<BMAP_GU, EPI_GU, 1, 2, 2, 4>(g, st);
         }
       case GEMM_RESID:
+        if (M <= kFewRowsResid) return launch_bf16<BMAP_PLAIN, EPI_RESID, 2, 1, 1, 1, 6>(g, st);
         switch (pick_shape(kResidShapes, M, g.N, g.K, g.part ? 2 : 1, 0.5f)) {
           case 0: return launch_bf16<BMAP_PLAIN, EPI_RESID, 4, 2, 2, 4>(g, st);
           case 1: return launch_bf16<BMAP_PLAIN, EPI_RESID, 4, 2, 2, 2>(g, st);
