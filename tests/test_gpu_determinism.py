@@ -101,3 +101,43 @@ def test_shared_prompt_prefill_is_exact():
             np.testing.assert_array_equal(together[u], one.cpu().numpy()[0])
     finally:
         eng.close()
+
+
+def test_few_row_tiles_are_batch_invariant():
+    """At the 7B widths: users decoded one at a time (the few-row GEMM tiles: a
+    decode level of one user is 10 target rows, its verify tree 80) give bitwise
+    the lists and scores they get inside the 32-user batch (the wide tiles), and
+    so does the target-only search.  Two layers keep it quick; the tile choice
+    depends only on the row count."""
+    from paper_2410_05165_amd.binding import Engine
+    from synth import get_workload, make_catalog, make_prefixes, make_weights
+    w = get_workload("b7")
+    w = w.with_(target=w.target.__class__(2, 4096, 32, 11008, w.target.vocab, w.target.item_base))
+    cat = make_catalog(w)
+    pre = make_prefixes(w, cat)
+    print("[few rows] weights of a two-layer 7B-width target", flush=True)
+    eng = Engine(w, make_weights(w, "target"), make_weights(w, "draft"), cat)
+    try:
+        B, K, L = w.batch, w.K, w.L
+
+        def run(prefix, search=False):
+            b = prefix.shape[0]
+            items = torch.zeros((b, K, L), dtype=torch.int32, device=DEV)
+            scores = torch.zeros((b, K), dtype=torch.float32, device=DEV)
+            n = torch.zeros(b, dtype=torch.int32, device=DEV)
+            (eng.atspeed_target_search if search else eng.atspeed_decode_topk)(prefix, items, scores, n)
+            torch.cuda.synchronize()
+            return items.cpu().numpy(), scores.cpu().numpy(), n.cpu().numpy()
+        P = torch.from_numpy(pre).to(DEV)
+        full = run(P)
+        full_s = run(P, True)
+        for x, y in zip(full, full_s):
+            assert (x == y).all()
+        for u in (0, 13, 31):
+            print(f"[few rows] user {u} alone", flush=True)
+            for search in (False, True):
+                one = run(P[u:u + 1].contiguous(), search)
+                for x, y in zip(one, full):
+                    assert (x[0] == y[u]).all(), (u, search)
+    finally:
+        eng.close()
