@@ -104,10 +104,10 @@ def _level_beams(eng, w, prefix):
     return si, sl, sn
 
 
-def _setup(mode, multistep=False, **hp):
+def _setup(mode, multistep=False, name="small", **hp):
     from paper_2410_05165_amd.align import AlignTrainer
     from paper_2410_05165_amd.binding import Engine
-    e = env("small")
+    e = env(name)
     w = e["w"]
     eng = Engine(w, e["tw"], e["dw"], e["cat"])
     prefix = torch.from_numpy(e["pre"]).to(DEV)
@@ -230,11 +230,15 @@ def test_align_data_small(multistep):
         eng.close()
 
 
-@pytest.mark.parametrize("mode,alpha,multistep", [("S", 1.0, False), ("R", 1.0, False), ("S", 0.5, False),
-                                                  ("S", 0.5, True), ("R", 0.5, True)])
-def test_align_step_matches_oracle(mode, alpha, multistep):
+@pytest.mark.parametrize("name,mode,alpha,multistep", [
+    ("small", "S", 1.0, False), ("small", "R", 1.0, False), ("small", "S", 0.5, False), ("small", "S", 0.5, True),
+    ("small", "R", 0.5, True), ("tiny", "S", 0.5, True), ("tiny", "R", 0.5, False)])
+def test_align_step_matches_oracle(name, mode, alpha, multistep):
+    """One step against the oracle: bf16 at the small shape, fp32 at the tiny one
+    (the fp32 instantiations of the head-gradient, hidden-row and AdamW kernels;
+    an fp32 head is the master copy itself)."""
     hp = dict(alpha=alpha, lr=2e-3, betas=(0.9, 0.99), eps=1e-8, weight_decay=0.01)
-    e, eng, prefix, tr, data, _, _ = _setup(mode, multistep, **hp)
+    e, eng, prefix, tr, data, _, _ = _setup(mode, multistep, name, **hp)
     try:
         w = e["w"]
         B, T, L, cb, nit, K = w.batch, eng.max_nodes, w.L, w.codebook, eng.n_item, w.K
@@ -267,7 +271,7 @@ def test_align_step_matches_oracle(mode, alpha, multistep):
             return H[u] if p == () else H[B + u * T + slot[u][p]]
 
         want_loss, grads = aligned_loss(mode, lq_of, lp_of, e["trie"], Y, K, L, cb, alpha)
-        tag = f"[align {mode} alpha {alpha}{' multi-step' if multistep else ''}]"
+        tag = f"[align {name} {mode} alpha {alpha}{' multi-step' if multistep else ''}]"
         print(f"{tag} loss GPU {loss:.8f} oracle {want_loss:.8f}; {len(grads)} contexts", flush=True)
         assert abs(loss - want_loss) <= 1e-5 * abs(want_loss) + 1e-7
         hid = {k: h_of(*k) for k in grads}
@@ -287,7 +291,7 @@ def test_align_step_matches_oracle(mode, alpha, multistep):
         want_w, _, _ = adamw_step(master0, 0.0, 0.0, G, 1, hp["lr"], hp["betas"][0], hp["betas"][1], hp["eps"],
                                   hp["weight_decay"])
         np.testing.assert_allclose(master, want_w, rtol=1e-6, atol=1e-6 * hp["lr"])
-        assert np.array_equal(head, round_bf16(master))
+        assert np.array_equal(head, round_bf16(master) if w.dtype == "bf16" else master)
         assert not np.array_equal(head, head0)
     finally:
         eng.close()
