@@ -18,7 +18,8 @@ decode, the strict and relaxed decodes after draft alignment (AtSpeed-S /
 AtSpeed-R training of the draft's item head on the benchmark users, measured on
 them and on held-out users), and the target-only beam search that the paper's
 walltime speedup WS is measured against (with the speedup of each decode, and
-WS at batch sizes 1, 4 and 32 with the random and the aligned draft); the
+WS at batch sizes 1, 4 and 32 with the random and the aligned draft), and the
+stress decode (config 5: 1M items, 128 users x 1,024 tokens, K 50); the
 roofline kernel is the target's gate/up GEMM over the timed decodes.
 
 Prints ONE JSON line.  Progress goes to stderr.
@@ -500,6 +501,49 @@ def ws_by_batch(w, tw, dw, cat, pre, dev, steps, warmup, batches=(1, 4, 32), tra
                                 "in both), first B users; the aligned draft is trained on those users")
 
 
+def stress_line(tw, dw, dev, steps, warmup):
+    """Config 5 (stress): 1M items, 128 users with 1,024-token prefixes, K 50,
+    N 100, the same 7B-shaped target and draft (the same seeded weights as the
+    benchmark's, passed in).  Whole decodes (natural drafts) and the target-only
+    search on the same context (paths recomputed: the tree-KV reuse buffers would
+    need 74 GB more at this shape)."""
+    import numpy as np
+    import torch
+    from paper_2410_05165_amd.binding import Engine
+    from synth import get_workload, make_catalog, make_prefixes
+    w = get_workload("stress")
+    t0 = time.time()
+    cat = make_catalog(w)
+    pre = make_prefixes(w, cat)
+    eng = Engine(w, tw, dw, cat)
+    log(f"stress: {len(cat)} items, prefixes {pre.shape}, workspace {eng.ws.numel() / 2**30:.1f} GiB "
+        f"({time.time() - t0:.1f}s)")
+    prefix = torch.from_numpy(pre).to(dev)
+    r, out, _, _ = timed_decodes(eng, w, prefix, steps, warmup, roofline=False)
+    B, K, L = w.batch, w.K, w.L
+    items = torch.zeros((B, K, L), dtype=torch.int32, device=dev)
+    scores = torch.zeros((B, K), dtype=torch.float32, device=dev)
+    n = torch.zeros(B, dtype=torch.int32, device=dev)
+    eng.atspeed_target_search(prefix, items, scores, n)
+    torch.cuda.synchronize()
+    assert (items.cpu().numpy() == out[0]).all(), "stress: decode differs from the target-only search"
+    t1 = time.perf_counter()
+    for _ in range(steps):
+        eng.atspeed_target_search(prefix, items, scores, n)
+    torch.cuda.synchronize()
+    ms_search = 1e3 * (time.perf_counter() - t1) / steps
+    eng.close()
+    res = {k: r[k] for k in ("lists_per_s", "ms_per_decode", "steps", "ms_prefill", "ms_draft", "ms_verify",
+                             "lists_per_s_decode_only", "target_tree_rows")}
+    res.update(target_search_ms=ms_search, ws=round(ms_search / r["ms_per_decode"], 3),
+               workload=f"stress: B={B}, P={w.prefix_len}, K={K}, N={w.N}, {w.n_items} items, strict, natural drafts",
+               lists_mean=float(out[2].mean()))
+    log(f"stress decode: {r['ms_per_decode']:.0f} ms per {B} users ({r['lists_per_s']:.0f} lists/s; prefill "
+        f"{r['ms_prefill']:.0f} ms, verify {r['ms_verify']:.0f} ms, {r['steps']} steps); target-only search "
+        f"{ms_search:.0f} ms")
+    return res
+
+
 def aligned_line(w, tw, dw, cat, pre, dev, steps, warmup, ref_lists=None, train_steps=300, alpha=0.5, peak_lr=1e-2):
     """Draft alignment, then natural decodes: AtSpeed-S for strict verification,
     AtSpeed-R for relaxed, on the multi-step data of the benchmark users (the
@@ -577,7 +621,7 @@ def main():
                     help="only the headline decode (profiling runs): no other profiles, verify step, probe or relaxed line")
     ap.add_argument("--only", default="",
                     help="comma list of extra sections to run: "
-                         "schedule,paper_as,all_accept,verify,probe,relaxed,aligned,search,ws")
+                         "schedule,paper_as,all_accept,verify,probe,relaxed,aligned,search,ws,stress")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one plain device copy of this size (HBM counter calibration)")
     args = ap.parse_args()
@@ -591,7 +635,8 @@ def main():
     from synth import get_workload, make_catalog, make_prefixes, make_weights
     from paper_2410_05165_amd.binding import Engine
 
-    sections = {"schedule", "paper_as", "all_accept", "verify", "probe", "relaxed", "aligned", "search", "ws"}
+    sections = {"schedule", "paper_as", "all_accept", "verify", "probe", "relaxed", "aligned", "search", "ws",
+                "stress"}
     if args.no_extras:
         sections = set()
     elif args.only:
@@ -787,6 +832,9 @@ def main():
             extras["relaxed_decode_aligned"] = al
     elif mode != 0 and "relaxed" in sections:
         extras["relaxed_decode"] = relaxed_line(w, tw, dw, cat, pre, dev, args.steps, args.warmup)
+
+    if "stress" in sections and w.name == "b7":
+        extras["stress_decode"] = stress_line(tw, dw, dev, max(2, min(args.steps, 3)), 1)
 
     cpu = None
     if not args.no_cpu_baseline and mode == 0:
