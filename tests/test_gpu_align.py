@@ -342,3 +342,58 @@ def test_align_training_small(mode):
         if reng is not None:
             reng.close()
         eng.close()
+
+
+def test_align_errors_leave_a_usable_context():
+    """Argument and state errors of the alignment calls, each caught by the host
+    checks or by the context-tree kernel's own validation before any access it
+    could not bound: the call returns its status and a valid batch then works."""
+    from paper_2410_05165_amd.align import AlignTrainer
+    from paper_2410_05165_amd.binding import AtspeedError, Engine
+    e = env("small")
+    w = e["w"]
+    B, K, L = w.batch, w.K, w.L
+    eng = Engine(w, e["tw"], e["dw"], e["cat"])
+    inv, state = 1, 5          # ATSPEED_E_INVALID, ATSPEED_E_STATE
+    try:
+        prefix = torch.from_numpy(e["pre"]).to(DEV)
+        items, n, _ = _decode(eng, w, prefix)
+        eng.atspeed_prefill(prefix)
+        tr = AlignTrainer(eng, "S", alpha=0.5)
+        with pytest.raises(AtspeedError) as ex:           # a step before any batch
+            tr.step()
+        assert ex.value.status == state
+        cases = []
+        bad = items.clone(); bad[3, 0, 2] = w.codebook + 40           # code out of range
+        cases.append(("code out of range", bad, n, None))
+        cat = set(map(tuple, e["cat"].tolist()))
+        probe = next((a, b, c, d) for a in range(3) for b in range(256) for c in range(3) for d in range(3)
+                     if (a, b, c, d) not in cat)
+        bad = items.clone(); bad[5, 1] = torch.tensor(probe, dtype=torch.int32)   # not a catalog item
+        cases.append(("not in the catalog", bad, n, None))
+        bad_n = n.clone(); bad_n[2] = 0
+        cases.append(("no sequences", items, bad_n, None))
+        bad_n = n.clone(); bad_n[2] = K + 1
+        cases.append(("more sequences than S", items, bad_n, None))
+        lens = torch.full((B, K), L, dtype=torch.int32, device=DEV); lens[0, n[0] - 1] = 2
+        cases.append(("last sequence shorter than L", items, n, lens))
+        lens = torch.full((B, K), L, dtype=torch.int32, device=DEV); lens[4, 0] = L + 1
+        cases.append(("length above L", items, n, lens))
+        for what, it, nn, ll in cases:
+            with pytest.raises(AtspeedError) as ex:
+                tr.data(it, nn, ll)
+            assert ex.value.status == inv, what
+            print(f"[align errors] {what}: ATSPEED_E_INVALID")
+            with pytest.raises(AtspeedError) as ex:       # the failed batch is not trainable
+                tr.step()
+            assert ex.value.status == state, what
+        tr.data(items, n)
+        tr.args.alpha = 1.5
+        with pytest.raises(AtspeedError) as ex:
+            tr.step()
+        assert ex.value.status == inv
+        tr.args.alpha = 0.5
+        tr.args.step = 0
+        assert np.isfinite(tr.step())
+    finally:
+        eng.close()
