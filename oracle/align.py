@@ -45,11 +45,20 @@ fixed (the selection is piecewise constant in z):
 Training the draft's item-head rows W (z = W h for the normed final hidden h of
 the context) then has dL/dW = sum_c w_c (dl/dz)(c) h(c)^T.
 
+D' for AtSpeed-S with lambda < 1 (Sec. 3.1): the top-K sequences of constrained
+beam search (width K, every level's beams kept for multi-step data) under the
+token-level mixture m(c | s) = (1 - lambda) q(c | s) + lambda p(c | s) of the two
+models' item distributions, a sequence scored by sum_t log m(y_t | y_<t); ties
+by the lexicographically smaller sequence, as in every other search here.
+
 The optimizer is AdamW (the paper's implementation details) with decoupled
 weight decay: w <- w - lr wd w - lr m_hat / (sqrt(v_hat) + eps), m_hat and v_hat
 the bias-corrected first and second moments.
 
-Parity: pinned in tests/test_oracle_align.py -- the gradients against central
+Parity: pinned in tests/test_oracle_align.py -- the mixture search against
+the target's and the draft's own beam search at lambda = 1 and 0, against
+brute-force enumeration of a small catalog and against a hand-worked table
+(tests/golden/mixture_example.json); the gradients against central
 finite differences of the losses, a hand-worked context for each loss
 (tests/golden/align_example.json), the regulariser's sign (negative when every
 code of V_c is more probable under the target than the K-th sequence's code,
@@ -64,9 +73,11 @@ first-step closed form (a step of lr times the gradient's sign without decay).
 from __future__ import annotations
 
 import math
-from typing import Dict, List, Sequence, Tuple
+from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
+
+from .search import Decision, top_boundary
 
 Path = Tuple[int, ...]
 
@@ -203,3 +214,33 @@ def adamw_step(w: np.ndarray, m: np.ndarray, v: np.ndarray, g: np.ndarray, step:
     w = w - lr * weight_decay * w
     w = w - lr * m_hat / (np.sqrt(v_hat) + eps)
     return w, m, v
+
+
+def mixed_log(lq: np.ndarray, lp: np.ndarray, lam: float) -> np.ndarray:
+    """log((1 - lam) q + lam p) of two log-probability rows (lam 0 and 1 return a row unchanged)."""
+    if lam == 1.0:
+        return np.asarray(lp, dtype=np.float64)
+    if lam == 0.0:
+        return np.asarray(lq, dtype=np.float64)
+    mx = np.maximum(lq, lp)
+    return mx + np.log((1.0 - lam) * np.exp(lq - mx) + lam * np.exp(lp - mx))
+
+
+def mixture_beam_search(lp_of, lq_of, trie, K: int, L: int, codebook: int, lam: float,
+                        log: Optional[List[Decision]] = None):
+    """Constrained beam search of width K under the mixture (1 - lam) q + lam p;
+    lp_of / lq_of(path) -> item log-probs of the target / draft at that context.
+    Returns the beams (path, mixed score) of every level 1..L."""
+    beams = [((), 0.0)]
+    levels = []
+    for lvl in range(1, L + 1):
+        cands = []
+        for path, score in beams:
+            row = mixed_log(lq_of(path), lp_of(path), lam)
+            for c in trie.children(path):
+                cands.append((path + (c,), score + float(row[codebook * (lvl - 1) + c])))
+        beams, margin, pair = top_boundary(cands, K)
+        if log is not None:
+            log.append(Decision("mixture_topk", lvl, margin, pair))
+        levels.append(beams)
+    return levels

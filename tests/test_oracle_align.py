@@ -6,7 +6,7 @@ import os
 import numpy as np
 import pytest
 
-from oracle.align import (adamw_step, label_distributions, rec_loss, align_r, align_s, aligned_loss, constrained_topk, context_weights, head_gradient,
+from oracle.align import (adamw_step, label_distributions, mixture_beam_search, rec_loss, align_r, align_s, aligned_loss, constrained_topk, context_weights, head_gradient,
                           log_pK_of)
 from oracle.search import table_scorer
 from oracle.trie import Trie
@@ -202,3 +202,50 @@ def test_aggregate_gradient_finite_differences(mode):
             zm[k][j] -= h
             fd = (total(zp)[0] - total(zm)[0]) / (2 * h)
             assert abs(fd - w * g[j]) < 1e-7, (k, j, fd, w * g[j])
+
+
+def _mixture_tables():
+    ex = json.load(open(os.path.join(GOLDEN, "mixture_example.json")))
+    key = lambda path: "".join(str(c) for c in path)
+    lp = lambda path: np.log(np.array(ex["rows"][key(path)]["p"]))
+    lq = lambda path: np.log(np.array(ex["rows"][key(path)]["q"]))
+    return ex, lp, lq
+
+
+def test_mixture_search_hand_example():
+    ex, lp, lq = _mixture_tables()
+    trie = Trie(np.array([[0, 0], [0, 1], [1, 0], [1, 1]]))
+    for case in ex["cases"]:
+        levels = mixture_beam_search(lp, lq, trie, case["K"], ex["L"], ex["codebook"], case["lambda"])
+        for got, want in zip(levels, (case["level1"], case["level2"])):
+            assert [p for p, _ in got] == [tuple(p) for p, _ in want], case
+            np.testing.assert_allclose([s for _, s in got], [math.log(v) for _, v in want], rtol=0, atol=1e-12)
+
+
+def test_mixture_search_reduces_to_each_model_and_to_enumeration():
+    from oracle.search import beam_search
+    rng = np.random.default_rng(11)
+    cb, L = 3, 3
+    cat = np.array([[a, b, c] for a in range(3) for b in range(3) for c in range(3) if (a * 7 + b * 3 + c) % 5 != 2])
+    trie = Trie(cat)
+    paths = {()} | {tuple(r[:t]) for r in cat.tolist() for t in range(1, L)}
+    P = {p: np.log(rng.dirichlet(np.ones(cb * L))) for p in paths}
+    Q = {p: np.log(rng.dirichlet(np.ones(cb * L))) for p in paths}
+    lp, lq = (lambda p: P[p]), (lambda p: Q[p])
+    for lam, table in ((1.0, P), (0.0, Q)):
+        want = beam_search(table_scorer(table), trie, 4, L, cb)
+        got = mixture_beam_search(lp, lq, trie, 4, L, cb, lam)
+        for g, wv in zip(got, want):
+            assert [p for p, _ in g] == [p for p, _ in wv]
+            np.testing.assert_allclose([s for _, s in g], [s for _, s in wv], rtol=0, atol=1e-12)
+    # width at least the catalog: the last level ranks every item by its mixed
+    # sequence log-probability, summed here in probability space per token
+    lam = 0.3
+    got = mixture_beam_search(lp, lq, trie, len(cat), L, cb, lam)[-1]
+    score = {}
+    for item in map(tuple, cat.tolist()):
+        score[item] = sum(math.log((1 - lam) * math.exp(Q[item[:t]][cb * t + item[t]])
+                                   + lam * math.exp(P[item[:t]][cb * t + item[t]])) for t in range(L))
+    want = sorted(score.items(), key=lambda kv: (-kv[1], kv[0]))
+    assert [p for p, _ in got] == [p for p, _ in want]
+    np.testing.assert_allclose([s for _, s in got], [s for _, s in want], rtol=0, atol=1e-12)
