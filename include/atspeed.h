@@ -287,6 +287,24 @@ ATSPEED_API atspeed_status atspeed_target_search(atspeed_ctx* ctx, int32_t B, in
                                                  int32_t* step_items_dev, int32_t* step_lens_dev,
                                                  int32_t* step_n_dev);
 
+/* Mixture beam search: the training sequences D' of AtSpeed-S (Sec. 3.1) for a
+ * mixing weight lambda in [0, 1] -- constrained beam search of width K whose
+ * token distribution is (1 - lambda) q + lambda p (the draft's and the target's
+ * item distributions), a sequence scored by the sum of the log of the mixture
+ * over its tokens.  Prefill of both models, then L levels, each a forward of
+ * the target and of the draft over the tree of the Y_t paths (with
+ * reuse_tree_kv the target carries the earlier levels' K/V) and the strict
+ * TopK of the next level under the mixture.  lambda = 1 gives bitwise the
+ * lists and beams of atspeed_target_search.  Outputs as atspeed_target_search
+ * (scores: cumulative log-mixture).  Leaves the draft's root log-probs mixed:
+ * atspeed_draft and atspeed_align_data need atspeed_prefill again.
+ * ATSPEED_E_INVALID for lambda outside [0, 1]; ATSPEED_E_STATE without a
+ * draft.  Synchronises once per level. */
+ATSPEED_API atspeed_status atspeed_mixed_search(atspeed_ctx* ctx, float lambda, int32_t B, int32_t P,
+                                                const int32_t* prefix_dev, int32_t* items_dev, float* scores_dev,
+                                                int32_t* n_items_dev, int32_t* step_items_dev,
+                                                int32_t* step_lens_dev, int32_t* step_n_dev);
+
 /* Log-probabilities a verify step consumes (parity and inspection access).
  * model 0: the target's log p(. | x, path) of every node the last verify (or
  * tree_logits) forwarded; model 1: the draft's log q(. | x, path) of every node
@@ -309,7 +327,8 @@ ATSPEED_API atspeed_status atspeed_logprobs(atspeed_ctx* ctx, int32_t model, flo
  * of Sec. 3.1 with lambda = 1, the target's top-K lists (atspeed_decode_topk in
  * strict mode) -- the last beam-search step's sequences -- or, for the
  * multi-step data the paper also evaluates, the target's K beams of every
- * beam-search step (lengths 1..L).  The last sequence of a user must be a whole
+ * beam-search step (lengths 1..L; atspeed_target_search), or for lambda < 1
+ * those of the mixture (atspeed_mixed_search).  The last sequence of a user must be a whole
  * item: it is the K-th sequence of the p_K term.  The contexts are each user's
  * root and every distinct proper prefix of its sequences; for a context c with
  * draft and target item distributions q, p and V_c the K trie-valid codes of

@@ -23,7 +23,7 @@ SYMBOLS = ("atspeed_workspace_bytes", "atspeed_create", "atspeed_destroy", "atsp
            "atspeed_prefill", "atspeed_draft", "atspeed_get_tree", "atspeed_verify", "atspeed_tree_logits",
            "atspeed_accept", "atspeed_accept_noalloc", "atspeed_decode_topk", "atspeed_logprobs", "atspeed_get_state", "atspeed_set_state",
            "atspeed_set_timing", "atspeed_get_timing", "atspeed_align_data", "atspeed_align_step",
-           "atspeed_target_search")
+           "atspeed_target_search", "atspeed_mixed_search")
 KERNEL_CLASSES = ("qkv", "o", "gu", "down", "lm_head", "attention", "row", "select")
 
 
@@ -110,6 +110,7 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
     lib.atspeed_align_data.argtypes = [vp, i32, pi32, pi32, pi32, C.POINTER(AlignArgs)]
     lib.atspeed_align_step.argtypes = [vp, C.POINTER(AlignArgs), C.POINTER(C.c_double)]
     lib.atspeed_target_search.argtypes = [vp, i32, i32, pi32, pi32, pf, pi32, pi32, pi32, pi32]
+    lib.atspeed_mixed_search.argtypes = [vp, C.c_float, i32, i32, pi32, pi32, pf, pi32, pi32, pi32, pi32]
     for name in SYMBOLS:
         fn = getattr(lib, name)
         if fn.restype is C.c_int:  # default
@@ -251,6 +252,11 @@ class Engine:
         B, P = prefix.shape
         self._check(self.lib.atspeed_target_search(self.ctx, B, P, _ptr(prefix), _ptr(items), _ptr(scores),
                                                    _ptr(n_items), _ptr(step_items), _ptr(step_lens), _ptr(step_n)))
+
+    def atspeed_mixed_search(self, lam, prefix, items, scores, n_items, step_items=None, step_lens=None, step_n=None):
+        B, P = prefix.shape
+        self._check(self.lib.atspeed_mixed_search(self.ctx, lam, B, P, _ptr(prefix), _ptr(items), _ptr(scores),
+                                                  _ptr(n_items), _ptr(step_items), _ptr(step_lens), _ptr(step_n)))
 
     def atspeed_logprobs(self, model, lp, root):
         self._check(self.lib.atspeed_logprobs(self.ctx, model, _ptr(lp), _ptr(root)))

@@ -319,6 +319,36 @@ __global__ void adamw_kernel(float* __restrict__ master, float* __restrict__ m, 
   }
 }
 
+// log((1 - lam) q + lam p) in place over the draft's log-prob rows: rows
+// [0, nrows[u]) of each user's rows_per_user (every row when nrows is null).
+// lam 1 and 0 copy one model's row unchanged.
+__global__ void __launch_bounds__(256)
+mix_logprobs_kernel(float* __restrict__ lq, const float* __restrict__ lp, const int* __restrict__ nrows,
+                    int rows_per_user, int nitem, float lam) {
+  const int u = blockIdx.x / rows_per_user, r = blockIdx.x % rows_per_user;
+  if (nrows && r >= nrows[u]) return;
+  const size_t off = (size_t)blockIdx.x * nitem;
+  for (int j = threadIdx.x; j < nitem; j += 256) {
+    const float q = lq[off + j], p = lp[off + j];
+    float m;
+    if (lam >= 1.f) {
+      m = p;
+    } else if (lam <= 0.f) {
+      m = q;
+    } else {
+      const float mx = fmaxf(q, p);
+      m = mx + logf((1.f - lam) * expf(q - mx) + lam * expf(p - mx));
+    }
+    lq[off + j] = m;
+  }
+}
+
+void launch_mix_logprobs(float* lq, const float* lp, const int* nrows, int B, int rows_per_user, int nitem, float lam,
+                         hipStream_t st) {
+  hipLaunchKernelGGL(mix_logprobs_kernel, dim3(B * rows_per_user), dim3(256), 0, st, lq, lp, nrows, rows_per_user,
+                     nitem, lam);
+}
+
 void launch_align_tree(const int* items, const int* lens, const int* n_items, int S, const TreeDev& tr,
                        const TrieDev& trie, int B, int L, int item_base, int codebook, float* ctx_weight,
                        float* label_weight, float* root_weight, int* kslot, int* err, hipStream_t st) {

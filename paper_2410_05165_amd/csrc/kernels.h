@@ -72,6 +72,9 @@ void launch_align_logpk(const int* items, const int* n_items, const int* kslot, 
 void launch_align_grad(const AlignRows& ar, const TrieDev& trie, const TreeDev& tr, int B, int M, int nitem,
                        int codebook, int L, int K, int mode, float alpha, float* dz, float* loss_rows,
                        hipStream_t st);
+// log((1 - lam) exp(lq) + lam exp(lp)) into lq, rows [0, nrows[u]) of each user (all if null).
+void launch_mix_logprobs(float* lq, const float* lp, const int* nrows, int B, int rows_per_user, int nitem, float lam,
+                         hipStream_t st);
 void launch_head_grad(bool bf16, const float* dz, const void* h_root, const void* h_rows, const int* Mdev, int B,
                       int nitem, int d, float* dW, hipStream_t st);
 void launch_align_hidden(bool bf16, const void* h_root, const void* h_rows, const int* slot, const int* Mdev, int B,

@@ -1208,6 +1208,45 @@ atspeed_status atspeed_align_step(atspeed_ctx* c, const atspeed_align_args* a, d
   return ATSPEED_OK;
 }
 
+atspeed_status atspeed_mixed_search(atspeed_ctx* c, float lambda, int32_t B, int32_t P, const int32_t* prefix,
+                                    int32_t* items, float* scores, int32_t* n_items, int32_t* step_items,
+                                    int32_t* step_lens, int32_t* step_n) {
+  if (!c) return fail(ATSPEED_E_INVALID, "ctx is null");
+  if (!items || !scores || !n_items) return fail(ATSPEED_E_INVALID, "null output");
+  if (!(lambda >= 0.f && lambda <= 1.f)) return fail(ATSPEED_E_INVALID, "mixed_search: lambda outside [0, 1]");
+  if ((step_items != nullptr) != (step_lens != nullptr) || (step_items != nullptr) != (step_n != nullptr))
+    return fail(ATSPEED_E_INVALID, "step_items, step_lens and step_n are given together or not at all");
+  if (!c->dft.present) return fail(ATSPEED_E_STATE, "context has no draft model");
+  ST_TRY(prefill_impl(c, B, P, prefix, nullptr, true));
+  const atspeed_config& cf = c->cfg;
+  const int L = cf.L, path_rows = std::max(1, cf.K * (L - 1));
+  if (step_n) HIP_TRY(hipMemsetAsync(step_n, 0, sizeof(int) * B, c->st));
+  for (int l = 0; l < L; ++l) {
+    // the Y_t paths alone, through the target and the draft
+    launch_tree_from_beams(c->state, c->tree, c->trie, B, cf.target.item_base, cf.codebook, L, c->st);
+    HIP_TRY(hipGetLastError());
+    ST_TRY(tree_forward(*c, nullptr, true));
+    HIP_TRY(hipMemsetAsync(c->lo, 0, sizeof(int) * B, c->st));
+    launch_plan_tree(c->tree, c->lo, c->state.npath, B, c->P, c->rows, nullptr, c->st);
+    HIP_TRY(hipGetLastError());
+    ST_TRY(forward(*c, c->dft, false, B * path_rows, path_rows, nullptr));
+    // the mixture into the draft's rows, then the strict TopK of the next level
+    if (l == 0) launch_mix_logprobs(c->dft.root, c->tgt.root, nullptr, B, 1, c->nitem, lambda, c->st);
+    else launch_mix_logprobs(c->dft.lp, c->tgt.lp, c->state.npath, B, c->Tmax, c->nitem, lambda, c->st);
+    HIP_TRY(hipGetLastError());
+    launch_verify_strict(c->state, c->tree, c->trie, c->dft.lp, c->dft.root, c->nitem, cf.codebook, L, c->keys,
+                         c->max_cand, c->acc_tmp, c->tafter_tmp, B, c->st);
+    HIP_TRY(hipGetLastError());
+    if (step_items) {
+      launch_append_beams(c->state, B, L, step_items, step_lens, step_n, c->st);
+      HIP_TRY(hipGetLastError());
+    }
+  }
+  c->dft_prefilled = false;   // the draft's root row now holds the mixture
+  c->drafted = false;
+  return write_lists(c, B, items, scores, n_items);
+}
+
 atspeed_status atspeed_set_timing(atspeed_ctx* c, int32_t enable) {
   if (!c) return fail(ATSPEED_E_INVALID, "ctx is null");
   HIP_TRY(fold_timing(*c));

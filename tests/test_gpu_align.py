@@ -397,3 +397,110 @@ def test_align_errors_leave_a_usable_context():
         assert np.isfinite(tr.step())
     finally:
         eng.close()
+
+
+def _search(eng, w, prefix, lam=None):
+    B, K, L = prefix.shape[0], w.K, w.L
+    out = (torch.zeros((B, K, L), dtype=torch.int32, device=DEV), torch.zeros((B, K), device=DEV),
+           torch.zeros(B, dtype=torch.int32, device=DEV), torch.zeros((B, K * L, L), dtype=torch.int32, device=DEV),
+           torch.zeros((B, K * L), dtype=torch.int32, device=DEV), torch.zeros(B, dtype=torch.int32, device=DEV))
+    if lam is None:
+        eng.atspeed_target_search(prefix, *out)
+    else:
+        eng.atspeed_mixed_search(lam, prefix, *out)
+    torch.cuda.synchronize()
+    return tuple(x.cpu().numpy() for x in out)
+
+
+def _level_paths(si, sl, sn, u, t):
+    return [tuple(int(c) for c in si[u, i, :t]) for i in range(sn[u]) if sl[u, i] == t]
+
+
+@pytest.mark.parametrize("reuse", [0, 1])
+def test_mixed_search_lambda_one_is_the_target_search(reuse):
+    from paper_2410_05165_amd.binding import Engine
+    e = env("small")
+    w = e["w"]
+    eng = Engine(w, e["tw"], e["dw"], e["cat"], reuse_tree_kv=reuse)
+    try:
+        prefix = torch.from_numpy(e["pre"]).to(DEV)
+        a = _search(eng, w, prefix)
+        b = _search(eng, w, prefix, 1.0)
+        for x, y in zip(a, b):
+            assert np.array_equal(x, y)
+        c = _search(eng, w, prefix, 0.5)
+        assert not np.array_equal(a[0], c[0])       # the mixture moves the lists
+    finally:
+        eng.close()
+
+
+@pytest.mark.parametrize("lam", [0.5, 0.2])
+def test_mixed_search_tiny_matches_oracle(lam):
+    """fp32: every level's beams equal the oracle's mixture beam search over its
+    own target and draft (fp64), outside a near-tie (the first differing level's
+    top-K decision has a margin below 1e-3, and the comparison stops there);
+    the final scores within 1e-4."""
+    from paper_2410_05165_amd.binding import Engine
+    from oracle.align import mixture_beam_search
+    e = env("tiny")
+    w = e["w"]
+    eng = Engine(w, e["tw"], e["dw"], e["cat"])
+    try:
+        prefix = torch.from_numpy(e["pre"]).to(DEV)
+        items, scores, n, si, sl, sn = _search(eng, w, prefix, lam)
+        o = oracle_user("tiny", 0)
+        log = []
+        levels = mixture_beam_search(lambda p: o["lp"]([p])[0], lambda p: o["lq"]([p])[0], e["trie"], w.K, w.L,
+                                     w.codebook, lam, log)
+        for t, lvl in enumerate(levels, 1):
+            got = sorted(_level_paths(si, sl, sn, 0, t))
+            want = sorted(p for p, _ in lvl)
+            if got != want:
+                assert log[t - 1].margin < 1e-3, (t, got, want)
+                print(f"[mixed tiny] level {t} differs at a near-tie (margin {log[t - 1].margin:.2e})")
+                return
+        gs = {tuple(int(c) for c in items[0, k]): float(scores[0, k]) for k in range(n[0])}
+        for p, s in levels[-1]:
+            assert abs(gs[p] - s) <= 1e-4, (p, gs[p], s)
+        print(f"[mixed tiny] lambda {lam}: all {w.L} levels equal the oracle")
+    finally:
+        eng.close()
+
+
+def test_mixed_search_small_level1_on_shared_rows():
+    """bf16: the first level of the mixture search equals the oracle's TopK of
+    the mixture of the GPU's own root rows (target and draft, from a prefill),
+    outside near-ties."""
+    from paper_2410_05165_amd.binding import Engine
+    from oracle.align import mixed_log
+    from oracle.search import top_boundary
+    e = env("small")
+    w = e["w"]
+    B, T, nit = w.batch, None, w.n_item_tokens
+    eng = Engine(w, e["tw"], e["dw"], e["cat"])
+    try:
+        prefix = torch.from_numpy(e["pre"]).to(DEV)
+        eng.atspeed_prefill(prefix)
+        T = eng.max_nodes
+        lp = torch.empty((B, T, nit), device=DEV)
+        tr = torch.empty((B, nit), device=DEV)
+        dr = torch.empty((B, nit), device=DEV)
+        eng.atspeed_logprobs(0, lp, tr)
+        eng.atspeed_logprobs(1, lp, dr)
+        TR, DR = tr.cpu().numpy().astype(np.float64), dr.cpu().numpy().astype(np.float64)
+        lam = 0.5
+        items, scores, n, si, sl, sn = _search(eng, w, prefix, lam)
+        equal = 0
+        for u in range(B):
+            m = mixed_log(DR[u], TR[u], lam)
+            cands = [((c,), float(m[c])) for c in e["trie"].children(())]
+            sel, margin, _ = top_boundary(cands, w.K)
+            got = sorted(_level_paths(si, sl, sn, u, 1))
+            if got != sorted(p for p, _ in sel):
+                assert margin < 1e-3, (u, margin)
+                continue
+            equal += 1
+        print(f"[mixed small] level 1: {equal} of {B} users equal, the rest at near-ties")
+        assert equal >= B - 2
+    finally:
+        eng.close()
