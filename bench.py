@@ -297,14 +297,16 @@ def cpu_baseline(w, tw, dw, pre, cat, gpu_items):
                        f"(bf16 vs fp64 logits); host cpus={os.cpu_count()}")
 
 
-def decode_bound_probe(eng, w, prefix, levels, steps):
-    """Target-only beam step at t = 1 (the K beams of every user forwarded, K*B
-    rows): the weights and the prefix KV cache stream once per step with little
-    arithmetic per byte, so it is HBM-bound; reports its algorithmic bytes/s."""
+def decode_bound_probe(eng, w, prefix, levels, steps, users=None):
+    """Target-only beam step at t = 1 (the K beams of each of the first ``users``
+    users forwarded, K rows per user): the weights and the prefix KV cache stream
+    once per step with little arithmetic per byte, so it is HBM-bound at few
+    users; reports its algorithmic bytes/s."""
     import torch
-    B, K, L = w.batch, w.K, w.L
-    eng.atspeed_prefill(prefix)
-    t1, nb1, p1, s1 = levels[0]
+    K, L = w.K, w.L
+    B = w.batch if users is None else users
+    eng.atspeed_prefill(prefix[:B].contiguous())
+    t1, nb1, p1, s1 = (x[:B] for x in levels[0])
     upload_tree(eng, [[tuple(int(c) for c in p1[u, k, :1]) for k in range(nb1[u])] for u in range(B)], B)
     rows = int(nb1.sum())
 
@@ -323,8 +325,9 @@ def decode_bound_probe(eng, w, prefix, levels, steps):
     weights = m.n_layers * (4 * m.d_model ** 2 + 3 * m.d_model * m.d_ffn) * 2 + w.n_item_tokens * m.d_model * 2
     kv = m.n_layers * 2 * B * w.prefix_len * m.d_model * 2
     gbs = (weights + kv) / (ms * 1e-3) / 1e9
-    log(f"decode-bound probe: {rows} rows, {ms:.2f} ms/step, {gbs:.0f} GB/s ({gbs / PEAK_HBM_GBS:.1%} of HBM)")
-    return dict(rows=rows, ms_per_step=round(ms, 3), bytes=weights + kv, gbs=round(gbs, 1),
+    log(f"decode-bound probe: {B} users, {rows} rows, {ms:.2f} ms/step, {gbs:.0f} GB/s "
+        f"({gbs / PEAK_HBM_GBS:.1%} of HBM)")
+    return dict(users=B, rows=rows, ms_per_step=round(ms, 3), bytes=weights + kv, gbs=round(gbs, 1),
                 hbm_frac=round(gbs / PEAK_HBM_GBS, 4),
                 what="target-only beam step at t=1: target weights + prefix KV read once per step")
 
@@ -790,6 +793,7 @@ def main():
 
     if mode == 0 and "probe" in sections:
         extras["decode_bound"] = decode_bound_probe(eng, w, prefix, levels, max(3, args.steps // 2))
+        extras["decode_bound_one_user"] = decode_bound_probe(eng, w, prefix, levels, max(3, args.steps // 2), users=1)
 
     eng.close()
 

@@ -706,6 +706,18 @@ constexpr Shape kResidShapes[] = {
 // (three) to 128; o and down 64x32 (six) to 128 rows, 15 and 30 instead of 22
 // and 50 us at 1-64 rows.
 constexpr int kFewRowsQkv = 128, kFewRowsGu = 128, kFewRowsResid = 128;
+// A little above that (a prompt of one user, the verify tree of a few): one
+// M-tile of 192 rows over all the rows, split among four waves so that every
+// SIMD of a CU issues MFMAs (the two-wave tiles of the same height leave half
+// of them idle), and each weight slice crosses the chip once.  Measured at the
+// 7B projections with cold weights, 129-192 rows: q/k/v 192x64 of 2x2 waves
+// (four stages) 45-49 instead of 55-60 us, gate/up 192x128 of 2x2 waves (four
+// stages, the whole 160 KB of LDS) 55-59 instead of 65-69, o and down 256x32
+// of four waves in a column (four stages) 23-24 and 49-54 instead of 24-25
+// and 52-55; at 193-256 rows q/k/v 256x64 of 4x2 waves (three stages) 51-54
+// instead of 57-60 and o/down 192x64 of 2x2 waves (four stages) 54-56 instead
+// of 56-61 us for down.  Above 256 rows the shapes below are as fast or faster.
+constexpr int kMidRows = 192, kMidRows2 = 256;
 
 template <int NSH>
 int pick_shape(const Shape (&sh)[NSH], int M, int N, int K, int kparts, float partial) {
@@ -730,6 +742,8 @@ hipError_t gemm(const GemmCall& g, hipStream_t st) {
       case GEMM_QKV:
         if (M <= 32) return launch_bf16<BMAP_QKV, EPI_QKV, 1, 2, 1, 1, 6>(g, st);
         if (M <= kFewRowsQkv) return launch_bf16<BMAP_QKV, EPI_QKV, 2, 1, 1, 2, 4>(g, st);
+        if (M <= kMidRows) return launch_bf16<BMAP_QKV, EPI_QKV, 2, 2, 3, 1, 4>(g, st);
+        if (M <= kMidRows2) return launch_bf16<BMAP_QKV, EPI_QKV, 4, 2, 2, 1, 3>(g, st);
         switch (pick_shape(kQkvShapes, M, g.N, g.K, 1, 1.f)) {
           case 0: return launch_bf16<BMAP_QKV, EPI_QKV, 4, 2, 2, 4>(g, st);
           case 1: return launch_bf16<BMAP_QKV, EPI_QKV, 4, 2, 1, 4, 3>(g, st);
@@ -741,6 +755,7 @@ hipError_t gemm(const GemmCall& g, hipStream_t st) {
         if (M <= 32) return launch_bf16<BMAP_GU, EPI_GU, 2, 1, 1, 2, 4>(g, st);
         if (M <= 64) return launch_bf16<BMAP_GU, EPI_GU, 2, 2, 1, 2, 4>(g, st);
         if (M <= kFewRowsGu) return launch_bf16<BMAP_GU, EPI_GU, 2, 1, 1, 2, 3>(g, st);
+        if (M <= kMidRows) return launch_bf16<BMAP_GU, EPI_GU, 2, 2, 3, 2, 4>(g, st);
         switch (pick_shape(kGuShapes, M, g.N, g.K, 1, 1.f)) {
           case 0: return launch_bf16<BMAP_GU, EPI_GU, 4, 2, 2, 4>(g, st);
           case 1: return launch_bf16<BMAP_GU, EPI_GU, 4, 2, 1, 4, 3>(g, st);
@@ -748,6 +763,8 @@ hipError_t gemm(const GemmCall& g, hipStream_t st) {
         }
       case GEMM_RESID:
         if (M <= kFewRowsResid) return launch_bf16<BMAP_PLAIN, EPI_RESID, 2, 1, 1, 1, 6>(g, st);
+        if (M <= kMidRows) return launch_bf16<BMAP_PLAIN, EPI_RESID, 4, 1, 2, 1, 4>(g, st);
+        if (M <= kMidRows2) return launch_bf16<BMAP_PLAIN, EPI_RESID, 2, 2, 3, 1, 4>(g, st);
         switch (pick_shape(kResidShapes, M, g.N, g.K, g.part ? 2 : 1, 0.5f)) {
           case 0: return launch_bf16<BMAP_PLAIN, EPI_RESID, 4, 2, 2, 4>(g, st);
           case 1: return launch_bf16<BMAP_PLAIN, EPI_RESID, 4, 2, 2, 2>(g, st);
