@@ -704,8 +704,12 @@ constexpr Shape kResidShapes[] = {
 // 32 rows, 27 instead of 54 us, and 64x64 (four) to 128 rows; gate/up 64x64
 // (four) to 32 rows, 42-45 instead of 60-64 us, 64x128 (four) to 64, 64x64
 // (three) to 128; o and down 64x32 (six) to 128 rows, 15 and 30 instead of 22
-// and 50 us at 1-64 rows.
-constexpr int kFewRowsQkv = 128, kFewRowsGu = 128, kFewRowsResid = 128;
+// and 50 us at 1-64 rows.  From 65 rows one M-tile of 128 rows split over four
+// waves beats two of 64 (measured at 80-128 rows with warm clocks): q/k/v
+// 128x64 of 2x2 waves 34-38 instead of 38-44 us, gate/up 128x128 of 2x2 waves
+// 48-53 instead of 55-61, o and down 128x32 of four waves in a column 17-18
+// and 35-39 instead of 17-18 and 36-42 (all four stages).
+constexpr int kFewRowsQkv = 128, kFewRowsGu = 128, kFewRowsResid = 128, kNarrowRows = 64;
 // A little above that (a prompt of one user, the verify tree of a few): one
 // M-tile of 192 rows over all the rows, split among four waves so that every
 // SIMD of a CU issues MFMAs (the two-wave tiles of the same height leave half
@@ -741,7 +745,8 @@ hipError_t gemm(const GemmCall& g, hipStream_t st) {
     switch (g.kind) {
       case GEMM_QKV:
         if (M <= 32) return launch_bf16<BMAP_QKV, EPI_QKV, 1, 2, 1, 1, 6>(g, st);
-        if (M <= kFewRowsQkv) return launch_bf16<BMAP_QKV, EPI_QKV, 2, 1, 1, 2, 4>(g, st);
+        if (M <= kNarrowRows) return launch_bf16<BMAP_QKV, EPI_QKV, 2, 1, 1, 2, 4>(g, st);
+        if (M <= kFewRowsQkv) return launch_bf16<BMAP_QKV, EPI_QKV, 2, 2, 2, 1, 4>(g, st);
         if (M <= kMidRows) return launch_bf16<BMAP_QKV, EPI_QKV, 2, 2, 3, 1, 4>(g, st);
         if (M <= kMidRows2) return launch_bf16<BMAP_QKV, EPI_QKV, 4, 2, 2, 1, 3>(g, st);
         switch (pick_shape(kQkvShapes, M, g.N, g.K, 1, 1.f)) {
@@ -753,8 +758,8 @@ hipError_t gemm(const GemmCall& g, hipStream_t st) {
         }
       case GEMM_GU:
         if (M <= 32) return launch_bf16<BMAP_GU, EPI_GU, 2, 1, 1, 2, 4>(g, st);
-        if (M <= 64) return launch_bf16<BMAP_GU, EPI_GU, 2, 2, 1, 2, 4>(g, st);
-        if (M <= kFewRowsGu) return launch_bf16<BMAP_GU, EPI_GU, 2, 1, 1, 2, 3>(g, st);
+        if (M <= kNarrowRows) return launch_bf16<BMAP_GU, EPI_GU, 2, 2, 1, 2, 4>(g, st);
+        if (M <= kFewRowsGu) return launch_bf16<BMAP_GU, EPI_GU, 2, 2, 2, 2, 4>(g, st);
         if (M <= kMidRows) return launch_bf16<BMAP_GU, EPI_GU, 2, 2, 3, 2, 4>(g, st);
         switch (pick_shape(kGuShapes, M, g.N, g.K, 1, 1.f)) {
           case 0: return launch_bf16<BMAP_GU, EPI_GU, 4, 2, 2, 4>(g, st);
@@ -762,7 +767,8 @@ hipError_t gemm(const GemmCall& g, hipStream_t st) {
           default: return launch_bf16<BMAP_GU, EPI_GU, 1, 2, 2, 4>(g, st);
         }
       case GEMM_RESID:
-        if (M <= kFewRowsResid) return launch_bf16<BMAP_PLAIN, EPI_RESID, 2, 1, 1, 1, 6>(g, st);
+        if (M <= kNarrowRows) return launch_bf16<BMAP_PLAIN, EPI_RESID, 2, 1, 1, 1, 6>(g, st);
+        if (M <= kFewRowsResid) return launch_bf16<BMAP_PLAIN, EPI_RESID, 4, 1, 1, 1, 4>(g, st);
         if (M <= kMidRows) return launch_bf16<BMAP_PLAIN, EPI_RESID, 4, 1, 2, 1, 4>(g, st);
         if (M <= kMidRows2) return launch_bf16<BMAP_PLAIN, EPI_RESID, 2, 2, 3, 1, 4>(g, st);
         switch (pick_shape(kResidShapes, M, g.N, g.K, g.part ? 2 : 1, 0.5f)) {
