@@ -141,3 +141,36 @@ def test_few_row_tiles_are_batch_invariant():
                     assert (x[0] == y[u]).all(), (u, search)
     finally:
         eng.close()
+
+
+def test_tile_shapes_by_row_count_are_batch_invariant():
+    """At the 7B widths: a user's prefill alone runs P target rows, inside the
+    32-user batch P + 31 (P - shared) rows, so the two take different GEMM tile
+    shapes (narrow tiles to 64 rows, tall four-wave tiles at 65-128, 129-192 and
+    193-256, the cost model's wide tiles above).  Its root logits are bitwise the
+    same either way, for prefix lengths that put the lone user in each range."""
+    from paper_2410_05165_amd.binding import Engine
+    from synth import get_workload, make_catalog, make_prefixes, make_weights
+    w = get_workload("b7")
+    w = w.with_(target=w.target.__class__(2, 4096, 32, 11008, w.target.vocab, w.target.item_base), hist_items=48)
+    cat = make_catalog(w)
+    pre = make_prefixes(w, cat)
+    assert pre.shape[1] >= 256
+    print("[tiles] weights of a two-layer 7B-width target", flush=True)
+    eng = Engine(w, make_weights(w, "target"), make_weights(w, "draft"), cat, max_prefix=pre.shape[1])
+    try:
+        nv = w.L * w.codebook
+        for P in (40, 100, 160, 220, 256):
+            prefix = torch.from_numpy(np.ascontiguousarray(pre[:, :P])).to(DEV)
+            batch = torch.zeros((w.batch, nv), dtype=torch.float32, device=DEV)
+            eng.atspeed_prefill(prefix, batch)
+            torch.cuda.synchronize()
+            for u in (0, 31):
+                print(f"[tiles] P={P} user {u} alone", flush=True)
+                one = torch.zeros((1, nv), dtype=torch.float32, device=DEV)
+                eng.atspeed_prefill(prefix[u:u + 1].contiguous(), one)
+                torch.cuda.synchronize()
+                assert torch.isfinite(one).all()
+                assert torch.equal(one[0], batch[u]), (P, u)
+    finally:
+        eng.close()
