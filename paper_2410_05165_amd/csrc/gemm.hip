@@ -722,6 +722,7 @@ constexpr int kFewRowsQkv = 128, kFewRowsGu = 128, kFewRowsResid = 128, kNarrowR
 // instead of 57-60 and o/down 192x64 of 2x2 waves (four stages) 54-56 instead
 // of 56-61 us for down.  Above 256 rows the shapes below are as fast or faster.
 constexpr int kMidRows = 192, kMidRows2 = 256;
+constexpr int kHeadFewRows = 320;
 
 template <int NSH>
 int pick_shape(const Shape (&sh)[NSH], int M, int N, int K, int kparts, float partial) {
@@ -779,6 +780,11 @@ hipError_t gemm(const GemmCall& g, hipStream_t st) {
           default: return launch_bf16<BMAP_PLAIN, EPI_RESID, 2, 2, 2, 2, 3>(g, st);
         }
       default:
+        // the item rows of the output head (1,024 columns): up to a few hundred
+        // rows 64x32 tiles of two waves with six stages give twice the
+        // workgroups of the model's pick and stream the head in 20-22 instead of
+        // 32-37 us (1-320 rows, warm clocks)
+        if (M <= kHeadFewRows) return launch_bf16<BMAP_PLAIN, EPI_STORE, 2, 1, 1, 1, 6>(g, st);
         switch (pick_shape(kRowShapes, M, g.N, g.K, 1, 0.5f)) {
           case 0: return launch_bf16<BMAP_PLAIN, EPI_STORE, 4, 2, 2, 4>(g, st);
           case 1: return launch_bf16<BMAP_PLAIN, EPI_STORE, 4, 2, 2, 2>(g, st);
