@@ -697,18 +697,21 @@ constexpr Shape kResidShapes[] = {
 
 // Few rows (a decode level of a few users, the verify tree of one user): the
 // weight stream is the whole cost, and the tiles above leave most CUs idle (a
-// 256-column tile gives q/k/v 48 workgroups).  Narrow tiles of two waves with
-// four to six LDS stages give 190-380 workgroups, each streaming a thin weight
-// slice; their crossover row counts against the shapes above, measured at the
-// 7B projections with cold weights (1-192 rows): q/k/v 32x64 (six stages) to
-// 32 rows, 27 instead of 54 us, and 64x64 (four) to 128 rows; gate/up 64x64
-// (four) to 32 rows, 42-45 instead of 60-64 us, 64x128 (four) to 64, 64x64
-// (three) to 128; o and down 64x32 (six) to 128 rows, 15 and 30 instead of 22
-// and 50 us at 1-64 rows.  From 65 rows one M-tile of 128 rows split over four
-// waves beats two of 64 (measured at 80-128 rows with warm clocks): q/k/v
-// 128x64 of 2x2 waves 34-38 instead of 38-44 us, gate/up 128x128 of 2x2 waves
-// 48-53 instead of 55-61, o and down 128x32 of four waves in a column 17-18
-// and 35-39 instead of 17-18 and 36-42 (all four stages).
+// 256-column tile gives q/k/v 48 workgroups).  Narrow tiles with four to six
+// LDS stages give 190-380 workgroups, each streaming a thin weight slice.
+// Measured at the 7B projections (1-256 rows, cold weights, warm clocks), with
+// the time of the cost model's shape in parentheses:
+//   1-32 rows    q/k/v 32x64 of two waves (six stages) 26-28 us (54); gate/up
+//                64x64 of two waves (four) 42-43 (60-64); o and down 64x32 of
+//                two waves (six) 15 and 30 (22 and 50);
+//   33-64        q/k/v 64x64 of 2x2 waves of 32x32 (four) 28-31 (two waves of
+//                32x64: 32-34); gate/up 64x128 of 2x2 waves (four) 44-45; o and
+//                down as above;
+//   65-128       one M-tile of 128 rows over four waves instead of two 64-row
+//                tiles: q/k/v 128x64 of 2x2 waves 34-38 (38-44), gate/up
+//                128x128 of 2x2 waves 48-53 (55-61), o and down 128x32 of four
+//                waves in a column 17-18 and 35-39 (17-18 and 36-42), all four
+//                stages.
 constexpr int kFewRowsQkv = 128, kFewRowsGu = 128, kFewRowsResid = 128, kNarrowRows = 64;
 // A little above that (a prompt of one user, the verify tree of a few): one
 // M-tile of 192 rows over all the rows, split among four waves so that every
@@ -746,7 +749,7 @@ hipError_t gemm(const GemmCall& g, hipStream_t st) {
     switch (g.kind) {
       case GEMM_QKV:
         if (M <= 32) return launch_bf16<BMAP_QKV, EPI_QKV, 1, 2, 1, 1, 6>(g, st);
-        if (M <= kNarrowRows) return launch_bf16<BMAP_QKV, EPI_QKV, 2, 1, 1, 2, 4>(g, st);
+        if (M <= kNarrowRows) return launch_bf16<BMAP_QKV, EPI_QKV, 2, 2, 1, 1, 4>(g, st);
         if (M <= kFewRowsQkv) return launch_bf16<BMAP_QKV, EPI_QKV, 2, 2, 2, 1, 4>(g, st);
         if (M <= kMidRows) return launch_bf16<BMAP_QKV, EPI_QKV, 2, 2, 3, 1, 4>(g, st);
         if (M <= kMidRows2) return launch_bf16<BMAP_QKV, EPI_QKV, 4, 2, 2, 1, 3>(g, st);
