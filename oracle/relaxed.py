@@ -58,7 +58,9 @@ follow min(p, q)); its parts are pinned where they reduce to a known law: with
 N = K = 1 it is Leviathan et al.'s speculative sampling, whose output follows
 pi_p exactly; with q = p every draft passes and the kept K are a uniform subset
 of the N drafts; q = p accepts every level.  The composite law with 0 < passes
-< K stays parity unpinned beyond GPU-vs-oracle agreement on the same streams.
+< K is pinned by its exact enumeration on a six-code level (every ordered draft
+set, acceptance pattern, kept subset and residual redraw weighed by its
+probability), against which the oracle's outcomes pass a chi-square test.
 """
 from __future__ import annotations
 

@@ -169,3 +169,122 @@ def test_paper_mode_keeps_a_uniform_subset_when_k_pass():
     chi2 = sum((c - exp) ** 2 / exp for c in counts.values())
     # chi-square with 2 dof, alpha = 1e-3: 13.82
     assert chi2 < 13.82, counts
+
+
+def _paper_level_law(p, q, N, K):
+    """Exact output law of one RELAXED_PAPER level (Algorithm 2 read with N
+    distinct drafts) by enumeration: the N drafts as every ordered draw without
+    replacement from q (probability prod q(y_i) / (1 - q(y_1) - ... - q(y_{i-1}))),
+    each accepted independently with probability min(1, p/q); with at least K
+    accepted, each K-subset of them equally likely and the level accepted;
+    otherwise the accepted ones plus K - #accepted distinct ordered draws without
+    replacement from max(0, p - q) with the accepted ones zeroed (all of its
+    support if that holds fewer), the level rejected.  Returns
+    {(accepted, frozenset of beams): probability}."""
+    import itertools
+    C = len(p)
+    law = {}
+
+    def add(key, pr):
+        law[key] = law.get(key, 0.0) + pr
+
+    for perm in itertools.permutations(range(C), N):
+        pd, rest = 1.0, 1.0
+        for y in perm:
+            pd *= q[y] / rest
+            rest -= q[y]
+        for mask in itertools.product((0, 1), repeat=N):
+            pr = pd
+            for y, m in zip(perm, mask):
+                a = min(1.0, p[y] / q[y])
+                pr *= a if m else 1.0 - a
+            if pr == 0.0:
+                continue
+            A = [y for y, m in zip(perm, mask) if m]
+            if len(A) >= K:
+                subs = list(itertools.combinations(A, K))
+                for s in subs:
+                    add((True, frozenset(s)), pr / len(subs))
+                continue
+            r = [0.0 if c in A else max(0.0, p[c] - q[c]) for c in range(C)]
+            pos = [c for c in range(C) if r[c] > 0.0]
+            B = K - len(A)
+            if len(pos) <= B:
+                add((False, frozenset(A) | frozenset(pos)), pr)
+                continue
+            for draw in itertools.permutations(pos, B):
+                pw, rest = 1.0, sum(r)
+                for c in draw:
+                    pw *= r[c] / rest
+                    rest -= r[c]
+                add((False, frozenset(A) | frozenset(draw)), pr * pw)
+    return law
+
+
+def _explicit_tables(p, q, cb):
+    """Scorers whose level-1 distributions are exactly p (target) and q (draft)
+    over cb codes, with a uniform second level."""
+    def tab(d):
+        t = {(): np.concatenate([np.log(np.asarray(d, dtype=np.float64)), np.full(cb, -50.0)])}
+        for c in range(cb):
+            t[(c,)] = np.concatenate([np.full(cb, -50.0), np.full(cb, -math.log(cb))])
+        return table_scorer(t)
+    return tab(p), tab(q)
+
+
+LAW_CASES = {
+    # the draft favours what the target does not: most drafts fail, a few pass
+    "reversed": ([0.30, 0.25, 0.20, 0.12, 0.08, 0.05], [0.05, 0.10, 0.15, 0.20, 0.22, 0.28]),
+    # partly aligned: passes of one to all four drafts all carry weight
+    "shifted": ([0.22, 0.20, 0.18, 0.16, 0.14, 0.10], [0.10, 0.28, 0.12, 0.25, 0.05, 0.20]),
+}
+
+
+@pytest.mark.parametrize("case", list(LAW_CASES))
+def test_paper_mode_level_law_matches_enumeration(case):
+    """The composite law of a RELAXED_PAPER level, where some but fewer than K
+    of the N drafts pass: over many Philox streams the oracle's (accepted,
+    level-1 beam set) outcomes follow the law enumerated exactly from pi_p and
+    pi_q (chi-square).  Mistakes that leave the special cases N = K = 1 and
+    q = p intact -- not zeroing the accepted drafts in the residual, ">" instead
+    of ">=", keeping the first K accepted, a residual drawn with replacement --
+    move this law."""
+    p0, q0 = LAW_CASES[case]
+    cb = len(p0)
+    trie = Trie(np.array([[a, b] for a in range(cb) for b in range(cb)]))
+    lp, lq = _explicit_tables(p0, q0, cb)
+    paths, logp, _ = level_dist([((), 0.0)], lp, trie, cb, 1.0)
+    _, logq, _ = level_dist([((), 0.0)], lq, trie, cb, 1.0)
+    p, q = np.exp(logp), np.exp(logq)
+    assert np.allclose(p, p0) and np.allclose(q, q0)
+    N, K, runs = 4, 3, 12000
+    law = _paper_level_law(p, q, N, K)
+    assert abs(sum(law.values()) - 1.0) < 1e-12
+    # the composite regime carries weight: some but fewer than K drafts pass
+    assert sum(v for (ok, s), v in law.items() if not ok) > 0.2
+    counts = {}
+    for r in range(runs):
+        rs = Streams((r, 31337), 0)
+        D = draft_paper(lq, trie, [()], [0.0], 1, N, cb, 1.0, rs, 0)
+        res = verify_paper(lp, lq, trie, [((), 0.0)], [0.0], D, K, 2, cb, 1.0, rs, 0)
+        key = (res.accepted == 1, frozenset(paths.index(b) for b, _ in res.levels[0]))
+        counts[key] = counts.get(key, 0) + 1
+    assert set(counts) <= set(law), set(counts) - set(law)
+    # bins with an expected count below 5 pooled into one
+    exp_, obs_ = [], []
+    small_e = small_o = 0.0
+    for key, pr in law.items():
+        if runs * pr < 5:
+            small_e += runs * pr
+            small_o += counts.get(key, 0)
+        else:
+            exp_.append(runs * pr)
+            obs_.append(counts.get(key, 0))
+    if small_e > 0:
+        exp_.append(small_e)
+        obs_.append(small_o)
+    exp_, obs_ = np.array(exp_), np.array(obs_, dtype=float)
+    chi2 = float(((obs_ - exp_) ** 2 / exp_).sum())
+    from scipy.stats import chi2 as chi2_dist
+    crit = float(chi2_dist.ppf(1 - 1e-3, len(exp_) - 1))
+    assert chi2 < crit, (chi2, crit, counts, law)
