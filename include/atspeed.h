@@ -398,7 +398,7 @@ ATSPEED_API atspeed_status atspeed_align_data(atspeed_ctx* ctx, int32_t S, const
  * draft.  Synchronises the stream. */
 ATSPEED_API atspeed_status atspeed_align_step(atspeed_ctx* ctx, const atspeed_align_args* args, double* loss_host);
 
-/* State access (host arrays; synchronise the stream)./* State access (host arrays; synchronise the stream).  t [B]; nbeams [B];
+/* State access (host arrays; synchronise the stream).  t [B]; nbeams [B];
  * paths [B, K, L] codes (entries past depth t undefined); scores [B, K] fp32. */
 ATSPEED_API atspeed_status atspeed_get_state(atspeed_ctx* ctx, int32_t B, int32_t* t, int32_t* nbeams,
                                  int32_t* paths, float* scores);
