@@ -69,6 +69,27 @@ def rope(x: np.ndarray, pos: np.ndarray, base: float = ROPE_BASE) -> np.ndarray:
     return np.concatenate([a * c - b * s, b * c + a * s], axis=-1)
 
 
+def attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, mask: np.ndarray,
+           pk: Optional[np.ndarray] = None, pv: Optional[np.ndarray] = None) -> np.ndarray:
+    """Multi-head attention with scale 1/sqrt(d_head): queries ``q`` [S, H, T, dh]
+    attend to the prefix keys/values ``pk``/``pv`` [H, P, dh] (if given) and to
+    their own sequence's keys ``k``/``v`` [S, H, T, dh] where ``mask`` [T, T]
+    allows.  Returns [S, H, T, dh]."""
+    dh = q.shape[-1]
+    sc = (q @ k.transpose(0, 1, 3, 2)) / np.sqrt(dh)                 # [S, H, T, T]
+    sc = np.where(mask[None, None], sc, -np.inf)
+    if pk is not None:
+        sp = np.einsum("shtd,hpd->shtp", q, pk) / np.sqrt(dh)
+        sc = np.concatenate([sp, sc], axis=-1)
+    m = np.max(sc, axis=-1, keepdims=True)
+    e = np.exp(sc - m)
+    pr = e / np.sum(e, axis=-1, keepdims=True)
+    if pk is not None:
+        P = pk.shape[1]
+        return np.einsum("shtp,hpd->shtd", pr[..., :P], pv) + pr[..., P:] @ v
+    return pr @ v
+
+
 class PrefixCache:
     """Per-layer K/V of a user's prefix (after RoPE and rounding), [H, P, dh]."""
 
@@ -118,46 +139,68 @@ class Decoder:
         itself, to the keys allowed by ``mask`` [T, T] (default: causal).
         Returns (item logits [S, T, n_item], per-layer (k, v) if keep_kv).
         """
-        d = self.dims
-        S, T = tokens.shape
-        H, dh = d.n_heads, d.d_head
+        T = tokens.shape[1]
         if mask is None:
             mask = np.tril(np.ones((T, T), dtype=bool))
         x = self.embed(tokens)                                          # [S, T, d]
         kvs = []
-        for l in range(d.n_layers):
-            p = f"l{l}."
-            h = self._r(rmsnorm(x, self.W(p + "attn_norm")))
-            q = (h @ self.W(p + "wq").T).reshape(S, T, H, dh).transpose(0, 2, 1, 3)   # [S, H, T, dh]
-            k = (h @ self.W(p + "wk").T).reshape(S, T, H, dh).transpose(0, 2, 1, 3)
-            v = (h @ self.W(p + "wv").T).reshape(S, T, H, dh).transpose(0, 2, 1, 3)
-            q = self._r(rope(q, pos))
-            k = self._r(rope(k, pos))
-            v = self._r(v)
+        for l in range(self.dims.n_layers):
+            _, x, k, v = self.block(l, x, pos, prefix.k[l] if prefix is not None else None,
+                                    prefix.v[l] if prefix is not None else None, mask)
             if keep_kv:
                 kvs.append((k, v))
-            sc = (q @ k.transpose(0, 1, 3, 2)) / np.sqrt(dh)                 # [S, H, T, T]
-            sc = np.where(mask[None, None], sc, -np.inf)
-            if prefix is not None:
-                pk, pv = prefix.k[l], prefix.v[l]                               # [H, P, dh]
-                sp = np.einsum("shtd,hpd->shtp", q, pk) / np.sqrt(dh)
-                sc = np.concatenate([sp, sc], axis=-1)
-            m = np.max(sc, axis=-1, keepdims=True)
-            e = np.exp(sc - m)
-            pr = e / np.sum(e, axis=-1, keepdims=True)
-            if prefix is not None:
-                P = prefix.length
-                o = np.einsum("shtp,hpd->shtd", pr[..., :P], prefix.v[l]) + pr[..., P:] @ v
-            else:
-                o = pr @ v
-            o = self._r(o.transpose(0, 2, 1, 3).reshape(S, T, d.d_model))
-            x = x + o @ self.W(p + "wo").T
-            h2 = self._r(rmsnorm(x, self.W(p + "ffn_norm")))
-            a = self._r(silu(h2 @ self.W(p + "w_gate").T) * (h2 @ self.W(p + "w_up").T))
-            x = x + a @ self.W(p + "w_down").T
-        hf = self._r(rmsnorm(x, self.W("final_norm")))
-        logits = hf @ self.W("lm_head_item").T
-        return logits, kvs
+        return self.head(x), kvs
+
+    def head(self, x: np.ndarray) -> np.ndarray:
+        """Item logits of residual-stream rows: final RMSNorm, then the item rows of the output head."""
+        return self._r(self.norm(-1, "", x)) @ self.W("lm_head_item").T
+
+    def block(self, l: int, x: np.ndarray, pos: np.ndarray, pk: Optional[np.ndarray] = None,
+              pv: Optional[np.ndarray] = None, mask: Optional[np.ndarray] = None):
+        """Decoder block ``l`` on the residual stream ``x`` [S, T, d] at positions
+        ``pos`` [T]: every sequence attends to the prefix keys ``pk``/``pv``
+        [H, P, dh] (if given) and, within itself, to the keys ``mask`` [T, T]
+        allows (default: causal).  Returns (h, x_out, k, v): the residual after
+        the attention sublayer, after the FFN sublayer, and this block's k, v
+        [S, H, T, dh] after RoPE and rounding."""
+        S, T = x.shape[0], x.shape[1]
+        if mask is None:
+            mask = np.tril(np.ones((T, T), dtype=bool))
+        p = f"l{l}."
+        hn = self._r(self.norm(l, "attn_norm", x))
+        q, k, v = (self._r(a) for a in self.qkv(l, hn, pos))
+        o = self._r(self.merge_heads(attend(q, k, v, mask, pk, pv)))
+        h = x + o @ self.W(p + "wo").T
+        h2 = self._r(self.norm(l, "ffn_norm", h))
+        a = self._r(self.swiglu(l, h2))
+        return h, h + a @ self.W(p + "w_down").T, k, v
+
+    # -- the steps of a block (unrounded results; the block rounds them where
+    #    the bf16 model does)
+    def norm(self, l: int, which: str, x: np.ndarray) -> np.ndarray:
+        """RMSNorm of layer ``l`` (``which``: attn_norm or ffn_norm; l < 0: the final norm)."""
+        return rmsnorm(x, self.W("final_norm" if l < 0 else f"l{l}.{which}"))
+
+    def qkv(self, l: int, hn: np.ndarray, pos: np.ndarray):
+        """q, k (after RoPE) and v [S, H, T, dh] of the normalised rows ``hn`` [S, T, d]."""
+        d = self.dims
+        S, T = hn.shape[0], hn.shape[1]
+        H, dh = d.n_heads, d.d_head
+        p = f"l{l}."
+        q = (hn @ self.W(p + "wq").T).reshape(S, T, H, dh).transpose(0, 2, 1, 3)
+        k = (hn @ self.W(p + "wk").T).reshape(S, T, H, dh).transpose(0, 2, 1, 3)
+        v = (hn @ self.W(p + "wv").T).reshape(S, T, H, dh).transpose(0, 2, 1, 3)
+        return rope(q, pos), rope(k, pos), v
+
+    def merge_heads(self, o: np.ndarray) -> np.ndarray:
+        """[S, H, T, dh] -> [S, T, d]."""
+        S, H, T, dh = o.shape
+        return o.transpose(0, 2, 1, 3).reshape(S, T, H * dh)
+
+    def swiglu(self, l: int, h2: np.ndarray) -> np.ndarray:
+        """SiLU(W_gate h2) * (W_up h2) of layer ``l``."""
+        p = f"l{l}."
+        return silu(h2 @ self.W(p + "w_gate").T) * (h2 @ self.W(p + "w_up").T)
 
     # -- prefix and paths
     def prefill(self, prefix_tokens: np.ndarray) -> PrefixCache:
