@@ -405,6 +405,34 @@ ATSPEED_API atspeed_status atspeed_get_state(atspeed_ctx* ctx, int32_t B, int32_
 ATSPEED_API atspeed_status atspeed_set_state(atspeed_ctx* ctx, int32_t B, const int32_t* t, const int32_t* nbeams,
                                  const int32_t* paths, const float* scores);
 
+/* Residual-stream and activation capture (instrumentation for kernel-by-kernel
+ * parity tests; the decoder block is the LLaMA block of the implementation
+ * details, Sec. 4.1, with tree-based attention, Sec. 3.3).  Arms the NEXT
+ * forward of the target model (in atspeed_prefill, atspeed_tree_logits,
+ * atspeed_verify or a decode) to copy, on the context's stream, the values of
+ * its forwarded rows at every rounding point of the block (R = max_rows):
+ *   x_dev   (device, fp32, [2 n_layers + 1][R][d_model]): index 2l is layer l's
+ *           input residual, 2l + 1 the residual after its attention sublayer,
+ *           2 n_layers the residual after the last layer (not written by a
+ *           prefill, whose final norm runs on each user's last row only);
+ *   act_dev (device, bf16 bit patterns, may be null; bf16 models only): per
+ *           layer l at element offset l R (6 d_model + d_ffn), six [R][d_model]
+ *           arrays -- the normalised input of q/k/v, q and k after RoPE, v, the
+ *           attention output, the normalised input of gate/up -- then SiLU(gate)
+ *           * up as [R][d_ffn]; after the layers (offset n_layers R (6 d_model +
+ *           d_ffn)) the final norm's output [R][d_model] (not written by a
+ *           prefill);
+ *   plan_dev (device, [3 R + 1] int32): each row's user, position and tree
+ *           slot (u * max_nodes + node; -1 for a prefix row) as three arrays of
+ *           R, then the forward's row count.
+ * Rows past R are not copied (check the row count).  The capture disarms itself
+ * after that forward; all three pointers null disarms it at once.
+ * ATSPEED_E_INVALID for a null x_dev or plan_dev with the others set,
+ * max_rows <= 0, or act_dev with an fp32 model.  Adds device copies to the
+ * forward; buffers are caller-owned. */
+ATSPEED_API atspeed_status atspeed_capture_hidden(atspeed_ctx* ctx, float* x_dev, void* act_dev, int32_t* plan_dev,
+                                                  int32_t max_rows);
+
 /* Kernel timing (instrumentation for measurement).  enable is a bit mask of the
  * kernel classes to time (bit ATSPEED_K_x; ATSPEED_TIME_ALL for every class),
  * optionally or-ed with ATSPEED_TIME_TARGET_ONLY:

@@ -21,6 +21,7 @@ STATUS = {0: "OK", 1: "E_INVALID", 2: "E_SHAPE", 3: "E_WORKSPACE", 4: "E_DEVICE"
 LAYER_ORDER = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down")
 SYMBOLS = ("atspeed_workspace_bytes", "atspeed_create", "atspeed_destroy", "atspeed_last_error",
            "atspeed_prefill", "atspeed_draft", "atspeed_get_tree", "atspeed_verify", "atspeed_tree_logits",
+           "atspeed_capture_hidden",
            "atspeed_accept", "atspeed_accept_noalloc", "atspeed_decode_topk", "atspeed_logprobs", "atspeed_get_state", "atspeed_set_state",
            "atspeed_set_timing", "atspeed_get_timing", "atspeed_align_data", "atspeed_align_step",
            "atspeed_target_search", "atspeed_mixed_search")
@@ -97,6 +98,7 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
     lib.atspeed_get_tree.argtypes = [vp, C.POINTER(Tree)]
     lib.atspeed_verify.argtypes = [vp, pi32, pi32, pf]
     lib.atspeed_tree_logits.argtypes = [vp, pf]
+    lib.atspeed_capture_hidden.argtypes = [vp, pf, vp, pi32, i32]
     lib.atspeed_accept.argtypes = [vp, pf, pf, pi32, pi32]
     lib.atspeed_accept_noalloc.argtypes = [vp, pf, pf, pi32, pi32]
     lib.atspeed_decode_topk.argtypes = [vp, i32, i32, pi32, pi32, pf, pi32, C.POINTER(Stats)]
@@ -232,6 +234,9 @@ class Engine:
 
     def atspeed_verify(self, accepted=None, t_after=None, logits=None):
         self._check(self.lib.atspeed_verify(self.ctx, _ptr(accepted), _ptr(t_after), _ptr(logits)))
+
+    def atspeed_capture_hidden(self, x=None, plan=None, max_rows=0, act=None):
+        self._check(self.lib.atspeed_capture_hidden(self.ctx, _ptr(x), _ptr(act), _ptr(plan), int(max_rows)))
 
     def atspeed_tree_logits(self, logits):
         self._check(self.lib.atspeed_tree_logits(self.ctx, _ptr(logits)))

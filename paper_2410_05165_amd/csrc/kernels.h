@@ -42,6 +42,8 @@ struct AttnCall {
 hipError_t attention(const AttnCall& a, hipStream_t st);
 
 // Misc
+hipError_t gather_kv_rows(const void* kc, const void* vc, const Rows& rows, int rmax, int kv_mode, int H, int dh,
+                          int Pmax, void* ko, void* vo, hipStream_t st);
 hipError_t embed(bool bf16, const void* emb, const Rows& rows, int Mmax, int d, float* x, hipStream_t st);
 // add (may be null): a k-split GEMM's second partial product, added to x first;
 // the sum is written back to x when row_index is null.

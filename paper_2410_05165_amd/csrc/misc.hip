@@ -15,6 +15,31 @@ __global__ void embed_kernel(const T* __restrict__ emb, const int* __restrict__ 
   }
 }
 
+// Copy of the k and v rows a forward wrote, in row order (instrumentation of
+// the residual capture): row r's k/v sit in the prefix cache [B][H][Pmax][dh]
+// at (user, position) (kv_mode 0) or in the tree K/V [slot][d] (kv_mode 1).
+__global__ void gather_kv_rows_kernel(const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc, Rows rows,
+                                      int rmax, int kv_mode, int H, int dh, int Pmax, bf16_t* __restrict__ ko,
+                                      bf16_t* __restrict__ vo) {
+  const int M = min(*rows.M, rmax), d = H * dh;
+  const size_t total = (size_t)M * d;
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < total; i += (size_t)gridDim.x * blockDim.x) {
+    const int r = (int)(i / d), c = (int)(i % d), head = c / dh, j = c % dh;
+    const size_t src = kv_mode == 0 ? (((size_t)rows.user[r] * H + head) * Pmax + rows.pos[r]) * dh + j
+                                    : (size_t)rows.slot[r] * d + c;
+    ko[i] = kc[src];
+    vo[i] = vc[src];
+  }
+}
+
+hipError_t gather_kv_rows(const void* kc, const void* vc, const Rows& rows, int rmax, int kv_mode, int H, int dh,
+                          int Pmax, void* ko, void* vo, hipStream_t st) {
+  const int blocks = (int)std::max<size_t>(1, std::min<size_t>(4096, ((size_t)rmax * H * dh + 255) / 256));
+  hipLaunchKernelGGL(gather_kv_rows_kernel, dim3(blocks), dim3(256), 0, st, (const bf16_t*)kc, (const bf16_t*)vc,
+                     rows, rmax, kv_mode, H, dh, Pmax, (bf16_t*)ko, (bf16_t*)vo);
+  return hipGetLastError();
+}
+
 hipError_t embed(bool bf16, const void* emb, const Rows& rows, int Mmax, int d, float* x, hipStream_t st) {
   int blocks = (int)std::min<size_t>(4096, ((size_t)Mmax * d + 255) / 256);
   if (blocks < 1) blocks = 1;

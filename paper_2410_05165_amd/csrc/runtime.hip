@@ -146,6 +146,11 @@ struct atspeed_ctx {
   int* fidx = nullptr;             // [B*Tmax] per user, the nodes still to forward
   int* fcnt = nullptr;             // [B]
   int64_t rows_fwd = 0;            // target tree rows forwarded (decode statistics)
+  // residual-stream capture of the next target forward (atspeed_capture_hidden)
+  float* cap_x = nullptr;        // [2 n_layers + 1][cap_rows][d] fp32
+  bf16_t* cap_act = nullptr;     // bf16 inputs of every GEMM and attention (layout at atspeed_capture_hidden)
+  int32_t* cap_plan = nullptr;   // [3][cap_rows] user, position, slot of each row; then the row count
+  int cap_rows = 0;
   // timing instrumentation
   uint32_t timing_mask = 0;   // kernel classes whose launches are bracketed by events
   bool timing_target_only = false;  // skip the draft model's launches
@@ -489,6 +494,29 @@ atspeed_status forward(atspeed_ctx& c, ModelRt& r, bool prefill, int Mmax, int T
     ~Current() { c.fwd_model = nullptr; }
   } current(c, r);
   const double M = Mmax;
+  // residual-stream capture (armed by atspeed_capture_hidden for one target
+  // forward): the row plan now, x at every sublayer boundary below
+  const bool cap = c.cap_x != nullptr && &r == &c.tgt;
+  const int crow = cap ? std::min(Mmax, c.cap_rows) : 0;
+  auto capture = [&](int idx) -> hipError_t {
+    return hipMemcpyAsync(c.cap_x + (size_t)idx * c.cap_rows * d, c.x, (size_t)crow * d * sizeof(float),
+                          hipMemcpyDeviceToDevice, st);
+  };
+  // bf16 activations: per layer [xn1 | q | k | v | ao | xn2] of [cap_rows][d], then a of [cap_rows][f];
+  // after the layers the final norm's output [cap_rows][d]
+  const bool cap_act = cap && c.cap_act != nullptr && c.bf16;
+  const size_t act_layer = (size_t)c.cap_rows * (6 * (size_t)d + f);
+  auto act = [&](int l, int part) -> bf16_t* { return c.cap_act + (size_t)l * act_layer + (size_t)part * c.cap_rows * d; };
+  auto capture_act = [&](int l, int part, const void* src, int width) -> hipError_t {
+    return hipMemcpyAsync(act(l, part), src, (size_t)crow * width * sizeof(bf16_t), hipMemcpyDeviceToDevice, st);
+  };
+  if (cap) {
+    const int* src[3] = {c.rows.user, c.rows.pos, c.rows.slot};
+    for (int i = 0; i < 3; ++i)
+      HIP_TRY(hipMemcpyAsync(c.cap_plan + (size_t)i * c.cap_rows, src[i], (size_t)crow * sizeof(int),
+                             hipMemcpyDeviceToDevice, st));
+    HIP_TRY(hipMemcpyAsync(c.cap_plan + (size_t)3 * c.cap_rows, c.rows.M, sizeof(int), hipMemcpyDeviceToDevice, st));
+  }
   MARK(ATSPEED_K_ROW);
   HIP_TRY(embed(c.bf16, r.emb, c.rows, Mmax, d, c.x, st));
   // bf16: the o and down projections split k at its midpoint (whole even
@@ -503,6 +531,8 @@ atspeed_status forward(atspeed_ctx& c, ModelRt& r, bool prefill, int Mmax, int T
     MARK(ATSPEED_K_ROW);
     HIP_TRY(rmsnorm(c.bf16, c.x, l > 0 ? part_down : nullptr, c.rows.M, Mmax, d, (const float*)w[0], c.xn, nullptr,
                     st));
+    if (cap) HIP_TRY(capture(2 * l));       // the layer's input (the previous k-split half added)
+    if (cap_act) HIP_TRY(capture_act(l, 0, c.xn, d));
     GemmCall g{};
     g.bf16 = c.bf16;
     g.Mmax = Mmax; g.Mdev = c.rows.M; g.scratch = c.scratch; g.rows = c.rows;
@@ -523,6 +553,11 @@ atspeed_status forward(atspeed_ctx& c, ModelRt& r, bool prefill, int Mmax, int T
       launch_broadcast_prefix_kv(pk, pv, B, H, (size_t)c.cfg.max_prefix * dh * es, (size_t)shared * dh * es, st);
       HIP_TRY(hipGetLastError());
     }
+    if (cap_act) {
+      HIP_TRY(capture_act(l, 1, c.q, d));
+      HIP_TRY(gather_kv_rows(prefill ? (void*)pk : (void*)tk, prefill ? (void*)pv : (void*)tv, c.rows, crow,
+                             prefill ? 0 : 1, H, dh, c.cfg.max_prefix, act(l, 2), act(l, 3), st));
+    }
     AttnCall at{};
     at.bf16 = c.bf16; at.q = c.q; at.pk = pk; at.pv = pv;
     at.tk = prefill ? nullptr : tk; at.tv = prefill ? nullptr : tv;
@@ -530,15 +565,19 @@ atspeed_status forward(atspeed_ctx& c, ModelRt& r, bool prefill, int Mmax, int T
     at.H = H; at.dh = dh; at.d = d; at.Pmax = c.cfg.max_prefix;
     MARK(ATSPEED_K_ATTN);
     HIP_TRY(attention(at, st));
+    if (cap_act) HIP_TRY(capture_act(l, 4, c.ao, d));
     g.kind = GEMM_RESID; g.A = c.ao; g.lda = d; g.N = d; g.K = d; g.w0 = w[4]; g.out = c.x; g.ldo = d;
     g.part = part_o;
     MARK_F(ATSPEED_K_O, 2.0 * M * d * d);
     HIP_TRY(gemm(g, st));
     MARK(ATSPEED_K_ROW);
     HIP_TRY(rmsnorm(c.bf16, c.x, part_o, c.rows.M, Mmax, d, (const float*)w[5], c.xn, nullptr, st));
+    if (cap) HIP_TRY(capture(2 * l + 1));   // after the attention sublayer
+    if (cap_act) HIP_TRY(capture_act(l, 5, c.xn, d));
     g.kind = GEMM_GU; g.A = c.xn; g.lda = d; g.N = 2 * f; g.K = d; g.w0 = w[6]; g.w1 = w[7]; g.split = f; g.hout = c.h;
     MARK_F(ATSPEED_K_GU, 2.0 * M * 2.0 * f * d);
     HIP_TRY(gemm(g, st));
+    if (cap_act) HIP_TRY(capture_act(l, 6, c.h, f));
     g.kind = GEMM_RESID; g.A = c.h; g.lda = f; g.N = d; g.K = f; g.w0 = w[8]; g.out = c.x; g.ldo = d;
     g.part = part_down;
     MARK_F(ATSPEED_K_DOWN, 2.0 * M * f * d);
@@ -549,6 +588,11 @@ atspeed_status forward(atspeed_ctx& c, ModelRt& r, bool prefill, int Mmax, int T
   const int Mmf = prefill ? B : Mmax;
   MARK(ATSPEED_K_ROW);
   HIP_TRY(rmsnorm(c.bf16, c.x, part_down, Mfin, Mmf, d, r.final_norm, c.xn, prefill ? c.row_last : nullptr, st));
+  // after the last layer (a prefill writes no whole residual back: its final
+  // norm runs on each user's last row only)
+  if (cap && !prefill) HIP_TRY(capture(2 * m.n_layers));
+  if (cap_act && !prefill) HIP_TRY(capture_act(m.n_layers, 0, c.xn, d));
+  if (cap) { c.cap_x = nullptr; c.cap_act = nullptr; c.cap_plan = nullptr; c.cap_rows = 0; }
   GemmCall g{};
   g.kind = GEMM_STORE; g.bf16 = c.bf16; g.A = c.xn; g.lda = d; g.Mmax = Mmf; g.Mdev = Mfin;
   g.N = c.nitem; g.K = d; g.w0 = r.lm_head; g.out = c.logits; g.ldo = c.nitem; g.scratch = c.scratch;
@@ -1245,6 +1289,19 @@ atspeed_status atspeed_mixed_search(atspeed_ctx* c, float lambda, int32_t B, int
   c->dft_prefilled = false;   // the draft's root row now holds the mixture
   c->drafted = false;
   return write_lists(c, B, items, scores, n_items);
+}
+
+atspeed_status atspeed_capture_hidden(atspeed_ctx* c, float* x, void* act, int32_t* plan, int32_t max_rows) {
+  if (!c) return fail(ATSPEED_E_INVALID, "null context");
+  if (x == nullptr && act == nullptr && plan == nullptr) {
+    c->cap_x = nullptr; c->cap_act = nullptr; c->cap_plan = nullptr; c->cap_rows = 0;
+    return ATSPEED_OK;
+  }
+  if (!x || !plan || max_rows <= 0)
+    return fail(ATSPEED_E_INVALID, "capture_hidden: x and plan buffers and max_rows > 0 needed");
+  if (act && !c->bf16) return fail(ATSPEED_E_INVALID, "capture_hidden: activations are captured for bf16 models only");
+  c->cap_x = x; c->cap_act = (bf16_t*)act; c->cap_plan = plan; c->cap_rows = max_rows;
+  return ATSPEED_OK;
 }
 
 atspeed_status atspeed_set_timing(atspeed_ctx* c, int32_t enable) {

@@ -1,0 +1,254 @@
+"""Kernel-by-kernel parity at the full 7B shape (32 layers, d 4096, 32 heads,
+FFN 11008, 32 users, 144-token prefixes with the shared 64-token prompt, the
+t = 0 draft tree of 1,920 rows): every step of every decoder block of the
+GPU's prefill and tree forward (the LLaMA block of the implementation details,
+Sec. 4.1, with tree-based attention, Sec. 3.3), recomputed by the oracle's step
+function from the GPU's own inputs to that step, for users 0 and 31 (user 31's
+prefill forwards only its own positions and takes the prompt's K/V from user 0).
+
+End to end, two correct bf16 computations of a 32-layer model at d 4096 drift
+apart by more than the 2e-2 logit bar: each bf16 rounding point turns a small
+difference into whole-ulp flips, and every layer adds more.  Fed its own
+inputs, each step leaves only its own arithmetic to compare:
+  * steps with bf16 results (the two RMSNorms, q/k/v with RoPE, attention,
+    SiLU(gate) * up, the final norm): bit-exact, except elements whose GPU value
+    is the rounding of a value within the GPU's own arithmetic error of the
+    exact one (near-ties, and values near zero, where cancellation makes that
+    error span several ulps);
+  * steps with fp32 results (the o and down projections with their residual
+    adds, the item head): within the GPU's own arithmetic error, and within the
+    1e-4 fp32 bar.
+The error bound of an element is derived from fp32 arithmetic (unit roundoff
+u = 2^-24): a dot product of length K accumulated in fp32 is within
+8 sqrt(K) u sum_k |x_k w_k| (a random walk of roundings, each at most u times
+the partial sum, which sum_k |x_k w_k| bounds, with a wide margin), RMSNorm
+within 64 u |y| (its fp32 sum of 4,096 squares), attention within 2^-14
+sum_j p_j |v_j| (probabilities carried as two bf16 halves, about 16 bits, and
+fp32 online softmax), SiLU(g) * u by propagating the bounds of g and u; a
+residual add adds 8 u |y|.  A wrong weight, index or formula moves values by
+far more.  At most 1% of a step's elements may be off the exact rounding.
+Measured: 0.001-0.11% of a step's elements off the exact rounding, each within
+0.07 of its bound; fp32 results within 1.4e-5 (0.007 of their bounds); the item
+logits from the GPU's last residual within 6e-6.
+"""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+from synth import get_workload, make_catalog, make_prefixes, make_weights  # noqa: E402
+from oracle.model import Decoder, attend  # noqa: E402
+from oracle.numerics import round_bf16  # noqa: E402
+
+USERS = (0, 31)
+U = 2.0 ** -24
+FLIP_FRACTION = 0.01  # at most this share of a step's elements off the exact rounding
+FP32_BAR = 1e-4       # the fp32 logit bar, also held by every fp32 result here
+
+
+def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
+    return (np.ascontiguousarray(bits).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def dot_bound(xa: np.ndarray, W: np.ndarray) -> np.ndarray:
+    """fp32 accumulation error bound of xa @ W.T (xa, W as fp64)."""
+    return 8.0 * np.sqrt(W.shape[1]) * U * (np.abs(xa) @ np.abs(W).T)
+
+
+def check_bf16(name, got_bits, exact, bound, stats):
+    """got_bits: the GPU's bf16 results; exact: the oracle's unrounded values
+    from the same inputs; bound: the GPU's arithmetic error bound per element.
+    Equal after rounding, or the GPU's value is the rounding of some value
+    within the bound of the exact one (a near-tie, or a value near zero whose
+    bound spans several ulps)."""
+    want = round_bf16(exact)
+    got = bf16_to_f64(got_bits)
+    diff = got != want
+    n = int(diff.sum())
+    worst = 0.0
+    if n:
+        g, y, b = got[diff], exact[diff], np.broadcast_to(bound, exact.shape)[diff]
+        with np.errstate(divide="ignore"):
+            ulp = np.where(g != 0, 2.0 ** (np.floor(np.log2(np.abs(np.where(g != 0, g, 1.0)))) - 7), 0.0)
+        # the rounding interval of g reaches the bound around the exact value
+        excess = np.maximum(np.abs(g - y) - 0.5 * ulp, 0.0)
+        worst = float((excess / b).max())
+        assert worst <= 1.0, (name, worst)
+        assert n <= FLIP_FRACTION * got.size, (name, n, got.size)
+    old = stats.get(name, (0, 0, 0.0))
+    stats[name] = (old[0] + n, old[1] + got.size, max(old[2], worst))
+
+
+def check_f32(name, got, exact, bound, stats):
+    r = float((np.abs(got - exact) / bound).max())
+    assert r <= 1.0, (name, r, float(np.abs(got - exact).max()))
+    assert np.abs(got - exact).max() <= FP32_BAR, (name, float(np.abs(got - exact).max()))
+    old = stats.get(name, (0.0, 0.0))
+    stats[name] = (max(old[0], float(np.abs(got - exact).max())), max(old[1], r))
+
+
+class Capture:
+    """The residual and activation capture of one target forward, on the device."""
+
+    def __init__(self, eng, w, rows, fn):
+        m = w.target
+        self.nl, self.d, self.f, self.R = m.n_layers, m.d_model, m.d_ffn, rows
+        self.x = torch.zeros((2 * self.nl + 1, rows, self.d), dtype=torch.float32, device="cuda")
+        self.layer = rows * (6 * self.d + self.f)
+        self.act = torch.zeros((self.nl * self.layer + rows * self.d,), dtype=torch.int16, device="cuda")
+        plan = torch.full((3 * rows + 1,), -2, dtype=torch.int32, device="cuda")
+        eng.atspeed_capture_hidden(self.x, plan, rows, act=self.act)
+        fn()
+        torch.cuda.synchronize()
+        p = plan.cpu().numpy()
+        self.M = int(p[3 * rows])
+        assert 0 < self.M <= rows, self.M
+        self.user, self.pos, self.slot = p[:3 * rows].reshape(3, rows)[:, :self.M]
+
+    def take(self, idx):
+        """Host copies of the captured values of rows ``idx``: x [2 nl + 1, n, d]
+        (fp64) and per layer the seven bf16 arrays (uint16)."""
+        ix = torch.from_numpy(np.asarray(idx)).cuda()
+        x = self.x[:, ix].cpu().numpy().astype(np.float64)
+        acts = []
+        for l in range(self.nl + 1):
+            base = l * self.layer
+            parts = []
+            for k in range(6 if l < self.nl else 1):
+                a = self.act[base + k * self.R * self.d: base + (k + 1) * self.R * self.d].view(self.R, self.d)
+                parts.append(a[ix].cpu().numpy().view(np.uint16))
+            if l < self.nl:
+                a = self.act[base + 6 * self.R * self.d: base + self.layer].view(self.R, self.f)
+                parts.append(a[ix].cpu().numpy().view(np.uint16))
+            acts.append(parts)
+        return x, acts
+
+
+def test_b7_every_kernel_against_the_oracle_step():
+    from paper_2410_05165_amd.binding import Engine
+    w = get_workload("b7")
+    m = w.target
+    nl, d, P, L, H, dh = m.n_layers, m.d_model, w.prefix_len, w.L, m.n_heads, m.d_head
+    cat = make_catalog(w)
+    pre = make_prefixes(w, cat)
+    print("[b7 kernels] generating weights", flush=True)
+    tw, dw = make_weights(w, "target"), make_weights(w, "draft")
+    eng = Engine(w, tw, dw, cat)
+    dev = torch.device("cuda:0")
+    B = w.batch
+
+    print("[b7 kernels] prefill with the capture armed", flush=True)
+    cp = Capture(eng, w, B * P, lambda: eng.atspeed_prefill(torch.from_numpy(pre).to(dev)))
+    rows0 = np.nonzero(cp.user == 0)[0]
+    assert (cp.pos[rows0] == np.arange(P)).all(), "user 0 forwards every prefix position"
+    pre_cap = {}
+    for u in USERS:
+        ru = np.nonzero(cp.user == u)[0]
+        S = int(cp.pos[ru][0])
+        assert (cp.pos[ru] == np.arange(S, P)).all()
+        # the user's prefix rows: the shared prompt positions are user 0's rows
+        # (same tokens; the prefill copies their K/V), the rest the user's own
+        pre_cap[u] = (S, cp.take(np.concatenate([rows0[:S], ru])))
+    del cp
+    torch.cuda.empty_cache()
+
+    print("[b7 kernels] draft, then the tree forward with the capture armed", flush=True)
+    eng.atspeed_draft()
+    T = eng.max_nodes
+    logits = torch.full((B, T, w.n_item_tokens), float("nan"), dtype=torch.float32, device=dev)
+    ct = Capture(eng, w, B * T, lambda: eng.atspeed_tree_logits(logits))
+    assert ct.M == 1920, ct.M
+    tn, tt, tp, td, _ = (a.cpu().numpy() for a in eng.tree_tensors(B))
+    lg = logits.cpu().numpy()
+    tree_cap = {}
+    for u in USERS:
+        r = np.nonzero(ct.user == u)[0]
+        nodes = ct.slot[r] - u * T
+        assert (nodes >= 0).all() and (td[u, nodes] < L).all()
+        assert (ct.pos[r] == P + td[u, nodes] - 1).all()
+        where = {int(n): i for i, n in enumerate(nodes)}
+        mask = np.zeros((len(r), len(r)), dtype=bool)   # ancestor-or-self among the user's rows
+        for i, n in enumerate(nodes):
+            a = int(n)
+            while a >= 0:
+                mask[i, where[a]] = True
+                a = int(tp[u, a])
+        tree_cap[u] = (nodes, mask, ct.take(r))
+    del ct
+    eng.close()
+
+    dec = Decoder(m, tw, w.dtype, cache_f64=True)
+    stats_b, stats_f = {}, {}
+
+    def heads(bits, n):   # [n, d] bf16 bits -> [1, H, n, dh] fp64
+        return bf16_to_f64(bits).reshape(1, n, H, dh).transpose(0, 2, 1, 3)
+
+    def rot_pairs(b):     # a rotated column's bound: its own and its rotate-half partner's
+        bb = b.reshape(b.shape[0], H, 2, dh // 2)
+        return (bb + bb[:, :, ::-1]).reshape(b.shape)
+
+    for l in range(nl):
+        dec._cache.clear()                       # one layer's fp64 weights at a time
+        p_ = f"l{l}."
+        Wq, Wk, Wv, Wo = (dec.W(p_ + n_) for n_ in ("wq", "wk", "wv", "wo"))
+        Wg, Wu, Wd = (dec.W(p_ + n_) for n_ in ("w_gate", "w_up", "w_down"))
+        for u in USERS:
+            S, (xp, ap) = pre_cap[u]
+            nodes, mask, (xt, at) = tree_cap[u]
+            pk_ = heads(ap[l][2], P)[0]          # the user's prefix K/V of this layer [H, P, dh]
+            pv_ = heads(ap[l][3], P)[0]
+            for kind, x, a, pos, n in (("prefix", xp, ap, np.arange(P), P),
+                                       ("tree", xt, at, P + td[u, nodes] - 1, len(nodes))):
+                sel = slice(S, P) if kind == "prefix" else slice(0, n)   # rows this forward computed
+                xn1, q, k, v, ao, xn2, act = a[l]
+                y = dec.norm(l, "attn_norm", x[2 * l][sel])
+                check_bf16("attn_norm", xn1[sel], y, 64 * U * np.abs(y), stats_b)
+                h1 = bf16_to_f64(xn1)
+                yq, yk, yv = (t[0].transpose(1, 0, 2).reshape(n, d) for t in dec.qkv(l, h1[None], pos))
+                check_bf16("q", q[sel], yq[sel], rot_pairs(dot_bound(h1[sel], Wq)), stats_b)
+                check_bf16("k", k[sel], yk[sel], rot_pairs(dot_bound(h1[sel], Wk)), stats_b)
+                check_bf16("v", v[sel], yv[sel], dot_bound(h1[sel], Wv), stats_b)
+                msk = np.tril(np.ones((n, n), dtype=bool)) if kind == "prefix" else mask
+                kw = {} if kind == "prefix" else dict(pk=pk_, pv=pv_)
+                qh, kh, vh = heads(q, n), heads(k, n), heads(v, n)
+                yo = dec.merge_heads(attend(qh, kh, vh, msk, **kw))[0]
+                # sum_j p_j |v_j|: the same attention over |v|
+                yav = dec.merge_heads(attend(qh, kh, np.abs(vh), msk,
+                                             **({} if kind == "prefix" else dict(pk=pk_, pv=np.abs(pv_)))))[0]
+                check_bf16("attention", ao[sel], yo[sel], 2.0 ** -14 * yav[sel], stats_b)
+                a1 = bf16_to_f64(ao[sel])
+                y = x[2 * l][sel] + a1 @ Wo.T
+                check_f32("o + residual", x[2 * l + 1][sel], y, dot_bound(a1, Wo) + 8 * U * np.abs(y), stats_f)
+                y = dec.norm(l, "ffn_norm", x[2 * l + 1][sel])
+                check_bf16("ffn_norm", xn2[sel], y, 64 * U * np.abs(y), stats_b)
+                h2 = bf16_to_f64(xn2[sel])
+                g_, u_ = h2 @ Wg.T, h2 @ Wu.T            # for the bound only
+                bg, bu = dot_bound(h2, Wg), dot_bound(h2, Wu)
+                sg = 1.0 / (1.0 + np.exp(-g_))
+                sil = g_ * sg
+                dsil = np.abs(sg * (1.0 + g_ * (1.0 - sg)))
+                ya = dec.swiglu(l, h2)
+                ba = np.abs(u_) * (dsil * bg + 4 * U * np.abs(sil)) + np.abs(sil) * bu + 4 * U * np.abs(ya)
+                check_bf16("silu(gate)*up", act[sel], ya, ba, stats_b)
+                if kind == "tree" or l + 1 < nl:   # a prefill captures no residual after the last layer
+                    a2 = bf16_to_f64(act[sel])
+                    y = x[2 * l + 1][sel] + a2 @ Wd.T
+                    check_f32("down + residual", x[2 * l + 2][sel], y, dot_bound(a2, Wd) + 8 * U * np.abs(y),
+                              stats_f)
+        print(f"[b7 kernels] layer {l:2d} checked; near-tie flips so far: "
+              + ", ".join(f"{k_} {v_[0]}" for k_, v_ in stats_b.items()), flush=True)
+    dec._cache.clear()
+    Wh = dec.W("lm_head_item")
+    for u in USERS:
+        nodes, mask, (xt, at) = tree_cap[u]
+        y = dec.norm(-1, "", xt[2 * nl])
+        check_bf16("final_norm", at[nl][0], y, 64 * U * np.abs(y), stats_b)
+        hf = bf16_to_f64(at[nl][0])
+        y = hf @ Wh.T
+        check_f32("item head", lg[u, nodes], y, dot_bound(hf, Wh) + 8 * U * np.abs(y), stats_f)
+    print("[b7 kernels] bf16 steps (elements off the exact rounding / elements, largest distance over its bound): "
+          + ", ".join(f"{k_} {v_[0]}/{v_[1]} ({v_[2]:.3f})" for k_, v_ in stats_b.items()), flush=True)
+    print("[b7 kernels] fp32 steps (max |err|, largest error over its bound): "
+          + ", ".join(f"{k_} {v_[0]:.2e} ({v_[1]:.3f})" for k_, v_ in stats_f.items()), flush=True)
