@@ -1,10 +1,11 @@
 """Kernel-by-kernel parity at the full 7B shape (32 layers, d 4096, 32 heads,
 FFN 11008, 32 users, 144-token prefixes with the shared 64-token prompt, the
-t = 0 draft tree of 1,920 rows): every step of every decoder block of the
-GPU's prefill and tree forward (the LLaMA block of the implementation details,
-Sec. 4.1, with tree-based attention, Sec. 3.3), recomputed by the oracle's step
-function from the GPU's own inputs to that step, for users 0 and 31 (user 31's
-prefill forwards only its own positions and takes the prompt's K/V from user 0).
+t = 0 draft tree of 1,920 rows) and at the stress shape (128 users with
+1,024-token prefixes, 38,400 tree rows): every step of the decoder blocks of
+the GPU's prefill and tree forward (the LLaMA block of the implementation
+details, Sec. 4.1, with tree-based attention, Sec. 3.3), recomputed by the
+oracle's step function from the GPU's own inputs to that step, for a user who
+forwards its whole prefix and one who takes the shared prompt's K/V from it.
 
 End to end, two correct bf16 computations of a 32-layer model at d 4096 drift
 apart by more than the 2e-2 logit bar: each bf16 rounding point turns a small
@@ -42,7 +43,6 @@ from synth import get_workload, make_catalog, make_prefixes, make_weights  # noq
 from oracle.model import Decoder, attend  # noqa: E402
 from oracle.numerics import round_bf16  # noqa: E402
 
-USERS = (0, 31)
 U = 2.0 ** -24
 FLIP_FRACTION = 0.01  # at most this share of a step's elements off the exact rounding
 FP32_BAR = 1e-4       # the fp32 logit bar, also held by every fp32 result here
@@ -103,9 +103,9 @@ class Capture:
         fn()
         torch.cuda.synchronize()
         p = plan.cpu().numpy()
-        self.M = int(p[3 * rows])
-        assert 0 < self.M <= rows, self.M
-        self.user, self.pos, self.slot = p[:3 * rows].reshape(3, rows)[:, :self.M]
+        self.M = int(p[3 * rows])                 # rows of the forward; the first min(M, R) are captured
+        assert self.M > 0, self.M
+        self.user, self.pos, self.slot = p[:3 * rows].reshape(3, rows)[:, :min(self.M, rows)]
 
     def take(self, idx):
         """Host copies of the captured values of rows ``idx``: x [2 nl + 1, n, d]
@@ -126,21 +126,34 @@ class Capture:
         return x, acts
 
 
-def test_b7_every_kernel_against_the_oracle_step():
+# b7: every layer, every prefix row the two users forward; stress (1,024-token
+# prefixes, 38,400 tree rows: the long-context attention and the large-batch
+# tile shapes): three layers and every 8th prefix row (the last included) of
+# the first two users, whose rows lead the forward
+CASES = {
+    "b7": dict(users=(0, 31), layers=None, stride=1, rows=None),
+    "stress": dict(users=(0, 1), layers=(0, 15, 31), stride=8, rows=2048),
+}
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_every_kernel_against_the_oracle_step(case):
     from paper_2410_05165_amd.binding import Engine
-    w = get_workload("b7")
+    cfg = CASES[case]
+    USERS = cfg["users"]
+    w = get_workload(case)
     m = w.target
     nl, d, P, L, H, dh = m.n_layers, m.d_model, w.prefix_len, w.L, m.n_heads, m.d_head
     cat = make_catalog(w)
     pre = make_prefixes(w, cat)
-    print("[b7 kernels] generating weights", flush=True)
+    print(f"[{case} kernels] generating weights", flush=True)
     tw, dw = make_weights(w, "target"), make_weights(w, "draft")
     eng = Engine(w, tw, dw, cat)
     dev = torch.device("cuda:0")
     B = w.batch
 
-    print("[b7 kernels] prefill with the capture armed", flush=True)
-    cp = Capture(eng, w, B * P, lambda: eng.atspeed_prefill(torch.from_numpy(pre).to(dev)))
+    print(f"[{case} kernels] prefill with the capture armed", flush=True)
+    cp = Capture(eng, w, cfg["rows"] or B * P, lambda: eng.atspeed_prefill(torch.from_numpy(pre).to(dev)))
     rows0 = np.nonzero(cp.user == 0)[0]
     assert (cp.pos[rows0] == np.arange(P)).all(), "user 0 forwards every prefix position"
     pre_cap = {}
@@ -154,17 +167,18 @@ def test_b7_every_kernel_against_the_oracle_step():
     del cp
     torch.cuda.empty_cache()
 
-    print("[b7 kernels] draft, then the tree forward with the capture armed", flush=True)
+    print(f"[{case} kernels] draft, then the tree forward with the capture armed", flush=True)
     eng.atspeed_draft()
     T = eng.max_nodes
     logits = torch.full((B, T, w.n_item_tokens), float("nan"), dtype=torch.float32, device=dev)
-    ct = Capture(eng, w, B * T, lambda: eng.atspeed_tree_logits(logits))
-    assert ct.M == 1920, ct.M
+    ct = Capture(eng, w, cfg["rows"] or B * T, lambda: eng.atspeed_tree_logits(logits))
+    assert ct.M == B * 3 * w.N, ct.M         # the t = 0 tree: drafted depths 1..3
     tn, tt, tp, td, _ = (a.cpu().numpy() for a in eng.tree_tensors(B))
     lg = logits.cpu().numpy()
     tree_cap = {}
     for u in USERS:
         r = np.nonzero(ct.user == u)[0]
+        assert len(r) == 3 * w.N, (u, len(r))
         nodes = ct.slot[r] - u * T
         assert (nodes >= 0).all() and (td[u, nodes] < L).all()
         assert (ct.pos[r] == P + td[u, nodes] - 1).all()
@@ -189,7 +203,7 @@ def test_b7_every_kernel_against_the_oracle_step():
         bb = b.reshape(b.shape[0], H, 2, dh // 2)
         return (bb + bb[:, :, ::-1]).reshape(b.shape)
 
-    for l in range(nl):
+    for l in (cfg["layers"] or range(nl)):
         dec._cache.clear()                       # one layer's fp64 weights at a time
         p_ = f"l{l}."
         Wq, Wk, Wv, Wo = (dec.W(p_ + n_) for n_ in ("wq", "wk", "wv", "wo"))
@@ -199,25 +213,29 @@ def test_b7_every_kernel_against_the_oracle_step():
             nodes, mask, (xt, at) = tree_cap[u]
             pk_ = heads(ap[l][2], P)[0]          # the user's prefix K/V of this layer [H, P, dh]
             pv_ = heads(ap[l][3], P)[0]
-            for kind, x, a, pos, n in (("prefix", xp, ap, np.arange(P), P),
-                                       ("tree", xt, at, P + td[u, nodes] - 1, len(nodes))):
-                sel = slice(S, P) if kind == "prefix" else slice(0, n)   # rows this forward computed
+            own = np.arange(S, P)[::-1][::cfg["stride"]][::-1]       # checked prefix rows (the last included)
+            for kind, x, a, pos, n, sel in (("prefix", xp, ap, np.arange(P), P, own),
+                                            ("tree", xt, at, P + td[u, nodes] - 1, len(nodes),
+                                             np.arange(len(nodes)))):
                 xn1, q, k, v, ao, xn2, act = a[l]
                 y = dec.norm(l, "attn_norm", x[2 * l][sel])
                 check_bf16("attn_norm", xn1[sel], y, 64 * U * np.abs(y), stats_b)
-                h1 = bf16_to_f64(xn1)
-                yq, yk, yv = (t[0].transpose(1, 0, 2).reshape(n, d) for t in dec.qkv(l, h1[None], pos))
-                check_bf16("q", q[sel], yq[sel], rot_pairs(dot_bound(h1[sel], Wq)), stats_b)
-                check_bf16("k", k[sel], yk[sel], rot_pairs(dot_bound(h1[sel], Wk)), stats_b)
-                check_bf16("v", v[sel], yv[sel], dot_bound(h1[sel], Wv), stats_b)
-                msk = np.tril(np.ones((n, n), dtype=bool)) if kind == "prefix" else mask
-                kw = {} if kind == "prefix" else dict(pk=pk_, pv=pv_)
-                qh, kh, vh = heads(q, n), heads(k, n), heads(v, n)
+                h1 = bf16_to_f64(xn1[sel])
+                yq, yk, yv = (t[0].transpose(1, 0, 2).reshape(len(sel), d) for t in dec.qkv(l, h1[None], pos[sel]))
+                check_bf16("q", q[sel], yq, rot_pairs(dot_bound(h1, Wq)), stats_b)
+                check_bf16("k", k[sel], yk, rot_pairs(dot_bound(h1, Wk)), stats_b)
+                check_bf16("v", v[sel], yv, dot_bound(h1, Wv), stats_b)
+                # the checked queries against every key of the forward (the GPU's k/v)
+                if kind == "prefix":
+                    msk = np.arange(n)[None, :] <= pos[sel][:, None]
+                    kw, kwa = {}, {}
+                else:
+                    msk = mask
+                    kw, kwa = dict(pk=pk_, pv=pv_), dict(pk=pk_, pv=np.abs(pv_))
+                qh, kh, vh = heads(q[sel], len(sel)), heads(k, n), heads(v, n)
                 yo = dec.merge_heads(attend(qh, kh, vh, msk, **kw))[0]
-                # sum_j p_j |v_j|: the same attention over |v|
-                yav = dec.merge_heads(attend(qh, kh, np.abs(vh), msk,
-                                             **({} if kind == "prefix" else dict(pk=pk_, pv=np.abs(pv_)))))[0]
-                check_bf16("attention", ao[sel], yo[sel], 2.0 ** -14 * yav[sel], stats_b)
+                yav = dec.merge_heads(attend(qh, kh, np.abs(vh), msk, **kwa))[0]   # sum_j p_j |v_j|
+                check_bf16("attention", ao[sel], yo, 2.0 ** -14 * yav, stats_b)
                 a1 = bf16_to_f64(ao[sel])
                 y = x[2 * l][sel] + a1 @ Wo.T
                 check_f32("o + residual", x[2 * l + 1][sel], y, dot_bound(a1, Wo) + 8 * U * np.abs(y), stats_f)
@@ -237,7 +255,7 @@ def test_b7_every_kernel_against_the_oracle_step():
                     y = x[2 * l + 1][sel] + a2 @ Wd.T
                     check_f32("down + residual", x[2 * l + 2][sel], y, dot_bound(a2, Wd) + 8 * U * np.abs(y),
                               stats_f)
-        print(f"[b7 kernels] layer {l:2d} checked; near-tie flips so far: "
+        print(f"[{case} kernels] layer {l:2d} checked; near-tie flips so far: "
               + ", ".join(f"{k_} {v_[0]}" for k_, v_ in stats_b.items()), flush=True)
     dec._cache.clear()
     Wh = dec.W("lm_head_item")
@@ -248,7 +266,7 @@ def test_b7_every_kernel_against_the_oracle_step():
         hf = bf16_to_f64(at[nl][0])
         y = hf @ Wh.T
         check_f32("item head", lg[u, nodes], y, dot_bound(hf, Wh) + 8 * U * np.abs(y), stats_f)
-    print("[b7 kernels] bf16 steps (elements off the exact rounding / elements, largest distance over its bound): "
+    print(f"[{case} kernels] bf16 steps (elements off the exact rounding / elements, largest distance over its bound): "
           + ", ".join(f"{k_} {v_[0]}/{v_[1]} ({v_[2]:.3f})" for k_, v_ in stats_b.items()), flush=True)
-    print("[b7 kernels] fp32 steps (max |err|, largest error over its bound): "
+    print(f"[{case} kernels] fp32 steps (max |err|, largest error over its bound): "
           + ", ".join(f"{k_} {v_[0]:.2e} ({v_[1]:.3f})" for k_, v_ in stats_f.items()), flush=True)
