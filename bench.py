@@ -348,9 +348,6 @@ def timed_decodes(eng, w, prefix, steps, warmup, roofline=True):
     for _ in range(warmup):
         eng.atspeed_decode_topk(prefix, items, scores, n, None)
     torch.cuda.synchronize()
-    acc = np.zeros((L, eng.cfg.max_batch), np.int32)
-    st = Stats()
-    st.accepted = acc.ctypes.data_as(C.POINTER(C.c_int32))
     if roofline:
         eng.atspeed_set_timing(["gu"], target_only=True)
     per = []
@@ -358,7 +355,7 @@ def timed_decodes(eng, w, prefix, steps, warmup, roofline=True):
     t0 = time.perf_counter()
     for _ in range(steps):
         a = time.perf_counter()
-        eng.atspeed_decode_topk(prefix, items, scores, n, st)    # returns after its final synchronisation
+        eng.atspeed_decode_topk(prefix, items, scores, n, None)  # returns after its last step's synchronisation
         per.append(time.perf_counter() - a)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
@@ -368,6 +365,13 @@ def timed_decodes(eng, w, prefix, steps, warmup, roofline=True):
         eng.atspeed_set_timing(False)
         gu = dict(ms=ms, launches=int(nl), gflop=gf)
     out = (items.cpu().numpy(), scores.cpu().numpy(), n.cpu().numpy())
+    # stage times, steps and accepted levels from one more decode outside the
+    # timed region (the per-stage timing synchronises between the stages)
+    acc = np.zeros((L, eng.cfg.max_batch), np.int32)
+    st = Stats()
+    st.accepted = acc.ctypes.data_as(C.POINTER(C.c_int32))
+    eng.atspeed_decode_topk(prefix, items, scores, n, st)
+    torch.cuda.synchronize()
     r = dict(lists_per_s=B * steps / elapsed, ms_per_decode=1e3 * elapsed / steps,
              ms_per_decode_median=1e3 * float(np.median(per)), steps=int(st.n_steps),
              ms_prefill=round(st.ms_prefill, 3), ms_draft=round(st.ms_draft, 3), ms_verify=round(st.ms_verify, 3),
