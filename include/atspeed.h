@@ -407,10 +407,14 @@ ATSPEED_API atspeed_status atspeed_set_state(atspeed_ctx* ctx, int32_t B, const 
 
 /* Residual-stream and activation capture (instrumentation for kernel-by-kernel
  * parity tests; the decoder block is the LLaMA block of the implementation
- * details, Sec. 4.1, with tree-based attention, Sec. 3.3).  Arms the NEXT
- * forward of the target model (in atspeed_prefill, atspeed_tree_logits,
- * atspeed_verify or a decode) to copy, on the context's stream, the values of
- * its forwarded rows at every rounding point of the block (R = max_rows):
+ * details, Sec. 4.1, with tree-based attention, Sec. 3.3).  Arms a coming
+ * forward of the target (model 0: in atspeed_prefill, atspeed_tree_logits,
+ * atspeed_verify or a decode) or of the draft (model 1: in atspeed_prefill or
+ * atspeed_draft, which forwards the paths of the current beams, then each
+ * drafted level's nodes but the last) -- the one after the next `skip`
+ * forwards of that model -- to copy, on the context's stream, the values of its
+ * forwarded rows at every rounding point of the block (R = max_rows; widths are
+ * that model's):
  *   x_dev   (device, fp32, [2 n_layers + 1][R][d_model]): index 2l is layer l's
  *           input residual, 2l + 1 the residual after its attention sublayer,
  *           2 n_layers the residual after the last layer (not written by a
@@ -427,11 +431,12 @@ ATSPEED_API atspeed_status atspeed_set_state(atspeed_ctx* ctx, int32_t B, const 
  *           R, then the forward's row count.
  * Rows past R are not copied (check the row count).  The capture disarms itself
  * after that forward; all three pointers null disarms it at once.
- * ATSPEED_E_INVALID for a null x_dev or plan_dev with the others set,
- * max_rows <= 0, or act_dev with an fp32 model.  Adds device copies to the
+ * ATSPEED_E_INVALID for a model other than 0 or 1, skip < 0, a null x_dev or
+ * plan_dev with the others set, max_rows <= 0, or act_dev with an fp32 model;
+ * ATSPEED_E_STATE for model 1 without a draft.  Adds device copies to the
  * forward; buffers are caller-owned. */
-ATSPEED_API atspeed_status atspeed_capture_hidden(atspeed_ctx* ctx, float* x_dev, void* act_dev, int32_t* plan_dev,
-                                                  int32_t max_rows);
+ATSPEED_API atspeed_status atspeed_capture_hidden(atspeed_ctx* ctx, int32_t model, int32_t skip, float* x_dev,
+                                                  void* act_dev, int32_t* plan_dev, int32_t max_rows);
 
 /* Kernel timing (instrumentation for measurement).  enable is a bit mask of the
  * kernel classes to time (bit ATSPEED_K_x; ATSPEED_TIME_ALL for every class),

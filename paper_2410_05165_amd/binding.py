@@ -98,7 +98,7 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
     lib.atspeed_get_tree.argtypes = [vp, C.POINTER(Tree)]
     lib.atspeed_verify.argtypes = [vp, pi32, pi32, pf]
     lib.atspeed_tree_logits.argtypes = [vp, pf]
-    lib.atspeed_capture_hidden.argtypes = [vp, pf, vp, pi32, i32]
+    lib.atspeed_capture_hidden.argtypes = [vp, i32, i32, pf, vp, pi32, i32]
     lib.atspeed_accept.argtypes = [vp, pf, pf, pi32, pi32]
     lib.atspeed_accept_noalloc.argtypes = [vp, pf, pf, pi32, pi32]
     lib.atspeed_decode_topk.argtypes = [vp, i32, i32, pi32, pi32, pf, pi32, C.POINTER(Stats)]
@@ -235,8 +235,9 @@ class Engine:
     def atspeed_verify(self, accepted=None, t_after=None, logits=None):
         self._check(self.lib.atspeed_verify(self.ctx, _ptr(accepted), _ptr(t_after), _ptr(logits)))
 
-    def atspeed_capture_hidden(self, x=None, plan=None, max_rows=0, act=None):
-        self._check(self.lib.atspeed_capture_hidden(self.ctx, _ptr(x), _ptr(act), _ptr(plan), int(max_rows)))
+    def atspeed_capture_hidden(self, x=None, plan=None, max_rows=0, act=None, model=0, skip=0):
+        self._check(self.lib.atspeed_capture_hidden(self.ctx, int(model), int(skip), _ptr(x), _ptr(act), _ptr(plan),
+                                                    int(max_rows)))
 
     def atspeed_tree_logits(self, logits):
         self._check(self.lib.atspeed_tree_logits(self.ctx, _ptr(logits)))

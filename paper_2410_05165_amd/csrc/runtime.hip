@@ -151,6 +151,8 @@ struct atspeed_ctx {
   bf16_t* cap_act = nullptr;     // bf16 inputs of every GEMM and attention (layout at atspeed_capture_hidden)
   int32_t* cap_plan = nullptr;   // [3][cap_rows] user, position, slot of each row; then the row count
   int cap_rows = 0;
+  int cap_model = 0;             // 0 target, 1 draft
+  int cap_skip = 0;              // forwards of that model to let pass before the captured one
   // timing instrumentation
   uint32_t timing_mask = 0;   // kernel classes whose launches are bracketed by events
   bool timing_target_only = false;  // skip the draft model's launches
@@ -496,7 +498,11 @@ atspeed_status forward(atspeed_ctx& c, ModelRt& r, bool prefill, int Mmax, int T
   const double M = Mmax;
   // residual-stream capture (armed by atspeed_capture_hidden for one target
   // forward): the row plan now, x at every sublayer boundary below
-  const bool cap = c.cap_x != nullptr && &r == &c.tgt;
+  bool cap = c.cap_x != nullptr && &r == (c.cap_model == 1 ? &c.dft : &c.tgt);
+  if (cap && c.cap_skip > 0) {
+    --c.cap_skip;
+    cap = false;
+  }
   const int crow = cap ? std::min(Mmax, c.cap_rows) : 0;
   auto capture = [&](int idx) -> hipError_t {
     return hipMemcpyAsync(c.cap_x + (size_t)idx * c.cap_rows * d, c.x, (size_t)crow * d * sizeof(float),
@@ -1291,8 +1297,12 @@ atspeed_status atspeed_mixed_search(atspeed_ctx* c, float lambda, int32_t B, int
   return write_lists(c, B, items, scores, n_items);
 }
 
-atspeed_status atspeed_capture_hidden(atspeed_ctx* c, float* x, void* act, int32_t* plan, int32_t max_rows) {
+atspeed_status atspeed_capture_hidden(atspeed_ctx* c, int32_t model, int32_t skip, float* x, void* act,
+                                      int32_t* plan, int32_t max_rows) {
   if (!c) return fail(ATSPEED_E_INVALID, "null context");
+  if (model != 0 && model != 1) return fail(ATSPEED_E_INVALID, "capture_hidden: model is 0 (target) or 1 (draft)");
+  if (skip < 0) return fail(ATSPEED_E_INVALID, "capture_hidden: skip < 0");
+  if (model == 1 && !c->dft.present) return fail(ATSPEED_E_STATE, "capture_hidden: context has no draft model");
   if (x == nullptr && act == nullptr && plan == nullptr) {
     c->cap_x = nullptr; c->cap_act = nullptr; c->cap_plan = nullptr; c->cap_rows = 0;
     return ATSPEED_OK;
@@ -1300,7 +1310,8 @@ atspeed_status atspeed_capture_hidden(atspeed_ctx* c, float* x, void* act, int32
   if (!x || !plan || max_rows <= 0)
     return fail(ATSPEED_E_INVALID, "capture_hidden: x and plan buffers and max_rows > 0 needed");
   if (act && !c->bf16) return fail(ATSPEED_E_INVALID, "capture_hidden: activations are captured for bf16 models only");
-  c->cap_x = x; c->cap_act = (bf16_t*)act; c->cap_plan = plan; c->cap_rows = max_rows;
+  c->cap_x = x; c->cap_act = (bf16_t*)act; c->cap_plan = plan; c->cap_rows = max_rows; c->cap_model = model;
+  c->cap_skip = skip;
   return ATSPEED_OK;
 }
 

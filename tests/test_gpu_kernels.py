@@ -5,7 +5,9 @@ t = 0 draft tree of 1,920 rows) and at the stress shape (128 users with
 the GPU's prefill and tree forward (the LLaMA block of the implementation
 details, Sec. 4.1, with tree-based attention, Sec. 3.3), recomputed by the
 oracle's step function from the GPU's own inputs to that step, for a user who
-forwards its whole prefix and one who takes the shared prompt's K/V from it.
+forwards its whole prefix and one who takes the shared prompt's K/V from it;
+and the 7B shape's draft model (4 layers, d 768, 12 heads, FFN 3072) in its
+prefill and its forward of the first drafted level.
 
 End to end, two correct bf16 computations of a 32-layer model at d 4096 drift
 apart by more than the 2e-2 logit bar: each bf16 rounding point turns a small
@@ -90,16 +92,17 @@ def check_f32(name, got, exact, bound, stats):
 
 
 class Capture:
-    """The residual and activation capture of one target forward, on the device."""
+    """The residual and activation capture of one forward of ``model`` (0
+    target, 1 draft; the one after ``skip`` others of it), on the device; the
+    first ``rows`` rows of the forward are kept."""
 
-    def __init__(self, eng, w, rows, fn):
-        m = w.target
-        self.nl, self.d, self.f, self.R = m.n_layers, m.d_model, m.d_ffn, rows
+    def __init__(self, eng, dims, rows, fn, model=0, skip=0):
+        self.nl, self.d, self.f, self.R = dims.n_layers, dims.d_model, dims.d_ffn, rows
         self.x = torch.zeros((2 * self.nl + 1, rows, self.d), dtype=torch.float32, device="cuda")
         self.layer = rows * (6 * self.d + self.f)
         self.act = torch.zeros((self.nl * self.layer + rows * self.d,), dtype=torch.int16, device="cuda")
         plan = torch.full((3 * rows + 1,), -2, dtype=torch.int32, device="cuda")
-        eng.atspeed_capture_hidden(self.x, plan, rows, act=self.act)
+        eng.atspeed_capture_hidden(self.x, plan, rows, act=self.act, model=model, skip=skip)
         fn()
         torch.cuda.synchronize()
         p = plan.cpu().numpy()
@@ -126,75 +129,45 @@ class Capture:
         return x, acts
 
 
-# b7: every layer, every prefix row the two users forward; stress (1,024-token
-# prefixes, 38,400 tree rows: the long-context attention and the large-batch
-# tile shapes): three layers and every 8th prefix row (the last included) of
-# the first two users, whose rows lead the forward
-CASES = {
-    "b7": dict(users=(0, 31), layers=None, stride=1, rows=None),
-    "stress": dict(users=(0, 1), layers=(0, 15, 31), stride=8, rows=2048),
-}
-
-
-@pytest.mark.parametrize("case", list(CASES))
-def test_every_kernel_against_the_oracle_step(case):
-    from paper_2410_05165_amd.binding import Engine
-    cfg = CASES[case]
-    USERS = cfg["users"]
-    w = get_workload(case)
-    m = w.target
-    nl, d, P, L, H, dh = m.n_layers, m.d_model, w.prefix_len, w.L, m.n_heads, m.d_head
-    cat = make_catalog(w)
-    pre = make_prefixes(w, cat)
-    print(f"[{case} kernels] generating weights", flush=True)
-    tw, dw = make_weights(w, "target"), make_weights(w, "draft")
-    eng = Engine(w, tw, dw, cat)
-    dev = torch.device("cuda:0")
-    B = w.batch
-
-    print(f"[{case} kernels] prefill with the capture armed", flush=True)
-    cp = Capture(eng, w, cfg["rows"] or B * P, lambda: eng.atspeed_prefill(torch.from_numpy(pre).to(dev)))
+def prefix_rows(cp, users, P):
+    """Per user: (S, captured values of its P prefix rows), the shared prompt
+    positions [0, S) being user 0's rows (same tokens; the prefill copies their
+    K/V), the rest the user's own."""
     rows0 = np.nonzero(cp.user == 0)[0]
     assert (cp.pos[rows0] == np.arange(P)).all(), "user 0 forwards every prefix position"
-    pre_cap = {}
-    for u in USERS:
+    out = {}
+    for u in users:
         ru = np.nonzero(cp.user == u)[0]
         S = int(cp.pos[ru][0])
         assert (cp.pos[ru] == np.arange(S, P)).all()
-        # the user's prefix rows: the shared prompt positions are user 0's rows
-        # (same tokens; the prefill copies their K/V), the rest the user's own
-        pre_cap[u] = (S, cp.take(np.concatenate([rows0[:S], ru])))
-    del cp
-    torch.cuda.empty_cache()
+        out[u] = (S, cp.take(np.concatenate([rows0[:S], ru])))
+    return out
 
-    print(f"[{case} kernels] draft, then the tree forward with the capture armed", flush=True)
-    eng.atspeed_draft()
-    T = eng.max_nodes
-    logits = torch.full((B, T, w.n_item_tokens), float("nan"), dtype=torch.float32, device=dev)
-    ct = Capture(eng, w, cfg["rows"] or B * T, lambda: eng.atspeed_tree_logits(logits))
-    assert ct.M == B * 3 * w.N, ct.M         # the t = 0 tree: drafted depths 1..3
-    tn, tt, tp, td, _ = (a.cpu().numpy() for a in eng.tree_tensors(B))
-    lg = logits.cpu().numpy()
-    tree_cap = {}
-    for u in USERS:
-        r = np.nonzero(ct.user == u)[0]
-        assert len(r) == 3 * w.N, (u, len(r))
-        nodes = ct.slot[r] - u * T
-        assert (nodes >= 0).all() and (td[u, nodes] < L).all()
-        assert (ct.pos[r] == P + td[u, nodes] - 1).all()
+
+def tree_rows(cp, users, T, parent, depth, P, L):
+    """Per user: (nodes, ancestor-or-self mask among the user's forwarded
+    nodes, captured values of those rows)."""
+    out = {}
+    for u in users:
+        r = np.nonzero(cp.user == u)[0]
+        nodes = cp.slot[r] - u * T
+        assert len(r) > 0 and (nodes >= 0).all() and (depth[u, nodes] < L).all()
+        assert (cp.pos[r] == P + depth[u, nodes] - 1).all()
         where = {int(n): i for i, n in enumerate(nodes)}
-        mask = np.zeros((len(r), len(r)), dtype=bool)   # ancestor-or-self among the user's rows
+        mask = np.zeros((len(r), len(r)), dtype=bool)
         for i, n in enumerate(nodes):
             a = int(n)
             while a >= 0:
                 mask[i, where[a]] = True
-                a = int(tp[u, a])
-        tree_cap[u] = (nodes, mask, ct.take(r))
-    del ct
-    eng.close()
+                a = int(parent[u, a])
+        out[u] = (nodes, mask, cp.take(r))
+    return out
 
-    dec = Decoder(m, tw, w.dtype, cache_f64=True)
-    stats_b, stats_f = {}, {}
+
+def check_layers(dec, dims, layers, pre_cap, tree_cap, depth, P, stride, stats_b, stats_f, tag):
+    """Every step of blocks ``layers`` on the captured prefix rows (every
+    ``stride``-th a user computed itself, its last included) and tree rows."""
+    nl, d, H, dh = dims.n_layers, dims.d_model, dims.n_heads, dims.d_head
 
     def heads(bits, n):   # [n, d] bf16 bits -> [1, H, n, dh] fp64
         return bf16_to_f64(bits).reshape(1, n, H, dh).transpose(0, 2, 1, 3)
@@ -203,19 +176,19 @@ def test_every_kernel_against_the_oracle_step(case):
         bb = b.reshape(b.shape[0], H, 2, dh // 2)
         return (bb + bb[:, :, ::-1]).reshape(b.shape)
 
-    for l in (cfg["layers"] or range(nl)):
+    for l in layers:
         dec._cache.clear()                       # one layer's fp64 weights at a time
         p_ = f"l{l}."
         Wq, Wk, Wv, Wo = (dec.W(p_ + n_) for n_ in ("wq", "wk", "wv", "wo"))
         Wg, Wu, Wd = (dec.W(p_ + n_) for n_ in ("w_gate", "w_up", "w_down"))
-        for u in USERS:
+        for u in tree_cap:
             S, (xp, ap) = pre_cap[u]
             nodes, mask, (xt, at) = tree_cap[u]
             pk_ = heads(ap[l][2], P)[0]          # the user's prefix K/V of this layer [H, P, dh]
             pv_ = heads(ap[l][3], P)[0]
-            own = np.arange(S, P)[::-1][::cfg["stride"]][::-1]       # checked prefix rows (the last included)
+            own = np.arange(S, P)[::-1][::stride][::-1]
             for kind, x, a, pos, n, sel in (("prefix", xp, ap, np.arange(P), P, own),
-                                            ("tree", xt, at, P + td[u, nodes] - 1, len(nodes),
+                                            ("tree", xt, at, P + depth[u, nodes] - 1, len(nodes),
                                              np.arange(len(nodes)))):
                 xn1, q, k, v, ao, xn2, act = a[l]
                 y = dec.norm(l, "attn_norm", x[2 * l][sel])
@@ -255,18 +228,107 @@ def test_every_kernel_against_the_oracle_step(case):
                     y = x[2 * l + 1][sel] + a2 @ Wd.T
                     check_f32("down + residual", x[2 * l + 2][sel], y, dot_bound(a2, Wd) + 8 * U * np.abs(y),
                               stats_f)
-        print(f"[{case} kernels] layer {l:2d} checked; near-tie flips so far: "
+        print(f"[{tag}] layer {l:2d} checked; elements off the exact rounding so far: "
               + ", ".join(f"{k_} {v_[0]}" for k_, v_ in stats_b.items()), flush=True)
+
+
+def report(tag, stats_b, stats_f):
+    print(f"[{tag}] bf16 steps (elements off the exact rounding / elements, largest distance over its bound): "
+          + ", ".join(f"{k_} {v_[0]}/{v_[1]} ({v_[2]:.3f})" for k_, v_ in stats_b.items()), flush=True)
+    print(f"[{tag}] fp32 steps (max |err|, largest error over its bound): "
+          + ", ".join(f"{k_} {v_[0]:.2e} ({v_[1]:.3f})" for k_, v_ in stats_f.items()), flush=True)
+
+
+# b7: every layer, every prefix row the two users forward; stress (1,024-token
+# prefixes, 38,400 tree rows: the long-context attention and the large-batch
+# tile shapes): three layers and every 8th prefix row (the last included) of
+# the first two users, whose rows lead the forward
+CASES = {
+    "b7": dict(users=(0, 31), layers=None, stride=1, rows=None),
+    "stress": dict(users=(0, 1), layers=(0, 15, 31), stride=8, rows=2048),
+}
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_every_kernel_against_the_oracle_step(case):
+    from paper_2410_05165_amd.binding import Engine
+    cfg = CASES[case]
+    w = get_workload(case)
+    m = w.target
+    nl, P, L, B = m.n_layers, w.prefix_len, w.L, w.batch
+    cat = make_catalog(w)
+    pre = make_prefixes(w, cat)
+    print(f"[{case} kernels] generating weights", flush=True)
+    tw, dw = make_weights(w, "target"), make_weights(w, "draft")
+    eng = Engine(w, tw, dw, cat)
+    prefix = torch.from_numpy(pre).cuda()
+
+    print(f"[{case} kernels] prefill with the capture armed", flush=True)
+    cp = Capture(eng, m, cfg["rows"] or B * P, lambda: eng.atspeed_prefill(prefix))
+    pre_cap = prefix_rows(cp, cfg["users"], P)
+    del cp
+    torch.cuda.empty_cache()
+
+    print(f"[{case} kernels] draft, then the tree forward with the capture armed", flush=True)
+    eng.atspeed_draft()
+    T = eng.max_nodes
+    logits = torch.full((B, T, w.n_item_tokens), float("nan"), dtype=torch.float32, device="cuda")
+    ct = Capture(eng, m, cfg["rows"] or B * T, lambda: eng.atspeed_tree_logits(logits))
+    assert ct.M == B * 3 * w.N, ct.M         # the t = 0 tree: drafted depths 1..3
+    tn, tt, tp, td, _ = (a.cpu().numpy() for a in eng.tree_tensors(B))
+    tree_cap = tree_rows(ct, cfg["users"], T, tp, td, P, L)
+    assert all(len(v_[0]) == 3 * w.N for v_ in tree_cap.values())
+    lg = logits.cpu().numpy()
+    del ct
+    eng.close()
+
+    dec = Decoder(m, tw, w.dtype, cache_f64=True)
+    stats_b, stats_f = {}, {}
+    check_layers(dec, m, cfg["layers"] or range(nl), pre_cap, tree_cap, td, P, cfg["stride"], stats_b, stats_f,
+                 f"{case} kernels")
     dec._cache.clear()
     Wh = dec.W("lm_head_item")
-    for u in USERS:
-        nodes, mask, (xt, at) = tree_cap[u]
+    for u, (nodes, mask, (xt, at)) in tree_cap.items():
         y = dec.norm(-1, "", xt[2 * nl])
         check_bf16("final_norm", at[nl][0], y, 64 * U * np.abs(y), stats_b)
         hf = bf16_to_f64(at[nl][0])
         y = hf @ Wh.T
         check_f32("item head", lg[u, nodes], y, dot_bound(hf, Wh) + 8 * U * np.abs(y), stats_f)
-    print(f"[{case} kernels] bf16 steps (elements off the exact rounding / elements, largest distance over its bound): "
-          + ", ".join(f"{k_} {v_[0]}/{v_[1]} ({v_[2]:.3f})" for k_, v_ in stats_b.items()), flush=True)
-    print(f"[{case} kernels] fp32 steps (max |err|, largest error over its bound): "
-          + ", ".join(f"{k_} {v_[0]:.2e} ({v_[1]:.3f})" for k_, v_ in stats_f.items()), flush=True)
+    report(f"{case} kernels", stats_b, stats_f)
+
+
+def test_b7_draft_kernels_against_the_oracle_step():
+    """The 7B shape's draft (4 layers, d 768, 12 heads of 64, FFN 3072): its
+    prefill and its forward of the first drafted level (N = 20 nodes per user at
+    depth 1, attending to the draft's prefix cache and themselves; the draft's
+    first forward at t = 0, over the paths of the empty beams, has no rows)."""
+    from paper_2410_05165_amd.binding import Engine
+    w = get_workload("b7")
+    m = w.draft
+    P, L, B, users = w.prefix_len, w.L, w.batch, (0, 31)
+    cat = make_catalog(w)
+    pre = make_prefixes(w, cat)
+    tw, dw = make_weights(w, "target"), make_weights(w, "draft")
+    eng = Engine(w, tw, dw, cat)
+    prefix = torch.from_numpy(pre).cuda()
+    print("[b7 draft kernels] prefill with the draft's capture armed", flush=True)
+    cp = Capture(eng, m, B * P, lambda: eng.atspeed_prefill(prefix), model=1)
+    pre_cap = prefix_rows(cp, users, P)
+    del cp
+    print("[b7 draft kernels] draft with the capture of its second forward armed", flush=True)
+    T = eng.max_nodes
+    ct = Capture(eng, m, B * w.N, lambda: eng.atspeed_draft(), model=1, skip=1)
+    assert ct.M == B * w.N, ct.M
+    tn, tt, tp, td, _ = (a.cpu().numpy() for a in eng.tree_tensors(B))
+    tree_cap = tree_rows(ct, users, T, tp, td, P, L)
+    assert all(len(v_[0]) == w.N and (td[u, v_[0]] == 1).all() for u, v_ in tree_cap.items())
+    del ct
+    eng.close()
+    dec = Decoder(m, dw, w.dtype, cache_f64=True)
+    stats_b, stats_f = {}, {}
+    check_layers(dec, m, range(m.n_layers), pre_cap, tree_cap, td, P, 1, stats_b, stats_f, "b7 draft kernels")
+    dec._cache.clear()
+    for u, (nodes, mask, (xt, at)) in tree_cap.items():
+        y = dec.norm(-1, "", xt[2 * m.n_layers])
+        check_bf16("final_norm", at[m.n_layers][0], y, 64 * U * np.abs(y), stats_b)
+    report("b7 draft kernels", stats_b, stats_f)
