@@ -332,3 +332,44 @@ def test_b7_draft_kernels_against_the_oracle_step():
         y = dec.norm(-1, "", xt[2 * m.n_layers])
         check_bf16("final_norm", at[m.n_layers][0], y, 64 * U * np.abs(y), stats_b)
     report("b7 draft kernels", stats_b, stats_f)
+
+
+def test_capture_error_paths_and_a_small_capture():
+    """The capture call's argument checks, and a capture of the tiny fp32
+    workload's prefill (residual only: activations are captured for bf16 models)
+    against the oracle's blocks on the same inputs within the fp32 bar."""
+    from paper_2410_05165_amd.binding import AtspeedError, Engine
+    w = get_workload("tiny")
+    cat = make_catalog(w)
+    pre = make_prefixes(w, cat)
+    tw, dw = make_weights(w, "target"), make_weights(w, "draft")
+    eng = Engine(w, tw, dw, cat)
+    m = w.target
+    x = torch.zeros((2 * m.n_layers + 1, w.prefix_len, m.d_model), dtype=torch.float32, device="cuda")
+    plan = torch.zeros(3 * w.prefix_len + 1, dtype=torch.int32, device="cuda")
+    act = torch.zeros(16, dtype=torch.int16, device="cuda")
+    for what, kw in (("model 2", dict(model=2)), ("skip -1", dict(skip=-1)), ("max_rows 0", dict(max_rows=0)),
+                     ("no plan", dict(plan=None)), ("activations of an fp32 model", dict(act=act))):
+        args = dict(x=x, plan=plan, max_rows=w.prefix_len)
+        args.update(kw)
+        with pytest.raises(AtspeedError) as ex:
+            eng.atspeed_capture_hidden(**args)
+        assert ex.value.status == 1, what          # ATSPEED_E_INVALID
+    eng.atspeed_capture_hidden()                    # all null: disarmed
+    eng.atspeed_capture_hidden(x=x, plan=plan, max_rows=w.prefix_len)
+    eng.atspeed_prefill(torch.from_numpy(pre).cuda())
+    torch.cuda.synchronize()
+    p = plan.cpu().numpy()
+    assert p[3 * w.prefix_len] == w.prefix_len
+    assert (p[w.prefix_len:2 * w.prefix_len] == np.arange(w.prefix_len)).all()
+    assert (p[2 * w.prefix_len:3 * w.prefix_len] == -1).all()
+    xs = x.cpu().numpy().astype(np.float64)
+    eng.close()
+    dec = Decoder(m, tw, w.dtype)
+    P = w.prefix_len
+    assert np.abs(xs[0] - dec.embed(pre[0][None])[0]).max() == 0.0
+    for l in range(m.n_layers):
+        h, xo, _, _ = dec.block(l, xs[2 * l][None], np.arange(P))
+        assert np.abs(h[0] - xs[2 * l + 1]).max() <= FP32_BAR
+        if l + 1 < m.n_layers:
+            assert np.abs(xo[0] - xs[2 * l + 2]).max() <= FP32_BAR
