@@ -115,7 +115,12 @@ __device__ __forceinline__ void load_stage(unsigned char* stage, int wave, const
 // The same stage load as untracked inline-asm DMA, for the pipelines with more
 // than two stages: the compiler counts only a few LDS-DMA stores in flight and
 // would drain all of them once per round, so these loads are issued where it
-// does not see them and the pipeline waits with an explicit vmcnt.
+// does not see them and the pipeline waits with an explicit vmcnt.  The asm
+// writes M0 (the LDS address) itself.  M0 is a reserved register, so the
+// compiler ignores its clobber (and warns); that is safe because the kernels
+// that use these loads contain no M0 use of the compiler's own (the two-stage
+// kernels, whose builtin DMA sets M0, contain no such asm).  Binding the
+// address to M0 as an asm operand instead was tried and faulted the GPU.
 __device__ __forceinline__ const void* uniform_ptr(const void* p) {
   const uint64_t v = (uint64_t)(uintptr_t)p;
   const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v), hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));

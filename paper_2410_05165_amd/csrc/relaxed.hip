@@ -261,7 +261,7 @@ verify_relaxed_kernel(StateDev s, TreeDev tr, TrieDev trie, const float* lpt, co
   __shared__ float red[4];
   __shared__ uint32_t fin[kMaxSel];      // per-slot / per-draft outcome paths
   __shared__ int acc_flag[kMaxSel];
-  __shared__ int nacc_s, stop_s;
+  __shared__ int nacc_s;
   const int u = blockIdx.x, tid = threadIdx.x;
   const int t = s.t[u], K = s.K;
   if (t >= L) {
@@ -320,7 +320,7 @@ verify_relaxed_kernel(StateDev s, TreeDev tr, TrieDev trie, const float* lpt, co
         if (tid == 0) nout = m;
       }
     } else if (ra.mode == 1) {  // EXACT
-      if (tid == 0) { nacc_s = 0; stop_s = 0; }
+      if (tid == 0) nacc_s = 0;
       __syncthreads();
       for (int k = tid; k < K; k += blockDim.x) {
         const int node = ra.slot_node[((size_t)u * (L + 1) + lvl) * K + k];

@@ -485,7 +485,7 @@ atspeed_status upload_rope(atspeed_ctx& c, ModelRt& r) {
 atspeed_status forward(atspeed_ctx& c, ModelRt& r, bool prefill, int Mmax, int Tq, float* dbg, int shared = 0) {
   const atspeed_model_dims& m = r.dims;
   const int d = m.d_model, f = m.d_ffn, H = m.n_heads, dh = r.dh();
-  const int B = c.B, P = c.P;
+  const int B = c.B;
   const size_t es = esize(c);
   hipStream_t st = c.st;
   // the marks below know which model they bracket (target launches forward
@@ -619,9 +619,6 @@ atspeed_status read_err(atspeed_ctx& c, int* out) {
   HIP_TRY(hipStreamSynchronize(c.st));
   return ATSPEED_OK;
 }
-
-// Tree of the context or the caller: the same layout, the caller's arrays.
-TreeDev tree_view(atspeed_ctx& c) { return c.tree; }
 
 // carry: the decode loop's own verify, which may take the nodes the previous
 // verify of the loop forwarded (with tree-KV reuse configured).

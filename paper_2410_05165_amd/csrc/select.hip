@@ -414,7 +414,7 @@ verify_strict_kernel(StateDev s, TreeDev tr, TrieDev trie, const float* lpt, con
   __shared__ int ptrie[kMaxPar], pslot[kMaxPar];
   __shared__ const float* plp[kMaxPar];
   __shared__ unsigned long long sel[2 * kMaxSel];
-  __shared__ int ok_s, stop_s, npar_s;
+  __shared__ int ok_s;
   constexpr int kTreeLds = 1024;     // nodes whose (depth, path) are staged in LDS
   __shared__ uint32_t tpath_s[kTreeLds];
   __shared__ int depth_s[kTreeLds];
@@ -442,7 +442,6 @@ verify_strict_kernel(StateDev s, TreeDev tr, TrieDev trie, const float* lpt, con
   const bool staged = ntree <= kTreeLds;
   if (staged)
     for (int i = tid; i < ntree; i += blockDim.x) { tpath_s[i] = tr.tpath[tb + i]; depth_s[i] = tr.depth[tb + i]; }
-  if (tid == 0) stop_s = 0;
   __syncthreads();
   unsigned long long* keys = keys_all + (size_t)u * max_cand;
   int accepted = 0, t_after = t;
