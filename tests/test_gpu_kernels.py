@@ -245,6 +245,9 @@ def report(tag, stats_b, stats_f):
 # the first two users, whose rows lead the forward
 CASES = {
     "b7": dict(users=(0, 31), layers=None, stride=1, rows=None),
+    # the relaxed workload's t = 0 tree: 3N = 120 nodes per user, 3,840 rows
+    # (other tile shapes than at 1,920 rows)
+    "b7_relaxed": dict(users=(0, 31), layers=(0, 15, 31), stride=4, rows=None),
     "stress": dict(users=(0, 1), layers=(0, 15, 31), stride=8, rows=2048),
 }
 
