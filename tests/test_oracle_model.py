@@ -184,3 +184,91 @@ def test_tree_forward_equals_per_path_forward():
     bad, _ = dec.forward(toks, len(prefix) + np.arange(len(nodes)), prefix=cache,
                          mask=ancestor_mask(parent).astype(bool))
     assert np.abs(bad[0] - per).max() > 1e-6
+
+
+def test_rmsnorm_epsilon_closed_form():
+    # The norm's epsilon is 1e-6 (reading of the model details; LLaMA-7B's value).
+    # A row whose mean square is itself 1e-6 makes it visible: [1e-3, -1e-3]
+    # normalises to [1, -1] / sqrt(2) with epsilon 1e-6 (1/sqrt(11) with 1e-5).
+    w = _tiny_workload(target=ModelDims(1, 2, 1, 1, 2, 0))
+    W = {"tok_emb": np.array([[1e-3, -1e-3]], np.float64),
+         "l0.wq": np.zeros((2, 2)), "l0.wk": np.zeros((2, 2)), "l0.wv": np.zeros((2, 2)), "l0.wo": np.zeros((2, 2)),
+         "l0.w_gate": np.zeros((1, 2)), "l0.w_up": np.zeros((1, 2)), "l0.w_down": np.zeros((2, 1)),
+         "l0.attn_norm": np.ones(2), "l0.ffn_norm": np.ones(2), "final_norm": np.ones(2),
+         "lm_head_item": np.eye(2)}
+    dec = Decoder(w.target, W, "fp32")
+    logits, _ = dec.forward(np.array([[0]]), np.arange(1))
+    np.testing.assert_allclose(logits[0, 0], [1 / math.sqrt(2.0), -1 / math.sqrt(2.0)], rtol=0, atol=1e-12)
+
+
+def _bf16_block_d2(wv, wo, wg, wu, wd, wq=None):
+    dims = ModelDims(1, 2, 1, 1, 2, 0)
+    W = {"tok_emb": np.zeros((1, 2)), "l0.wq": np.zeros((2, 2)) if wq is None else wq, "l0.wk": np.eye(2),
+         "l0.wv": wv, "l0.wo": wo, "l0.w_gate": wg, "l0.w_up": wu, "l0.w_down": wd,
+         "l0.attn_norm": np.ones(2), "l0.ffn_norm": np.ones(2), "final_norm": np.ones(2),
+         "lm_head_item": np.eye(2)}
+    return Decoder(dims, W, "bf16")
+
+
+def test_bf16_rounding_of_the_attention_output():
+    # Precision contract: the attention output is rounded to bf16 before the o
+    # projection.  W_q = 0 makes token 1 average the values of tokens 0 and 1;
+    # W_v = W_o = I, FFN off.  Token 0's normed row [1, 1] (1/sqrt(1 + 1e-6) ->
+    # 1 in bf16) and token 1's [1, 1 + 2^-6] / 1.00778 -> [0.9921875, 1.0078125]
+    # average to [1 - 2^-8, 1 + 2^-8]; the second is a bf16 tie and rounds to 1,
+    # so h_1 = x_1 + [1 - 2^-8, 1] (unrounded: 1 + 2^-8 in the second slot).
+    dec = _bf16_block_d2(np.eye(2), np.eye(2), np.zeros((1, 2)), np.zeros((1, 2)), np.zeros((2, 1)))
+    x = np.array([[[1.0, 1.0], [1.0, 1.0 + 2.0 ** -6]]])
+    h, xo, k, v = dec.block(0, x, np.arange(2))
+    assert h[0, 1, 0] == 1.0 + (1.0 - 2.0 ** -8) and h[0, 1, 1] == (1.0 + 2.0 ** -6) + 1.0
+    assert (xo == h).all()                       # FFN off
+    # k and v are bf16 values
+    from oracle.numerics import round_bf16
+    assert (round_bf16(k) == k).all() and (round_bf16(v) == v).all()
+
+
+def test_bf16_rounding_of_the_swiglu_product():
+    # Precision contract: SiLU(gate) * up is rounded to bf16 before the down
+    # projection.  Attention off (W_v = 0), x = [1, 1] normalises to [1, 1] in
+    # bf16; gate = up = the first coordinate, so the product is
+    # SiLU(1) = 1 / (1 + e^-1) = 0.7310585786..., whose bf16 rounding is
+    # 187 / 256 = 0.73046875; W_down puts it on the first coordinate.
+    dec = _bf16_block_d2(np.zeros((2, 2)), np.eye(2), np.array([[1.0, 0.0]]), np.array([[1.0, 0.0]]),
+                         np.array([[1.0], [0.0]]))
+    x = np.array([[[1.0, 1.0]]])
+    h, xo, _, _ = dec.block(0, x, np.arange(1))
+    assert (h == x).all()
+    assert xo[0, 0, 0] == 1.0 + 187.0 / 256.0 and xo[0, 0, 1] == 1.0
+    assert abs(1.0 / (1.0 + math.exp(-1.0)) - 0.7310585786300049) < 1e-15
+
+
+def test_bf16_rounding_of_the_final_norm():
+    # The final norm's output is rounded to bf16 before the item head: with an
+    # identity head the logits are bf16 values ([1, 3] normalises to
+    # [0.4472..., 1.3416...] -> [229/512, 172/128]).
+    dec = _bf16_block_d2(np.zeros((2, 2)), np.eye(2), np.zeros((1, 2)), np.zeros((1, 2)), np.zeros((2, 1)))
+    lg = dec.head(np.array([[1.0, 3.0]]))
+    assert lg[0, 0] == 229.0 / 512.0 and lg[0, 1] == 172.0 / 128.0
+
+
+def test_bf16_rounding_of_the_normalised_inputs():
+    # Precision contract: the normed rows entering q/k/v and gate/up are rounded
+    # to bf16.  Both cases use x = [1, 1 + k/64], whose norm is x / sqrt((1 +
+    # x_1^2) / 2 + 1e-6).
+    # (1) Attention input: x = [1, 1.109375] normalises to [0.946876, 1.050440]
+    # -> bf16 [242/256, 134/128]; W_v = [[1, 1], [0, 0]] sums them to 255/128
+    # exactly (unrounded inputs: 1.997316, whose rounding is 2); one token
+    # attends to itself, W_o = I, FFN off: h = x + [255/128, 0].
+    dec = _bf16_block_d2(np.array([[1.0, 1.0], [0.0, 0.0]]), np.eye(2), np.zeros((1, 2)), np.zeros((1, 2)),
+                         np.zeros((2, 1)))
+    h, _, _, _ = dec.block(0, np.array([[[1.0, 1.109375]]]), np.arange(1))
+    assert h[0, 0, 0] == 1.0 + 255.0 / 128.0 and h[0, 0, 1] == 1.109375
+    # (2) FFN input: attention off, x = [1, 1.078125] normalises to [0.961726,
+    # 1.036861] -> bf16 [246/256, 133/128]; gate = 64 x_0 (SiLU of 61.5 is 61.5 to
+    # 1e-26), up = x_1 / 64, so SiLU(gate) * up = (246/256)(133/128) = 0.998474,
+    # whose bf16 rounding is 1 (unrounded inputs: 0.997176, whose rounding is
+    # 255/256); W_down puts it on the first coordinate.
+    dec = _bf16_block_d2(np.zeros((2, 2)), np.eye(2), np.array([[64.0, 0.0]]), np.array([[0.0, 1.0 / 64.0]]),
+                         np.array([[1.0], [0.0]]))
+    h, xo, _, _ = dec.block(0, np.array([[[1.0, 1.078125]]]), np.arange(1))
+    assert xo[0, 0, 0] == 1.0 + 1.0 and xo[0, 0, 1] == 1.078125
