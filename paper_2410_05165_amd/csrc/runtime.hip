@@ -1054,13 +1054,8 @@ atspeed_status atspeed_set_state(atspeed_ctx* c, int32_t B, const int32_t* t, co
 
 // The users' final beams as lists: items [B, K, L] codes, scores [B, K], counts [B] (device).
 static atspeed_status write_lists(atspeed_ctx* c, int32_t B, int32_t* items, float* scores, int32_t* n_items) {
-  const int K = c->cfg.K, L = c->cfg.L;
-  std::vector<int> t(B), nb(B), paths((size_t)B * K * L);
-  std::vector<float> sc((size_t)B * K);
-  ST_TRY(atspeed_get_state(c, B, t.data(), nb.data(), paths.data(), sc.data()));
-  HIP_TRY(hipMemcpyAsync(items, paths.data(), paths.size() * 4, hipMemcpyHostToDevice, c->st));
-  HIP_TRY(hipMemcpyAsync(scores, sc.data(), sc.size() * 4, hipMemcpyHostToDevice, c->st));
-  HIP_TRY(hipMemcpyAsync(n_items, nb.data(), B * 4, hipMemcpyHostToDevice, c->st));
+  launch_write_lists(c->state, B, c->cfg.K, c->cfg.L, items, scores, n_items, c->st);
+  HIP_TRY(hipGetLastError());
   HIP_TRY(hipStreamSynchronize(c->st));
   return ATSPEED_OK;
 }

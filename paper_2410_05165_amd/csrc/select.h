@@ -99,6 +99,9 @@ void launch_carry_copy(const int* src, const int* nfwd, int B, int Tm, int n_lay
 // (launch_broadcast_prefix_kv, once per layer after the K/V projection).
 void launch_common_prefix(const int* prefix, int B, int P, int* out, hipStream_t st);
 void launch_plan_prefix(const int* prefix, int B, int P, int S, const Rows& rows, hipStream_t st);
+// Outputs of a decode from the state: items [B, K, L], scores [B, K], n_items [B] (device).
+void launch_write_lists(const StateDev& s, int B, int K, int L, int32_t* items, float* scores, int32_t* n_items,
+                        hipStream_t st);
 void launch_broadcast_prefix_kv(void* pk, void* pv, int B, int H, size_t head_bytes, size_t shared_bytes,
                                 hipStream_t st);
 void launch_draft_beam_scores(const StateDev& s, const TreeDev& tr, const float* lpq, const float* rootq, int nitem,

@@ -555,6 +555,25 @@ void launch_plan_prefix(const int* prefix, int B, int P, int S, const Rows& rows
   int blocks = std::max(1, std::min(1024, (total + 255) / 256));
   hipLaunchKernelGGL(plan_prefix_rows_kernel, dim3(blocks), dim3(256), 0, st, prefix, B, P, S, rows);
 }
+// The beams of every user as the decode's outputs: codes [B, K, L] unpacked
+// from the path keys (code of level l in byte 3 - l), scores [B, K], beam counts [B].
+__global__ void write_lists_kernel(StateDev s, int B, int K, int L, int32_t* __restrict__ items,
+                                   float* __restrict__ scores, int32_t* __restrict__ n_items) {
+  const int total = B * K;
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+    const uint32_t key = s.path[i];
+    for (int l = 0; l < L; ++l) items[(size_t)i * L + l] = (int32_t)((key >> (8 * (3 - l))) & 0xFFu);
+    scores[i] = s.score[i];
+    if (i % K == 0) n_items[i / K] = s.nb[i / K];
+  }
+}
+
+void launch_write_lists(const StateDev& s, int B, int K, int L, int32_t* items, float* scores, int32_t* n_items,
+                        hipStream_t st) {
+  const int blocks = std::max(1, std::min(1024, (B * K + 255) / 256));
+  hipLaunchKernelGGL(write_lists_kernel, dim3(blocks), dim3(256), 0, st, s, B, K, L, items, scores, n_items);
+}
+
 void launch_broadcast_prefix_kv(void* pk, void* pv, int B, int H, size_t head_bytes, size_t shared_bytes,
                                 hipStream_t st) {
   const size_t total = (size_t)(B - 1) * H * (shared_bytes / 16) * 2;
