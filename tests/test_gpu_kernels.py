@@ -1,7 +1,8 @@
 """Kernel-by-kernel parity at the full 7B shape (32 layers, d 4096, 32 heads,
 FFN 11008, 32 users, 144-token prefixes with the shared 64-token prompt, the
-t = 0 draft tree of 1,920 rows) and at the stress shape (128 users with
-1,024-token prefixes, 38,400 tree rows): every step of the decoder blocks of
+t = 0 draft tree of 1,920 rows), at the relaxed workload's tree (3,840 rows),
+at the stress shape (128 users with 1,024-token prefixes, 38,400 tree rows)
+and at the small workload (d 1024): every step of the decoder blocks of
 the GPU's prefill and tree forward (the LLaMA block of the implementation
 details, Sec. 4.1, with tree-based attention, Sec. 3.3), recomputed by the
 oracle's step function from the GPU's own inputs to that step, for a user who
@@ -249,6 +250,8 @@ CASES = {
     # (other tile shapes than at 1,920 rows)
     "b7_relaxed": dict(users=(0, 31), layers=(0, 15, 31), stride=4, rows=None),
     "stress": dict(users=(0, 1), layers=(0, 15, 31), stride=8, rows=2048),
+    # d 1024, 16 heads, FFN 2816, 16 users with their own 120-token prefixes
+    "small": dict(users=(0, 15), layers=None, stride=1, rows=None),
 }
 
 
