@@ -468,12 +468,10 @@ static hipError_t launch_attn(const AttnCall& a, hipStream_t st) {
   constexpr int DP = DH + 1;
   const size_t smem = sizeof(float) * (AQ * DP + AK * DP + AK * DH + AQ * (AK + 1));
   auto kern = attn_kernel<T, DH>;
-  static bool attr = false;
-  if (!attr) {
-    hipError_t err = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-    if (err != hipSuccess) return err;
-    attr = true;
-  }
+  // set on every launch: the attribute is per device, and this path (fp32
+  // workloads) is not the one whose launch cost matters
+  hipError_t err = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+  if (err != hipSuccess) return err;
   const float qscale = 1.4426950408889634f / sqrtf((float)DH);  // log2(e) / sqrt(d_head)
   dim3 grid(a.H, a.B, (a.Tq + AQ - 1) / AQ);  // query blocks slowest, as in the MFMA kernel
   hipLaunchKernelGGL(kern, grid, dim3(256), smem, st, (const T*)a.q, (const T*)a.pk, (const T*)a.pv,
