@@ -132,6 +132,41 @@ __device__ inline float block_lse(const float* v, int n, float tau, float* red) 
   return m + logf(s);
 }
 
+// Position of each wanted path among the level's candidates (the first match,
+// -1 if none), by the whole block: each thread compares its share of the
+// candidates with every wanted path (want and idx in LDS).  Replaces a serial
+// scan per wanted path over thousands of candidates in global memory.
+__device__ inline void find_candidates(const uint32_t* want, int nwant, const uint32_t* cpath, int n, int* idx) {
+  for (int i = threadIdx.x; i < nwant; i += blockDim.x) idx[i] = INT_MAX;
+  __syncthreads();
+  for (int c = threadIdx.x; c < n; c += blockDim.x) {
+    const uint32_t p = cpath[c];
+    for (int i = 0; i < nwant; ++i)
+      if (want[i] == p) atomicMin(&idx[i], c);
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < nwant; i += blockDim.x)
+    if (idx[i] == INT_MAX) idx[i] = -1;
+  __syncthreads();
+}
+
+// The same for the tree nodes of depth lvl (first matching node, -1 if none).
+__device__ inline void find_nodes(const uint32_t* want, int nwant, const uint32_t* tpath, const int* depth, int lvl,
+                                  int ntree, int* idx) {
+  for (int i = threadIdx.x; i < nwant; i += blockDim.x) idx[i] = INT_MAX;
+  __syncthreads();
+  for (int t = threadIdx.x; t < ntree; t += blockDim.x) {
+    if (depth[t] != lvl) continue;
+    const uint32_t p = tpath[t];
+    for (int i = 0; i < nwant; ++i)
+      if (want[i] == p) atomicMin(&idx[i], t);
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < nwant; i += blockDim.x)
+    if (idx[i] == INT_MAX) idx[i] = -1;
+  __syncthreads();
+}
+
 // ---------------------------------------------------------------- drafting
 // One drafted level (relaxed modes): EXACT draws K slots, PAPER N distinct.
 // New nodes are appended to the tree; lvl_lo/lvl_hi bound them; zq records the
@@ -262,6 +297,9 @@ verify_relaxed_kernel(StateDev s, TreeDev tr, TrieDev trie, const float* lpt, co
   __shared__ uint32_t fin[kMaxSel];      // per-slot / per-draft outcome paths
   __shared__ int acc_flag[kMaxSel];
   __shared__ int nacc_s;
+  __shared__ uint32_t want[kMaxSel];     // paths looked up among the candidates / tree nodes
+  __shared__ int cand_of[kMaxSel], node_of[kMaxSel];
+  __shared__ int run_s[2];               // first node of a depth and the end of its run
   const int u = blockIdx.x, tid = threadIdx.x;
   const int t = s.t[u], K = s.K;
   if (t >= L) {
@@ -322,11 +360,13 @@ verify_relaxed_kernel(StateDev s, TreeDev tr, TrieDev trie, const float* lpt, co
     } else if (ra.mode == 1) {  // EXACT
       if (tid == 0) nacc_s = 0;
       __syncthreads();
+      for (int k = tid; k < K; k += blockDim.x)
+        want[k] = tr.tpath[tb + ra.slot_node[((size_t)u * (L + 1) + lvl) * K + k]];
+      __syncthreads();
+      find_candidates(want, K, cb.path, n, cand_of);
       for (int k = tid; k < K; k += blockDim.x) {
-        const int node = ra.slot_node[((size_t)u * (L + 1) + lvl) * K + k];
-        const uint32_t y = tr.tpath[tb + node];
-        int ci = -1;
-        for (int c = 0; c < n; ++c) if (cb.path[c] == y) { ci = c; break; }
+        const uint32_t y = want[k];
+        const int ci = cand_of[k];
         float a = -INFINITY;
         if (ci >= 0) a = (cb.sp[ci] / ra.tau - zp) - (cb.sq[ci] / ra.tau - zq);
         const bool acc = logf(philox_u(ra, u, step, lvl, k, 0, 1)) <= a;
@@ -356,14 +396,24 @@ verify_relaxed_kernel(StateDev s, TreeDev tr, TrieDev trie, const float* lpt, co
     } else {  // PAPER: drafted nodes of this level, in draw order
       if (tid == 0) { nacc_s = 0; }
       __syncthreads();
-      int d0 = ntree, d1 = ntree;
-      for (int i = 0; i < ntree; ++i) if (tr.depth[tb + i] == lvl) { d0 = i; break; }
-      for (int i = d0; i < ntree && tr.depth[tb + i] == lvl; ++i) d1 = i + 1;
+      // the drafted nodes of this level: the run of depth lvl that starts at its
+      // first node (the tree is level-ordered)
+      if (tid == 0) { run_s[0] = ntree; run_s[1] = ntree; }
+      __syncthreads();
+      for (int i = tid; i < ntree; i += blockDim.x)
+        if (tr.depth[tb + i] == lvl) atomicMin(&run_s[0], i);
+      __syncthreads();
+      const int d0 = run_s[0];
+      for (int i = d0 + tid; i < ntree; i += blockDim.x)
+        if (tr.depth[tb + i] != lvl) atomicMin(&run_s[1], i);
+      __syncthreads();
+      const int d1 = run_s[1];
       const int nd = min(d1 - d0, kMaxSel);
+      for (int i = tid; i < nd; i += blockDim.x) want[i] = tr.tpath[tb + d0 + i];
+      __syncthreads();
+      find_candidates(want, nd, cb.path, n, cand_of);
       for (int i = tid; i < nd; i += blockDim.x) {
-        const uint32_t y = tr.tpath[tb + d0 + i];
-        int ci = -1;
-        for (int c = 0; c < n; ++c) if (cb.path[c] == y) { ci = c; break; }
+        const int ci = cand_of[i];
         float a = -INFINITY;
         if (ci >= 0) a = (cb.sp[ci] / ra.tau - zp) - (tr.q_score[tb + d0 + i] / ra.tau - zq);
         const bool acc = logf(philox_u(ra, u, step, lvl, i, 0, 1)) <= a;
@@ -391,16 +441,11 @@ verify_relaxed_kernel(StateDev s, TreeDev tr, TrieDev trie, const float* lpt, co
           const float r = zero ? 0.f : expf(cb.sp[c] / ra.tau - zp) - expf(qz);
           keys[c] = r > 0.f ? make_key(logf(r) + philox_g(ra, u, step, lvl, 0, cb.cidx[c], 3), cb.path[c]) : ~0ull;
         }
-        __syncthreads();
-        if (tid == 0) {  // number of positive residuals
-          int npos = 0;
-          for (int c = 0; c < n; ++c) npos += keys[c] != ~0ull;
-          sh.count = npos;
-        }
-        __syncthreads();
-        // every wave takes the count into a register before select_smallest's
-        // thread 0 reuses sh.count as its output counter
-        const int npos = sh.count;
+        // number of positive residuals (each thread counts the keys it wrote;
+        // held in a register, so select_smallest may reuse sh.count)
+        float cnt = 0.f;
+        for (int c = tid; c < n; c += blockDim.x) cnt += keys[c] != ~0ull ? 1.f : 0.f;
+        const int npos = (int)bsum(cnt, red);
         __syncthreads();
         const int extra = select_smallest(keys, n, min(K - m, npos), sel, sh);
         for (int i = tid; i < extra; i += blockDim.x) fin[m + i] = (uint32_t)sel[i];
@@ -424,16 +469,18 @@ verify_relaxed_kernel(StateDev s, TreeDev tr, TrieDev trie, const float* lpt, co
     }
     __syncthreads();
     const int m = sh.count;
+    for (int i = tid; i < m; i += blockDim.x) want[i] = (uint32_t)sel[i];
+    __syncthreads();
+    find_candidates(want, m, cb.path, n, cand_of);
+    find_nodes(want, m, tr.tpath + tb, tr.depth + tb, lvl, ntree, node_of);
     uint32_t mp = 0; float msp = 0.f, msq = 0.f; int mtrie = -1, mslot = -1;
     if (tid < m) {
-      mp = (uint32_t)sel[tid];
-      int ci = 0;
-      for (int c = 0; c < n; ++c) if (cb.path[c] == mp) { ci = c; break; }
+      mp = want[tid];
+      const int ci = cand_of[tid] >= 0 ? cand_of[tid] : 0;  // every outcome is a candidate
       const int pi = cb.par[ci];
       msp = cb.sp[ci];
       mtrie = trie_child(trie, P.trie[pi], path_code(mp, lvl0));
-      for (int i = 0; i < ntree; ++i)
-        if (tr.depth[tb + i] == lvl && tr.tpath[tb + i] == mp) { mslot = i; break; }
+      mslot = node_of[tid];
       msq = mslot >= 0 ? tr.q_score[tb + mslot] : cb.sq[ci];
     }
     __syncthreads();

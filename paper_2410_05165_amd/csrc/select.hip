@@ -18,7 +18,13 @@ namespace atspeed {
 
 // Paths of the current beams Y_t (depths 1..t), deduplicated and level-ordered,
 // become the first nodes of each user's tree; beam_slot[k] is beam k's node.
+// The nodes are looked up while the tree is built, so their depth, path key
+// and trie node are mirrored in LDS (a lookup then costs no round trip to
+// memory): at most K <= 128 beams times t < L <= 4 levels of nodes.
+constexpr int kMaxPathNodes = kMaxSel * 3;
 __global__ void tree_from_beams_kernel(StateDev s, TreeDev tr, TrieDev trie, int item_base, int codebook, int L) {
+  __shared__ int dep_s[kMaxPathNodes], trie_s[kMaxPathNodes];
+  __shared__ uint32_t path_s[kMaxPathNodes];
   const int u = blockIdx.x;
   if (threadIdx.x != 0) return;
   const int t = s.t[u];
@@ -33,22 +39,26 @@ __global__ void tree_from_beams_kernel(StateDev s, TreeDev tr, TrieDev trie, int
         const uint32_t pre = s.path[u * K + k] & mask;
         int found = -1;
         for (int i = 0; i < n; ++i)
-          if (tr.depth[tb + i] == l && tr.tpath[tb + i] == pre) { found = i; break; }
+          if (dep_s[i] == l && path_s[i] == pre) { found = i; break; }
         if (found < 0) {
           int parent = -1, ptrie = 0;
           if (l > 1) {
             const uint32_t pm = ~(0xFFFFFFFFu >> (8 * (l - 1)));
             for (int i = 0; i < n; ++i)
-              if (tr.depth[tb + i] == l - 1 && tr.tpath[tb + i] == (pre & pm)) { parent = i; break; }
-            ptrie = tr.ttrie[tb + parent];
+              if (dep_s[i] == l - 1 && path_s[i] == (pre & pm)) { parent = i; break; }
+            ptrie = parent >= 0 ? trie_s[parent] : 0;  // found: the prefix was added at level l - 1
           }
           const int code = path_code(pre, l - 1);
+          const int node = trie_child(trie, ptrie, code);
           tr.token[tb + n] = item_base + codebook * (l - 1) + code;
           tr.parent[tb + n] = parent;
           tr.depth[tb + n] = l;
           tr.q_score[tb + n] = 0.f;
           tr.tpath[tb + n] = pre;
-          tr.ttrie[tb + n] = trie_child(trie, ptrie, code);
+          tr.ttrie[tb + n] = node;
+          dep_s[n] = l;
+          path_s[n] = pre;
+          trie_s[n] = node;
           found = n++;
         }
         if (l == t) s.beam_slot[u * K + k] = found;
