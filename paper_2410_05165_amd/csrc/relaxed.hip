@@ -134,8 +134,8 @@ __device__ inline float block_lse(const float* v, int n, float tau, float* red) 
 
 // Position of each wanted path among the level's candidates (the first match,
 // -1 if none), by the whole block: each thread compares its share of the
-// candidates with every wanted path (want and idx in LDS).  Replaces a serial
-// scan per wanted path over thousands of candidates in global memory.
+// candidates with every wanted path (want and idx in LDS), where one thread per
+// wanted path would walk thousands of candidates in global memory.
 __device__ inline void find_candidates(const uint32_t* want, int nwant, const uint32_t* cpath, int n, int* idx) {
   for (int i = threadIdx.x; i < nwant; i += blockDim.x) idx[i] = INT_MAX;
   __syncthreads();
